@@ -1,0 +1,229 @@
+"""CPU oracle of the SemShareKV hot path -- TEST INFRASTRUCTURE ONLY.
+
+Python face of ``oracle.c`` (plain C, fp64, optional OpenMP over rows).  Only
+the test suite, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
+leg may import this package.  The product library never calls it and shares
+no code with it.
+
+Every function takes numpy arrays holding exact storage-dtype values (float32
+arrays are fine: they are widened to fp64 without change) and returns fp64
+arrays whose values are rounded to ``dtype`` where the product path stores
+them ("bf16", "fp32", or "f64" for no rounding).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_DT = {"fp32": 0, "bf16": 1, "f64": 2}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def build(verbose: bool = False) -> str:
+    """Compile oracle.c into liboracle.so next to it (gcc, IEEE fp64, no FMA
+    contraction, OpenMP)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-Wextra", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    I64, I32, F64, INT = ctypes.c_int64, ctypes.c_int32, ctypes.c_double, ctypes.c_int
+    sig = {
+        "orc_round_array": (None, [P, P, I64, INT]),
+        "orc_rope_embed": (None, [P, P, I64, I32, I64, F64, INT]),
+        "orc_lsh_project": (None, [P, P, P, I64, I32, I32]),
+        "orc_lsh_encode": (None, [P, P, P, I64, I32, I32]),
+        "orc_match": (None, [P, I64, P, I64, I32, P, P]),
+        "orc_gather_rows": (None, [P, P, I64, I64, P, I32, I64]),
+        "orc_qkv_rows": (None, [P, P, I64, P, P, P, I32, I32, I32, I32, F64, P, P, P, INT]),
+        "orc_deviation": (None, [P, P, P, I64, P, P, I32, P]),
+        "orc_attention_rows": (None, [P, P, I64, P, I64, P, P, I32, I32, I32, F64, P, INT]),
+        "orc_partial_prefill": (None, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, F64,
+                                       P, P, INT]),
+        "orc_select_recompute": (None, [P, I64, I64, P]),
+        "orc_similarity": (F64, [P, I64, F64, F64]),
+        "orc_num_threads": (INT, []),
+        "orc_set_num_threads": (None, [INT]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def num_threads() -> int:
+    return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    _load().orc_set_num_threads(int(n))
+
+
+def round_to(x, dtype: str) -> np.ndarray:
+    x = _f64(x)
+    y = np.empty_like(x)
+    _load().orc_round_array(_ptr(x), _ptr(y), x.size, _DT[dtype])
+    return y
+
+
+def rope_embed(x, pos0: int = 0, base: float = 10000.0, dtype: str = "f64") -> np.ndarray:
+    """RoPE of every row of x [n_tok, d]; row r sits at position pos0 + r."""
+    x = _f64(x)
+    n, d = x.shape
+    if d % 2:
+        raise ValueError("dim must be even")
+    y = np.empty_like(x)
+    _load().orc_rope_embed(_ptr(x), _ptr(y), n, d, int(pos0), float(base), _DT[dtype])
+    return y
+
+
+def lsh_project(x, planes) -> np.ndarray:
+    x, planes = _f64(x), _f64(planes)
+    n, d = x.shape
+    nb = planes.shape[0]
+    p = np.empty((n, nb), dtype=np.float64)
+    _load().orc_lsh_project(_ptr(x), _ptr(planes), _ptr(p), n, d, nb)
+    return p
+
+
+def lsh_encode(x, planes) -> np.ndarray:
+    """Sign-bit codes [n_tok, n_bits/64] uint64."""
+    x, planes = _f64(x), _f64(planes)
+    n, d = x.shape
+    nb = planes.shape[0]
+    if nb % 64:
+        raise ValueError("n_bits must be a multiple of 64")
+    c = np.empty((n, nb // 64), dtype=np.uint64)
+    _load().orc_lsh_encode(_ptr(x), _ptr(planes), _ptr(c), n, d, nb)
+    return c
+
+
+def match(tgt_codes, ref_codes) -> Tuple[np.ndarray, np.ndarray]:
+    """Top-1 Hamming match: (idx int32 [n_tgt], dist int32 [n_tgt])."""
+    t = np.ascontiguousarray(tgt_codes, dtype=np.uint64)
+    r = np.ascontiguousarray(ref_codes, dtype=np.uint64)
+    if t.ndim != 2 or r.ndim != 2 or t.shape[1] != r.shape[1]:
+        raise ValueError("codes must be [n, n_words] with equal n_words")
+    idx = np.empty(t.shape[0], dtype=np.int32)
+    dist = np.empty(t.shape[0], dtype=np.int32)
+    _load().orc_match(_ptr(t), t.shape[0], _ptr(r), r.shape[0], t.shape[1], _ptr(idx), _ptr(dist))
+    return idx, dist
+
+
+def gather_rows(src: np.ndarray, idx) -> np.ndarray:
+    """src [L, n_ref, ...] -> [L, n_tgt, ...] with row t = src[:, idx[t]] (bytewise)."""
+    src = np.ascontiguousarray(src)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    L, n_ref = src.shape[:2]
+    row_bytes = src[0, 0].nbytes if n_ref else 0
+    if idx.size and (idx.min() < 0 or idx.max() >= n_ref):
+        raise ValueError("index out of range")
+    dst = np.empty((L, idx.size) + src.shape[2:], dtype=src.dtype)
+    _load().orc_gather_rows(_ptr(src), _ptr(idx), idx.size, n_ref, _ptr(dst), L, row_bytes)
+    return dst
+
+
+def qkv_rows(x_sel, sel_pos, wq, wk, wv, n_q_heads: int, n_kv_heads: int, head_dim: int,
+             base: float = 10000.0, dtype: str = "f64"):
+    x = _f64(x_sel)
+    pos = np.ascontiguousarray(sel_pos, dtype=np.int32)
+    wq, wk, wv = _f64(wq), _f64(wk), _f64(wv)
+    n, hidden = x.shape
+    q = np.empty((n, n_q_heads * head_dim))
+    k = np.empty((n, n_kv_heads * head_dim))
+    v = np.empty((n, n_kv_heads * head_dim))
+    _load().orc_qkv_rows(_ptr(x), _ptr(pos), n, _ptr(wq), _ptr(wk), _ptr(wv), hidden, n_q_heads,
+                         n_kv_heads, head_dim, float(base), _ptr(q), _ptr(k), _ptr(v), _DT[dtype])
+    return q, k, v
+
+
+def deviation(k_cache, v_cache, sel_pos, k_new, v_new) -> np.ndarray:
+    kc, vc = _f64(k_cache), _f64(v_cache)
+    kn, vn = _f64(k_new), _f64(v_new)
+    pos = np.ascontiguousarray(sel_pos, dtype=np.int32)
+    row = kn.shape[1]
+    sig = np.empty(pos.size)
+    _load().orc_deviation(_ptr(kc), _ptr(vc), _ptr(pos), pos.size, _ptr(kn), _ptr(vn), row, _ptr(sig))
+    return sig
+
+
+def attention_rows(q, sel_pos, k_cache, v_cache, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                   scale: float = 0.0, dtype: str = "f64", rows=None) -> np.ndarray:
+    """Causal attention of selected rows over a cache [n_tok, Hkv*D].
+    Returns [n_sel, Hq*D]; with ``rows`` only those rows are computed (others NaN)."""
+    q = _f64(q)
+    pos = np.ascontiguousarray(sel_pos, dtype=np.int32)
+    kc = _f64(k_cache).reshape(-1, n_kv_heads * head_dim)
+    vc = _f64(v_cache).reshape(-1, n_kv_heads * head_dim)
+    if scale <= 0:
+        scale = 1.0 / np.sqrt(head_dim)
+    out = np.full((pos.size, n_q_heads * head_dim), np.nan)
+    r = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    _load().orc_attention_rows(_ptr(q), _ptr(pos), pos.size, _ptr(r), 0 if r is None else r.size,
+                               _ptr(kc), _ptr(vc), n_q_heads, n_kv_heads, head_dim, float(scale),
+                               _ptr(out), _DT[dtype])
+    return out
+
+
+def partial_prefill(x_sel, sel_pos, wq, wk, wv, k_cache, v_cache, n_q_heads: int, n_kv_heads: int,
+                    head_dim: int, base: float = 10000.0, scale: float = 0.0, dtype: str = "f64",
+                    want_out: bool = True, want_sigma: bool = False):
+    """One layer of partial prefill.  k_cache/v_cache [n_tok, Hkv*D] (or
+    [n_tok, Hkv, D]) are not modified; the updated caches are returned.
+    Returns (out [n_sel, Hq*D] or None, sigma [n_sel] or None, k_cache', v_cache')."""
+    x = _f64(x_sel)
+    pos = np.ascontiguousarray(sel_pos, dtype=np.int32)
+    wq, wk, wv = _f64(wq), _f64(wk), _f64(wv)
+    kc = _f64(k_cache).reshape(-1, n_kv_heads * head_dim).copy()
+    vc = _f64(v_cache).reshape(-1, n_kv_heads * head_dim).copy()
+    n, hidden = x.shape
+    out = np.empty((n, n_q_heads * head_dim)) if want_out else None
+    sig = np.empty(n) if want_sigma else None
+    _load().orc_partial_prefill(_ptr(x), _ptr(pos), n, _ptr(wq), _ptr(wk), _ptr(wv), _ptr(kc),
+                                _ptr(vc), kc.shape[0], hidden, n_q_heads, n_kv_heads, head_dim,
+                                float(base), float(scale), _ptr(out), _ptr(sig), _DT[dtype])
+    return out, sig, kc, vc
+
+
+def select_recompute(sigma, n_sel: int) -> np.ndarray:
+    s = _f64(sigma)
+    if not 0 <= n_sel <= s.size:
+        raise ValueError("n_sel out of range")
+    pos = np.empty(n_sel, dtype=np.int32)
+    _load().orc_select_recompute(_ptr(s), s.size, n_sel, _ptr(pos))
+    return pos
+
+
+def similarity(dist, dmin: float = 0.0, dmax: float = 30.0) -> float:
+    d = np.ascontiguousarray(dist, dtype=np.int32)
+    return float(_load().orc_similarity(_ptr(d), d.size, float(dmin), float(dmax)))
