@@ -1,0 +1,177 @@
+/*
+ * semshare.h -- C ABI of libsemshare.so, the MI355X (gfx950) hot path of
+ * SemShareKV: fuzzy token matching and KV reuse for one target prompt
+ * against a cached reference prompt (Zhao & Mastorakis, "SemShareKV:
+ * Efficient KVCache Sharing for Semantically Similar Prompts via Token-Level
+ * LSH Matching", arXiv 2509.24832).
+ *
+ * Common contract of every call
+ *  - Buffer pointers are DEVICE pointers owned by the caller.  The library
+ *    never allocates, frees or keeps them after the call returns.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *    asynchronously on it; no call synchronizes the device.
+ *  - Arguments are validated on the host before anything is enqueued.  On a
+ *    bad argument the call returns SEMSHARE_E_INVAL (or
+ *    SEMSHARE_E_UNSUPPORTED for a valid shape this build has no kernel for)
+ *    and enqueues nothing.  SEMSHARE_E_DEVICE reports a HIP launch error.
+ *    semshare_last_error() then returns a message (thread-local).
+ *  - Layouts are row-major and dense.  "dtype" is the storage type of the
+ *    floating-point buffers of the call; arithmetic accumulates in fp32.
+ *  - Buffers are aligned to their element size; the LSH, gather and
+ *    partial-prefill calls also need 16-byte aligned buffers (as any
+ *    allocator returns) and reject others with SEMSHARE_E_INVAL.
+ *  - A call with an empty problem (zero tokens) succeeds and enqueues
+ *    nothing.
+ */
+#ifndef SEMSHARE_H
+#define SEMSHARE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t semshare_status_t;
+enum {
+    SEMSHARE_OK = 0,
+    SEMSHARE_E_INVAL = -1,
+    SEMSHARE_E_UNSUPPORTED = -2,
+    SEMSHARE_E_DEVICE = -3
+};
+
+typedef int32_t semshare_dtype_t;
+enum { SEMSHARE_FP32 = 0, SEMSHARE_BF16 = 1 };
+
+/* Message describing the last failed call on this thread ("" if none). */
+const char* semshare_last_error(void);
+
+/* ABI version: major * 10000 + minor * 100 + patch. */
+int32_t semshare_version(void);
+
+/*
+ * RoPE injected into token embeddings (Section 4.3.1; Appendix A.1 Eq. 1,
+ * read as the standard rotary embedding): the row at position m has every
+ * pair (x[2k], x[2k+1]) rotated by the angle m * theta_k with
+ * theta_k = base^(-2k/dim), k = 0 .. dim/2-1.  Row r of x sits at position
+ * pos0 + r.  Angles are formed in fp64, reduced modulo 2*pi, then rotated in
+ * fp32 and rounded to `dtype`.
+ *   x, y   [n_tok][dim] dtype.  y may equal x (in place); no other overlap.
+ *   dim    even, > 0.   base > 0.   pos0 >= 0.
+ */
+semshare_status_t semshare_rope_embed(const void* x, void* y, int64_t n_tok, int32_t dim,
+                                      int64_t pos0, double base, semshare_dtype_t dtype,
+                                      void* stream);
+
+/*
+ * Random-hyperplane LSH of embeddings (Section 4.3 and Appendix A.2; the
+ * sign-bit family of the FAISS LSH index the implementation uses, Appendix D):
+ * bit j of row t is 1 iff <x_t, planes_j> > 0, computed with fp32
+ * accumulation of exact bf16/fp32 products.  Bit j is stored at bit (j % 64)
+ * of word j / 64.
+ *   x       [n_tok][dim] dtype
+ *   planes  [n_bits][dim] dtype (row j = hyperplane j)
+ *   codes   [n_tok][n_bits / 64] uint64 (output)
+ *   n_bits  64, 128 or 256.   dim: multiple of 64 (bf16) or of 4 (fp32).
+ */
+semshare_status_t semshare_lsh_encode(const void* x, const void* planes, uint64_t* codes,
+                                      int64_t n_tok, int32_t dim, int32_t n_bits,
+                                      semshare_dtype_t dtype, void* stream);
+
+/*
+ * Fuzzy token matching (Sections 4.2 and 4.3): for every target token, the
+ * reference token whose LSH code is nearest in Hamming distance; on equal
+ * distance the lowest reference index wins, so the answer is unique.  A
+ * bank of several reference prompts is their concatenation along the token
+ * axis (index b * n_per_ref + j).
+ *   tgt_codes  [n_tgt][n_words] uint64;   ref_codes [n_ref][n_words] uint64
+ *   n_words    1 .. 4.   n_ref in [1, 2^23).
+ *   idx        [n_tgt] int32 (output): matched reference index.
+ *   dist       [n_tgt] int32 (output, may be NULL): its Hamming distance.
+ */
+semshare_status_t semshare_match(const uint64_t* tgt_codes, int64_t n_tgt,
+                                 const uint64_t* ref_codes, int64_t n_ref, int32_t n_words,
+                                 int32_t* idx, int32_t* dist, void* stream);
+
+/*
+ * KV rearrangement (Section 4.3; Section 4.3.2 for keeping K post-RoPE):
+ * out[l][t] = ref[l][idx[t]] for every layer l, where a row is all kv heads
+ * of one token (n_kv_heads * head_dim elements), copied bit for bit.  Keys
+ * are not re-rotated to the target positions.
+ *   ref_k, ref_v  [n_layers][n_ref][n_kv_heads][head_dim] dtype
+ *   out_k, out_v  [n_layers][n_tgt][n_kv_heads][head_dim] dtype
+ *   idx           [n_tgt] int32.  A row whose index lies outside [0, n_ref)
+ *                 is written as zeros instead of being read.
+ *   ref_v and out_v may both be NULL (gathers K only), which also serves as
+ *   a plain row gather.  Row size n_kv_heads * head_dim * sizeof(dtype)
+ *   must be a multiple of 16 bytes.
+ */
+semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const int32_t* idx,
+                                     int64_t n_tgt, int64_t n_ref, void* out_k, void* out_v,
+                                     int32_t n_layers, int32_t n_kv_heads, int32_t head_dim,
+                                     semshare_dtype_t dtype, void* stream);
+
+/*
+ * One attention layer of partial prefill (Sections 4.2 and 4.3.3): only the
+ * selected tokens are recomputed, against the assembled (rearranged) cache.
+ *  1. q = RoPE_p(x Wq^T), k = RoPE_p(x Wk^T) per head and v = x Wv^T for
+ *     every selected row (position p = sel_pos[i]); RoPE is the standard
+ *     rotation of interleaved pairs within each head (theta_k =
+ *     rope_base^(-2k/head_dim)).
+ *  2. If deviation_out != NULL: deviation_out[i] = ||K_cache[p] - k||_2 +
+ *     ||V_cache[p] - v||_2 over the row's n_kv_heads*head_dim entries, against
+ *     the row held before step 3 (KV deviation, Appendix A.4), with k and v
+ *     as rounded to dtype.
+ *  3. Cache rows sel_pos[i] are overwritten with k (post-RoPE) and v.
+ *  4. If out != NULL: for every selected row and query head h,
+ *     out = softmax_{j <= p}(q_h . K[j][h/G] * sm_scale) V[j][h/G] over the
+ *     updated cache, G = n_q_heads / n_kv_heads (grouped-query attention).
+ *     out == NULL builds cache rows only (e.g. a prompt's own cache).
+ *   x_sel      [n_sel][hidden] dtype: layer input of the selected tokens.
+ *   sel_pos    [n_sel] int32, strictly ascending, in [0, n_tok).  Rows whose
+ *              position lies outside [0, n_tok) are skipped (not written,
+ *              not attended); ordering is the caller's contract.
+ *   wq         [n_q_heads*head_dim][hidden] dtype (nn.Linear layout)
+ *   wk, wv     [n_kv_heads*head_dim][hidden] dtype
+ *   k_cache, v_cache  [n_tok][n_kv_heads][head_dim] dtype of THIS layer.
+ *   sm_scale   0 means 1/sqrt(head_dim).
+ *   out        [n_sel][n_q_heads][head_dim] dtype, or NULL.
+ *   deviation_out  [n_sel] float32, or NULL.
+ *   workspace  device scratch of at least semshare_partial_prefill_workspace()
+ *              bytes, 256-byte aligned; contents on entry are ignored.
+ *   Supported: hidden % 64 == 0; bf16 with head_dim 128 or 64, 128 % G == 0
+ *   and n_kv_heads*head_dim % 128 == 0; fp32 with even head_dim <= 128 and
+ *   n_tok <= 8192.
+ */
+semshare_status_t semshare_partial_prefill(
+    const void* x_sel, const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
+    const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
+    int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base, float sm_scale,
+    void* out, float* deviation_out, void* workspace, size_t workspace_bytes,
+    semshare_dtype_t dtype, void* stream);
+
+/* Workspace bytes semshare_partial_prefill needs for these sizes (with an
+ * attention output requested and deviation requested -- an upper bound for
+ * the calls that request less).  Returns 0 for invalid sizes. */
+size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t hidden,
+                                          int32_t n_q_heads, int32_t n_kv_heads,
+                                          int32_t head_dim, semshare_dtype_t dtype);
+
+/*
+ * High-deviation token selection (Section 3 Insight 1; Section 4.2): the
+ * n_sel positions with the largest deviation sigma (ties: the lower
+ * position first), written in ascending position order.  One workgroup
+ * selects by radix over the float bits; sigma must hold non-negative finite
+ * values (as deviation_out produces).
+ *   sigma    [n_tok] float32.   n_tok <= 2^20.   0 <= n_sel <= n_tok.
+ *   sel_pos  [n_sel] int32 (output).
+ */
+semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
+                                            int32_t* sel_pos, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEMSHARE_H */

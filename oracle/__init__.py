@@ -154,14 +154,16 @@ def gather_rows(src: np.ndarray, idx) -> np.ndarray:
 
 
 def qkv_rows(x_sel, sel_pos, wq, wk, wv, n_q_heads: int, n_kv_heads: int, head_dim: int,
-             base: float = 10000.0, dtype: str = "f64"):
+             base: float = 10000.0, dtype: str = "f64", want_q: bool = True, want_kv: bool = True):
+    """Recomputed (q, k, v) rows; q or (k, v) is None when not wanted."""
     x = _f64(x_sel)
     pos = np.ascontiguousarray(sel_pos, dtype=np.int32)
-    wq, wk, wv = _f64(wq), _f64(wk), _f64(wv)
+    wq = _f64(wq) if want_q else None
+    wk, wv = (_f64(wk), _f64(wv)) if want_kv else (None, None)
     n, hidden = x.shape
-    q = np.empty((n, n_q_heads * head_dim))
-    k = np.empty((n, n_kv_heads * head_dim))
-    v = np.empty((n, n_kv_heads * head_dim))
+    q = np.empty((n, n_q_heads * head_dim)) if want_q else None
+    k = np.empty((n, n_kv_heads * head_dim)) if want_kv else None
+    v = np.empty((n, n_kv_heads * head_dim)) if want_kv else None
     _load().orc_qkv_rows(_ptr(x), _ptr(pos), n, _ptr(wq), _ptr(wk), _ptr(wv), hidden, n_q_heads,
                          n_kv_heads, head_dim, float(base), _ptr(q), _ptr(k), _ptr(v), _DT[dtype])
     return q, k, v

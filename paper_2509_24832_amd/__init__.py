@@ -1,0 +1,9 @@
+"""SemShareKV hot path for MI355X (gfx950): fuzzy token matching and KV reuse.
+
+The compute lives in libsemshare.so (HIP kernels behind the C ABI of
+include/semshare.h); ``semshare`` is its thin ctypes binding.
+"""
+from .semshare import (  # noqa: F401
+    BF16, FP32, SemShareError, declared_symbols, gather_kv, gather_rows, last_error, load, lsh_encode, match,
+    partial_prefill, partial_prefill_workspace_bytes, rope_embed, select_recompute, version,
+)

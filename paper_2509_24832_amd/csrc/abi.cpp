@@ -1,0 +1,189 @@
+// C ABI of libsemshare.so: host-side argument validation, workspace
+// planning and dispatch to the HIP launchers.  Nothing here allocates
+// device memory or synchronizes the device.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "semshare_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+semshare_status_t fail(semshare_status_t code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+semshare_status_t ok() {
+    g_err[0] = '\0';
+    return SEMSHARE_OK;
+}
+
+semshare_status_t from_hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(SEMSHARE_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool dtype_ok(semshare_dtype_t dt) { return dt == SEMSHARE_FP32 || dt == SEMSHARE_BF16; }
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+size_t dtype_size(semshare_dtype_t dt) { return dt == SEMSHARE_BF16 ? 2 : 4; }
+
+}  // namespace
+
+extern "C" {
+
+const char* semshare_last_error(void) { return g_err; }
+
+int32_t semshare_version(void) { return 10000; }
+
+semshare_status_t semshare_rope_embed(const void* x, void* y, int64_t n_tok, int32_t dim,
+                                      int64_t pos0, double base, semshare_dtype_t dtype,
+                                      void* stream) {
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "rope_embed: unknown dtype %d", dtype);
+    if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "rope_embed: n_tok < 0");
+    if (dim <= 0 || (dim & 1)) return fail(SEMSHARE_E_INVAL, "rope_embed: dim must be even and > 0 (got %d)", dim);
+    if (!(base > 0.0) || !std::isfinite(base)) return fail(SEMSHARE_E_INVAL, "rope_embed: base must be finite and > 0");
+    if (pos0 < 0) return fail(SEMSHARE_E_INVAL, "rope_embed: pos0 < 0");
+    if (pos0 + n_tok > (int64_t(1) << 40)) return fail(SEMSHARE_E_INVAL, "rope_embed: positions exceed 2^40");
+    if (n_tok == 0) return ok();
+    if (!x || !y) return fail(SEMSHARE_E_INVAL, "rope_embed: null buffer");
+    return from_hip(semshare::launch_rope_embed(x, y, n_tok, dim, pos0, base, dtype, (hipStream_t)stream),
+                    "rope_embed launch");
+}
+
+semshare_status_t semshare_lsh_encode(const void* x, const void* planes, uint64_t* codes,
+                                      int64_t n_tok, int32_t dim, int32_t n_bits,
+                                      semshare_dtype_t dtype, void* stream) {
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "lsh_encode: unknown dtype %d", dtype);
+    if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "lsh_encode: n_tok < 0");
+    if (n_bits != 64 && n_bits != 128 && n_bits != 256)
+        return fail(SEMSHARE_E_INVAL, "lsh_encode: n_bits must be 64, 128 or 256 (got %d)", n_bits);
+    if (dim <= 0) return fail(SEMSHARE_E_INVAL, "lsh_encode: dim must be > 0");
+    if (dtype == SEMSHARE_BF16 && dim % 64)
+        return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: bf16 needs dim %% 64 == 0 (got %d)", dim);
+    if (dtype == SEMSHARE_FP32 && dim % 4)
+        return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: fp32 needs dim %% 4 == 0 (got %d)", dim);
+    if (n_tok > (int64_t(1) << 31) - 64) return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: n_tok too large");
+    if (n_tok == 0) return ok();
+    if (!x || !planes || !codes) return fail(SEMSHARE_E_INVAL, "lsh_encode: null buffer");
+    if (!aligned16(x) || !aligned16(planes) || !aligned16(codes))
+        return fail(SEMSHARE_E_INVAL, "lsh_encode: buffers must be 16-byte aligned");
+    return from_hip(semshare::launch_lsh_encode(x, planes, codes, n_tok, dim, n_bits, dtype, (hipStream_t)stream),
+                    "lsh_encode launch");
+}
+
+semshare_status_t semshare_match(const uint64_t* tgt_codes, int64_t n_tgt,
+                                 const uint64_t* ref_codes, int64_t n_ref, int32_t n_words,
+                                 int32_t* idx, int32_t* dist, void* stream) {
+    if (n_tgt < 0) return fail(SEMSHARE_E_INVAL, "match: n_tgt < 0");
+    if (n_words < 1 || n_words > 4) return fail(SEMSHARE_E_INVAL, "match: n_words must be 1..4 (got %d)", n_words);
+    if (n_ref < 1) return fail(SEMSHARE_E_INVAL, "match: n_ref must be >= 1");
+    if (n_ref >= (int64_t(1) << 23)) return fail(SEMSHARE_E_UNSUPPORTED, "match: n_ref must be < 2^23");
+    if (n_tgt > (int64_t(1) << 31) - 1024) return fail(SEMSHARE_E_UNSUPPORTED, "match: n_tgt too large");
+    if (n_tgt == 0) return ok();
+    if (!tgt_codes || !ref_codes || !idx) return fail(SEMSHARE_E_INVAL, "match: null buffer");
+    return from_hip(semshare::launch_match(tgt_codes, n_tgt, ref_codes, n_ref, n_words, idx, dist, (hipStream_t)stream),
+                    "match launch");
+}
+
+semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const int32_t* idx,
+                                     int64_t n_tgt, int64_t n_ref, void* out_k, void* out_v,
+                                     int32_t n_layers, int32_t n_kv_heads, int32_t head_dim,
+                                     semshare_dtype_t dtype, void* stream) {
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "gather_kv: unknown dtype %d", dtype);
+    if (n_tgt < 0 || n_ref < 0 || n_layers < 0) return fail(SEMSHARE_E_INVAL, "gather_kv: negative size");
+    if (n_kv_heads <= 0 || head_dim <= 0) return fail(SEMSHARE_E_INVAL, "gather_kv: n_kv_heads and head_dim must be > 0");
+    if ((ref_v == nullptr) != (out_v == nullptr))
+        return fail(SEMSHARE_E_INVAL, "gather_kv: ref_v and out_v must both be set or both be NULL");
+    const int64_t row_bytes = (int64_t)n_kv_heads * head_dim * (int64_t)dtype_size(dtype);
+    if (row_bytes % 16) return fail(SEMSHARE_E_UNSUPPORTED, "gather_kv: row size %lld bytes is not a multiple of 16", (long long)row_bytes);
+    if ((int64_t)n_layers * n_tgt > (int64_t(1) << 30) || n_ref > (int64_t(1) << 31) - 1)
+        return fail(SEMSHARE_E_UNSUPPORTED, "gather_kv: too many rows");
+    if (n_tgt == 0 || n_layers == 0) return ok();
+    if (!ref_k || !out_k || !idx) return fail(SEMSHARE_E_INVAL, "gather_kv: null buffer");
+    if (!aligned16(ref_k) || !aligned16(out_k) || (ref_v && (!aligned16(ref_v) || !aligned16(out_v))))
+        return fail(SEMSHARE_E_INVAL, "gather_kv: buffers must be 16-byte aligned");
+    return from_hip(semshare::launch_gather_rows(ref_k, ref_v, idx, n_tgt, n_ref, out_k, out_v, n_layers, row_bytes,
+                                                 (hipStream_t)stream),
+                    "gather_kv launch");
+}
+
+size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t hidden,
+                                          int32_t n_q_heads, int32_t n_kv_heads,
+                                          int32_t head_dim, semshare_dtype_t dtype) {
+    if (!dtype_ok(dtype) || n_sel < 0 || n_tok < 0 || hidden <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 ||
+        head_dim <= 0 || n_q_heads % n_kv_heads)
+        return 0;
+    return semshare::plan_partial_prefill(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
+}
+
+semshare_status_t semshare_partial_prefill(
+    const void* x_sel, const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
+    const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
+    int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base, float sm_scale,
+    void* out, float* deviation_out, void* workspace, size_t workspace_bytes,
+    semshare_dtype_t dtype, void* stream) {
+    const char* fn = "partial_prefill";
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "%s: unknown dtype %d", fn, dtype);
+    if (n_sel < 0 || n_tok < 0) return fail(SEMSHARE_E_INVAL, "%s: negative size", fn);
+    if (n_sel > n_tok) return fail(SEMSHARE_E_INVAL, "%s: n_sel (%lld) > n_tok (%lld)", fn, (long long)n_sel, (long long)n_tok);
+    if (hidden <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0)
+        return fail(SEMSHARE_E_INVAL, "%s: sizes must be > 0", fn);
+    if (n_q_heads % n_kv_heads) return fail(SEMSHARE_E_INVAL, "%s: n_q_heads %% n_kv_heads != 0", fn);
+    if (head_dim & 1) return fail(SEMSHARE_E_INVAL, "%s: head_dim must be even", fn);
+    if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
+    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", fn);
+    if (n_tok > (int64_t(1) << 30) || (int64_t)n_kv_heads * head_dim * n_tok > (int64_t(1) << 40))
+        return fail(SEMSHARE_E_UNSUPPORTED, "%s: cache too large", fn);
+    const int32_t G = n_q_heads / n_kv_heads;
+    if (hidden % 64) return fail(SEMSHARE_E_UNSUPPORTED, "%s: hidden %% 64 != 0", fn);
+    if (dtype == SEMSHARE_BF16) {
+        if (head_dim != 128 && head_dim != 64)
+            return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 supports head_dim 64 or 128 (got %d)", fn, head_dim);
+        if (128 % G) return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 needs 128 %% (n_q_heads/n_kv_heads) == 0", fn);
+        if (((int64_t)n_kv_heads * head_dim) % 128)
+            return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 needs n_kv_heads*head_dim %% 128 == 0", fn);
+    } else {
+        if (head_dim > 128) return fail(SEMSHARE_E_UNSUPPORTED, "%s: fp32 supports head_dim <= 128", fn);
+        if (n_tok > 8192) return fail(SEMSHARE_E_UNSUPPORTED, "%s: fp32 path supports n_tok <= 8192", fn);
+    }
+    if (n_sel == 0) return ok();
+    if (!x_sel || !sel_pos || !wk || !wv || !k_cache || !v_cache)
+        return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (out && !wq) return fail(SEMSHARE_E_INVAL, "%s: wq is NULL but out is requested", fn);
+    if (!aligned16(x_sel) || !aligned16(wk) || !aligned16(wv) || !aligned16(k_cache) || !aligned16(v_cache) ||
+        (out && (!aligned16(wq) || !aligned16(out))))
+        return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
+    const semshare::PrefillPlan plan =
+        semshare::plan_partial_prefill(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
+    if (!workspace || workspace_bytes < plan.total)
+        return fail(SEMSHARE_E_INVAL, "%s: workspace of %zu bytes is smaller than the %zu required", fn,
+                    workspace_bytes, plan.total);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(SEMSHARE_E_INVAL, "%s: workspace not 256-byte aligned", fn);
+    semshare::PrefillArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden,
+                            n_q_heads, n_kv_heads, head_dim, rope_base,
+                            sm_scale > 0.0f ? sm_scale : (float)(1.0 / std::sqrt((double)head_dim)),
+                            out, deviation_out, workspace, workspace_bytes, dtype};
+    hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_partial_prefill_bf16(a, plan, (hipStream_t)stream)
+                                          : semshare::launch_partial_prefill_f32(a, plan, (hipStream_t)stream);
+    return from_hip(e, "partial_prefill launch");
+}
+
+semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
+                                            int32_t* sel_pos, void* stream) {
+    if (n_tok < 0 || n_sel < 0 || n_sel > n_tok)
+        return fail(SEMSHARE_E_INVAL, "select_recompute: need 0 <= n_sel <= n_tok");
+    if (n_tok > (int64_t(1) << 20)) return fail(SEMSHARE_E_UNSUPPORTED, "select_recompute: n_tok must be <= 2^20");
+    if (n_sel == 0) return ok();
+    if (!sigma || !sel_pos) return fail(SEMSHARE_E_INVAL, "select_recompute: null buffer");
+    return from_hip(semshare::launch_select_recompute(sigma, n_tok, n_sel, sel_pos, (hipStream_t)stream),
+                    "select_recompute launch");
+}
+
+}  // extern "C"

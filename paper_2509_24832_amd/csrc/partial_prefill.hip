@@ -1,0 +1,663 @@
+// One attention layer of partial prefill (Sections 4.2, 4.3.3; KV deviation
+// of Appendix A.4), bf16 storage with fp32 accumulation.
+//
+// Kernels, in stream order:
+//  1. prep        RoPE (cos, sin) table for the selected positions, one entry
+//                 per (row, pair) shared by all heads and by q and k; zeroes
+//                 the deviation sums.
+//  2. qkv_gemm    [n_sel, hidden] x [Wq;Wk;Wv]^T on v_mfma_f32_32x32x16_bf16,
+//                 128x128x64 tiles, LDS double buffering.  Epilogue through an
+//                 fp32 LDS tile: RoPE of q/k pairs, bf16 rounding, q to the
+//                 workspace, k/v scattered into the cache rows sel_pos (after
+//                 reading the old row for the deviation sums).  Tiles are
+//                 mapped XCD-major so the M tiles of one weight tile share an L2.
+//  3. dev_final   sigma = sqrt(sum dK^2) + sqrt(sum dV^2).
+//  4. attention   flash-style causal GQA attention of the selected rows over
+//                 the assembled cache.  A workgroup owns one kv head and 128
+//                 query columns (128/G selected rows x G heads); S^T = K Q^T
+//                 and O^T = V^T P^T on MFMA, so every lane holds one query
+//                 column and the softmax row statistics need a single
+//                 cross-lane exchange.  K and V^T tiles of 64 keys are staged
+//                 in LDS (V transposed on the way in).  Long key ranges are
+//                 split into chunks (split-KV) when there are too few tiles
+//                 to fill the chip.
+//  5. combine     log-sum-exp merge of the split-KV partial results.
+#include <climits>
+
+#include "semshare_internal.h"
+
+namespace semshare {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ------------------------------------------------------------------ prep
+
+__global__ void prep_kernel(const int32_t* __restrict__ pos, int64_t n_sel, int64_t n_tok,
+                            int32_t half_d, double log2_base, float2* __restrict__ rope,
+                            float* __restrict__ dev_sums) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n_sel * half_d) {
+        const int64_t m = i / half_d;
+        const int32_t k = (int32_t)(i - m * half_d);
+        int32_t p = pos[m];
+        if (p < 0 || p >= n_tok) p = 0;
+        const double theta = exp2(-(2.0 * (double)k / (double)(2 * half_d)) * log2_base);
+        float s, c;
+        rope_sincos((double)p, theta, &s, &c);
+        rope[i] = make_float2(c, s);
+    }
+    if (dev_sums && i < n_sel * 2) dev_sums[i] = 0.0f;
+}
+
+__global__ void dev_final_kernel(const float* __restrict__ sums, float* __restrict__ dev, int64_t n_sel) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n_sel) dev[i] = sqrtf(sums[2 * i]) + sqrtf(sums[2 * i + 1]);
+}
+
+// ------------------------------------------------------------------ QKV GEMM
+
+constexpr int GBM = 128, GBN = 128, GBK = 64;
+constexpr int GLDA = GBK + 8;   // bf16 per LDS operand row (144 B: conflict-free 16-B reads)
+constexpr int GLDC = GBN + 8;   // floats per LDS epilogue row
+constexpr int kGemmOperandBytes = 2 * (GBM + GBN) * GLDA * 2;
+constexpr int kGemmEpilogueBytes = GBM * GLDC * 4;
+constexpr int kGemmLdsBytes = kGemmOperandBytes > kGemmEpilogueBytes ? kGemmOperandBytes : kGemmEpilogueBytes;
+
+struct GemmArgs {
+    const uint16_t* x;      // [n_sel][hidden]
+    const int32_t* pos;     // [n_sel]
+    const uint16_t* w[3];   // Wq, Wk, Wv  (rows = output features)
+    int32_t seg_tiles[3];   // n-tiles per segment (0 for q in K/V-only mode)
+    int32_t seg_cols[3];    // output columns per segment
+    int32_t n_nt, n_mt;
+    int64_t n_sel, n_tok;
+    int32_t hidden, D;
+    uint16_t* q_out;        // [n_sel][Hq*D]
+    uint16_t* kv[2];        // k_cache, v_cache [n_tok][Hkv*D]
+    const float2* rope;     // [n_sel][D/2]
+    float* dev_sums;        // [n_sel][2] or null
+};
+
+__device__ __forceinline__ void gemm_load_regs(const uint16_t* p, u32x4_t (&r)[4]) {
+    const u32x4_t* q = reinterpret_cast<const u32x4_t*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = q[i];
+}
+
+__device__ __forceinline__ void gemm_store_lds(uint16_t* p, const u32x4_t (&r)[4]) {
+    u32x4_t* q = reinterpret_cast<u32x4_t*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) q[i] = r[i];
+}
+
+__global__ __launch_bounds__(256, 2) void qkv_gemm_kernel(GemmArgs g) {
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kGemmLdsBytes];
+    uint16_t* As = reinterpret_cast<uint16_t*>(smem);
+    uint16_t* Bs = As + 2 * GBM * GLDA;
+
+    // XCD-major tile order: workgroup b runs on XCD b % 8; all M tiles of one
+    // N (weight) tile go to the same XCD, consecutively.
+    const int b = blockIdx.x;
+    const int xcd = b & 7;
+    const int j = b >> 3;
+    const int n_idx = xcd + 8 * (j / g.n_mt);
+    const int m_idx = j % g.n_mt;
+    if (n_idx >= g.n_nt) return;
+    int seg = 0, nt = n_idx;
+    if (nt >= g.seg_tiles[0]) {
+        nt -= g.seg_tiles[0];
+        seg = 1;
+        if (nt >= g.seg_tiles[1]) { nt -= g.seg_tiles[1]; seg = 2; }
+    }
+    const uint16_t* wseg = seg == 0 ? g.w[0] : (seg == 1 ? g.w[1] : g.w[2]);
+    uint16_t* kvseg = seg == 2 ? g.kv[1] : g.kv[0];
+    const int seg_cols = seg == 0 ? g.seg_cols[0] : g.seg_cols[1];
+    const int64_t m0 = (int64_t)m_idx * GBM;
+    const int32_t ncol0 = nt * GBN;  // first column within the segment
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // global -> register assignment: 2 threads per row, 64 B each
+    const int lrow = tid >> 1, lk = (tid & 1) * 32;
+    int64_t arow = m0 + lrow;
+    if (arow > g.n_sel - 1) arow = g.n_sel - 1;  // tail rows: computed, never stored
+    const uint16_t* a_src = g.x + arow * g.hidden + lk;
+    const uint16_t* b_src = wseg + (int64_t)(ncol0 + lrow) * g.hidden + lk;
+    const int lds_off = lrow * GLDA + lk;
+
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int k = 0; k < 2; ++k) acc[i][k] = f32x16_t{};
+
+    u32x4_t ra[4], rb[4];
+    gemm_load_regs(a_src, ra);
+    gemm_load_regs(b_src, rb);
+    gemm_store_lds(As + lds_off, ra);
+    gemm_store_lds(Bs + lds_off, rb);
+    __syncthreads();
+
+    const int nk = g.hidden / GBK;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            gemm_load_regs(a_src + (kt + 1) * GBK, ra);
+            gemm_load_regs(b_src + (kt + 1) * GBK, rb);
+        }
+        const uint16_t* Ab = As + buf * GBM * GLDA;
+        const uint16_t* Bb = Bs + buf * GBN * GLDA;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            bf16x8_t av[2], bv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                av[i] = *reinterpret_cast<const bf16x8_t*>(Ab + (64 * wm + 32 * i + l32) * GLDA + 32 * half + 8 * s);
+                bv[i] = *reinterpret_cast<const bf16x8_t*>(Bb + (64 * wn + 32 * i + l32) * GLDA + 32 * half + 8 * s);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int k = 0; k < 2; ++k)
+                    acc[i][k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[k], acc[i][k], 0, 0, 0);
+        }
+        if (more) {
+            gemm_store_lds(As + (buf ^ 1) * GBM * GLDA + lds_off, ra);
+            gemm_store_lds(Bs + (buf ^ 1) * GBN * GLDA + lds_off, rb);
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: accumulators -> fp32 LDS tile
+    float* Cs = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int r = 64 * wm + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+                const int c = 64 * wn + 32 * k + l32;
+                Cs[r * GLDC + c] = acc[i][k][v];
+            }
+    __syncthreads();
+
+    const int half_d = g.D / 2;
+#pragma unroll 1
+    for (int ps = 0; ps < (GBM * GBN / 8) / 256; ++ps) {
+        const int item = ps * 256 + tid;
+        const int r = item >> 4, cg = item & 15;
+        const int64_t m = m0 + r;
+        const int32_t n = ncol0 + 8 * cg;  // column within the segment
+        float v8[8];
+        {
+            const float4 c0 = *reinterpret_cast<const float4*>(Cs + r * GLDC + 8 * cg);
+            const float4 c1 = *reinterpret_cast<const float4*>(Cs + r * GLDC + 8 * cg + 4);
+            v8[0] = c0.x; v8[1] = c0.y; v8[2] = c0.z; v8[3] = c0.w;
+            v8[4] = c1.x; v8[5] = c1.y; v8[6] = c1.z; v8[7] = c1.w;
+        }
+        float dsum = 0.0f;
+        if (m < g.n_sel) {
+            const int32_t p = g.pos[m];
+            if (seg < 2) {  // RoPE on q and k: pairs (2k, 2k+1) within the head
+                const int32_t k0 = (n % g.D) >> 1;
+                const float2* cs = g.rope + m * half_d + k0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float2 t = cs[e];
+                    const float x0 = v8[2 * e], x1 = v8[2 * e + 1];
+                    v8[2 * e] = t.x * x0 - t.y * x1;
+                    v8[2 * e + 1] = t.y * x0 + t.x * x1;
+                }
+            }
+            u32x4_t packed;
+            packed.x = pack_bf16x2(v8[0], v8[1]);
+            packed.y = pack_bf16x2(v8[2], v8[3]);
+            packed.z = pack_bf16x2(v8[4], v8[5]);
+            packed.w = pack_bf16x2(v8[6], v8[7]);
+            if (seg == 0) {
+                *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
+            } else if (p >= 0 && p < g.n_tok) {
+                uint16_t* dst = kvseg + (int64_t)p * seg_cols + n;
+                if (g.dev_sums) {
+                    const u32x4_t old = *reinterpret_cast<const u32x4_t*>(dst);
+                    const uint32_t ow[4] = {old.x, old.y, old.z, old.w};
+                    const uint32_t nw[4] = {packed.x, packed.y, packed.z, packed.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float d0 = bf16_lo(ow[e]) - bf16_lo(nw[e]);
+                        const float d1 = bf16_hi(ow[e]) - bf16_hi(nw[e]);
+                        dsum += d0 * d0 + d1 * d1;
+                    }
+                }
+                *reinterpret_cast<u32x4_t*>(dst) = packed;
+            }
+        }
+        if (g.dev_sums && seg > 0) {
+            // the 16 threads of one tile row are 16 consecutive lanes
+            dsum += __shfl_xor(dsum, 8, 16);
+            dsum += __shfl_xor(dsum, 4, 16);
+            dsum += __shfl_xor(dsum, 2, 16);
+            dsum += __shfl_xor(dsum, 1, 16);
+            if (cg == 0 && m < g.n_sel && dsum != 0.0f) atomicAdd(g.dev_sums + 2 * m + (seg - 1), dsum);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ attention
+
+constexpr int KT = 64;  // keys per LDS tile
+
+struct AttnArgs {
+    const uint16_t* q;        // [n_sel][Hq][D]
+    const int32_t* pos;       // [n_sel]
+    const uint16_t* k_cache;  // [n_tok][Hkv][D]
+    const uint16_t* v_cache;
+    uint16_t* out;            // [n_sel][Hq][D]
+    float* part_o;            // [items][128][D]
+    float* part_ml;           // [items][128][2]
+    int32_t* n_used;          // [n_tiles * Hkv]
+    int64_t n_sel, n_tok;
+    int32_t Hq, Hkv, G, R;
+    int32_t n_tiles, chunk, n_chunks;
+    float cl2;                // sm_scale * log2(e)
+};
+
+template <int D>
+struct AttnLds {
+    static constexpr int KLD = D + 8;   // bf16 per K row  (D=128: 272 B)
+    static constexpr int VLD = KT + 4;  // bf16 per V^T row (136 B)
+    static constexpr int kBytes = 2 * KT * KLD * 2;
+    static constexpr int vBytes = 2 * D * VLD * 2;
+    static constexpr int kChunksPerKey = D / 8;              // 16-B chunks per key row
+    static constexpr int kKLoads = KT * kChunksPerKey / 256;  // K u32x4_t loads per thread
+    static constexpr int kVItems = 16 * (D / 8);              // (key quad, d group) items
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
+    using L = AttnLds<D>;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[L::kBytes + L::vBytes];
+    __shared__ int32_t s_pos[128];
+    __shared__ int32_t s_pmin, s_pmax;
+    uint16_t* Ks = reinterpret_cast<uint16_t*>(smem);
+    uint16_t* Vt = reinterpret_cast<uint16_t*>(smem + L::kBytes);
+
+    const int b = blockIdx.x;
+    const int g = b % a.Hkv;
+    const int jj = b / a.Hkv;
+    const int tile = a.n_tiles - 1 - jj / a.n_chunks;  // longest (latest) tiles first
+    const int chunk_id = jj % a.n_chunks;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int col = 32 * wave + l32;
+    const int row_local = col % a.R, head_local = col / a.R;
+    const int64_t row = (int64_t)tile * a.R + row_local;
+    const int head = g * a.G + head_local;
+
+    if (tid < a.R) {
+        const int64_t r = (int64_t)tile * a.R + tid;
+        int32_t p = r < a.n_sel ? a.pos[r] : -1;
+        if (p < 0 || p >= a.n_tok) p = -1;
+        s_pos[tid] = p;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        int32_t mn = INT_MAX, mx = -1;
+        for (int i = lane; i < a.R; i += 64) {
+            const int32_t p = s_pos[i];
+            if (p >= 0) { mn = min(mn, p); mx = max(mx, p); }
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            mn = min(mn, __shfl_xor(mn, o));
+            mx = max(mx, __shfl_xor(mx, o));
+        }
+        if (lane == 0) { s_pmin = mn; s_pmax = mx; }
+    }
+    __syncthreads();
+    const int32_t pmin = s_pmin, pmax = s_pmax;
+    const int32_t p_l = s_pos[row_local];
+    if (chunk_id == 0 && tid == 0 && a.n_chunks > 1)
+        a.n_used[tile * a.Hkv + g] = pmax < 0 ? 0 : pmax / a.chunk + 1;
+    const int32_t kbeg = chunk_id * a.chunk;
+    const int32_t kend = min(kbeg + a.chunk, pmax + 1);
+    if (kbeg >= kend) return;
+
+    // Q^T operand: lane half h holds d in [h*D/2, h*D/2 + D/2)
+    bf16x8_t qf[D / 16];
+    {
+        const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(a.q + ((p_l >= 0 ? row : 0) * a.Hq + head) * (int64_t)D + half * (D / 2));
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) {
+            u32x4_t w = p_l >= 0 ? qp[s] : u32x4_t{0u, 0u, 0u, 0u};
+            qf[s] = __builtin_bit_cast(bf16x8_t, w);
+        }
+    }
+
+    const int64_t row_stride = (int64_t)a.Hkv * D;  // elements between consecutive keys
+    const uint16_t* kbase = a.k_cache + (int64_t)g * D;
+    const uint16_t* vbase = a.v_cache + (int64_t)g * D;
+    const int32_t last_key = (int32_t)a.n_tok - 1;
+
+    u32x4_t rk[L::kKLoads];
+    u32x4_t rv[4];
+    const bool v_owner = tid < L::kVItems;
+    const int v_dg = tid % (D / 8), v_kq = tid / (D / 8);
+
+    auto load_regs = [&](int32_t k0) {
+#pragma unroll
+        for (int i = 0; i < L::kKLoads; ++i) {
+            const int item = i * 256 + tid;
+            const int key = item / L::kChunksPerKey, ch = item % L::kChunksPerKey;
+            const int32_t kk = min(k0 + key, last_key);
+            rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + kk * row_stride + ch * 8);
+        }
+        if (v_owner) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int32_t kk = min(k0 + 4 * v_kq + i, last_key);
+                rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + kk * row_stride + v_dg * 8);
+            }
+        }
+    };
+    auto store_lds = [&](int buf) {
+        uint16_t* kb = Ks + buf * KT * L::KLD;
+#pragma unroll
+        for (int i = 0; i < L::kKLoads; ++i) {
+            const int item = i * 256 + tid;
+            const int key = item / L::kChunksPerKey, ch = item % L::kChunksPerKey;
+            *reinterpret_cast<u32x4_t*>(kb + key * L::KLD + ch * 8) = rk[i];
+        }
+        if (v_owner) {
+            uint16_t* vb = Vt + buf * D * L::VLD;
+            const uint32_t w0[4] = {rv[0].x, rv[0].y, rv[0].z, rv[0].w};
+            const uint32_t w1[4] = {rv[1].x, rv[1].y, rv[1].z, rv[1].w};
+            const uint32_t w2[4] = {rv[2].x, rv[2].y, rv[2].z, rv[2].w};
+            const uint32_t w3[4] = {rv[3].x, rv[3].y, rv[3].z, rv[3].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                u32x2_t lo, hi;  // d = 8*dg + 2e (lo halves) and 2e+1 (hi halves), keys 4kq..4kq+3
+                lo.x = __builtin_amdgcn_perm(w1[e], w0[e], 0x05040100u);
+                lo.y = __builtin_amdgcn_perm(w3[e], w2[e], 0x05040100u);
+                hi.x = __builtin_amdgcn_perm(w1[e], w0[e], 0x07060302u);
+                hi.y = __builtin_amdgcn_perm(w3[e], w2[e], 0x07060302u);
+                *reinterpret_cast<u32x2_t*>(vb + (8 * v_dg + 2 * e) * L::VLD + 4 * v_kq) = lo;
+                *reinterpret_cast<u32x2_t*>(vb + (8 * v_dg + 2 * e + 1) * L::VLD + 4 * v_kq) = hi;
+            }
+        }
+    };
+
+    f32x16_t oacc[D / 32];
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) oacc[i] = f32x16_t{};
+    float m_run = -1.0e30f, l_run = 0.0f;
+    const float cl2 = a.cl2;
+
+    load_regs(kbeg);
+    store_lds(0);
+    __syncthreads();
+    const int n_kt = (kend - kbeg + KT - 1) / KT;
+    for (int it = 0; it < n_kt; ++it) {
+        const int32_t kt = kbeg + it * KT;
+        const int buf = it & 1;
+        const bool more = it + 1 < n_kt;
+        if (more) load_regs(kt + KT);
+
+        const uint16_t* kb = Ks + buf * KT * L::KLD;
+        f32x16_t sacc[2] = {f32x16_t{}, f32x16_t{}};
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                const bf16x8_t kv = *reinterpret_cast<const bf16x8_t*>(kb + (32 * mb + l32) * L::KLD + half * (D / 2) + 8 * s);
+                sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qf[s], sacc[mb], 0, 0, 0);
+            }
+        }
+        // sacc[mb][v] = score of key kt + 32mb + 8(v/4) + 4half + (v%4) for this lane's column
+        if (kt + KT - 1 > pmin || kt + KT > kend) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int32_t key = kt + 32 * mb + 8 * (v >> 2) + 4 * half + (v & 3);
+                    if (key > p_l || key >= kend) sacc[mb][v] = -INFINITY;
+                }
+        }
+        float mx = sacc[0][0];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[mb][v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * cl2);
+        const float mc = m_new * cl2;
+        float lsum = 0.0f;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mb][v], cl2, -mc));
+                sacc[mb][v] = pv;
+                lsum += pv;
+            }
+        l_run = l_run * alpha + lsum;
+        m_run = m_new;
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
+
+        const uint16_t* vb = Vt + buf * D * L::VLD;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {  // 16 keys per MFMA k-step
+            const int mb = s >> 1, v0 = 8 * (s & 1);
+            bf16x8_t pb;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pb[e] = (__bf16)sacc[mb][v0 + e];
+#pragma unroll
+            for (int i = 0; i < D / 32; ++i) {
+                const uint16_t* vr = vb + (32 * i + l32) * L::VLD + 16 * s + 4 * half;
+                const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
+                const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 8);
+                const u32x4_t w = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+                oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, w), pb, oacc[i], 0, 0, 0);
+            }
+        }
+        if (more) store_lds(buf ^ 1);
+        __syncthreads();
+    }
+
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    if (p_l < 0) return;
+    // oacc[i][v] = O[col][d = 32i + 8(v/4) + 4half + (v%4)]
+    if (pmax + 1 <= a.chunk) {
+        const float inv = 1.0f / l_tot;
+        uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D;
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int d0 = 32 * i + 8 * r + 4 * half;
+                u32x2_t w;
+                w.x = pack_bf16x2(oacc[i][4 * r] * inv, oacc[i][4 * r + 1] * inv);
+                w.y = pack_bf16x2(oacc[i][4 * r + 2] * inv, oacc[i][4 * r + 3] * inv);
+                *reinterpret_cast<u32x2_t*>(op + d0) = w;
+            }
+    } else {
+        const int64_t item = ((int64_t)tile * a.Hkv + g) * a.n_chunks + chunk_id;
+        float* po = a.part_o + (item * 128 + col) * D;
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int d0 = 32 * i + 8 * r + 4 * half;
+                *reinterpret_cast<float4*>(po + d0) =
+                    make_float4(oacc[i][4 * r], oacc[i][4 * r + 1], oacc[i][4 * r + 2], oacc[i][4 * r + 3]);
+            }
+        if (half == 0) *reinterpret_cast<float2*>(a.part_ml + (item * 128 + col) * 2) = make_float2(m_run, l_tot);
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t tg = blockIdx.x / 32;  // tile * Hkv + g
+    const int col = (blockIdx.x % 32) * 4 + wave;
+    const int32_t nu = a.n_used[tg];
+    if (nu <= 1) return;
+    const int tile = (int)(tg / a.Hkv), g = (int)(tg % a.Hkv);
+    const int row_local = col % a.R, head_local = col / a.R;
+    const int64_t row = (int64_t)tile * a.R + row_local;
+    if (row >= a.n_sel) return;
+    const int32_t p = a.pos[row];
+    if (p < 0 || p >= a.n_tok) return;
+    const int head = g * a.G + head_local;
+    const int64_t item0 = tg * a.n_chunks;
+    float M = -1.0e30f;
+    for (int c = 0; c < nu; ++c) M = fmaxf(M, a.part_ml[((item0 + c) * 128 + col) * 2]);
+    constexpr int PER = D / 64;
+    float acc[PER] = {};
+    float Lsum = 0.0f;
+    for (int c = 0; c < nu; ++c) {
+        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((item0 + c) * 128 + col) * 2);
+        const float w = __builtin_amdgcn_exp2f((ml.x - M) * a.cl2);
+        Lsum += w * ml.y;
+        const float* po = a.part_o + ((item0 + c) * 128 + col) * D + PER * lane;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) acc[e] += w * po[e];
+    }
+    const float inv = 1.0f / Lsum;
+    uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D + PER * lane;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) op[e] = f32_to_bf16(acc[e] * inv);
+}
+
+template <int D>
+hipError_t launch_attention(const AttnArgs& args, hipStream_t s) {
+    const unsigned grid = (unsigned)((int64_t)args.n_tiles * args.Hkv * args.n_chunks);
+    hipLaunchKernelGGL(attention_kernel<D>, dim3(grid), dim3(256), 0, s, args);
+    if (args.n_chunks > 1)
+        hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)((int64_t)args.n_tiles * args.Hkv * 32)), dim3(256), 0, s,
+                           args);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+PrefillPlan plan_partial_prefill(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, int dtype) {
+    PrefillPlan p{};
+    const int32_t G = n_q_heads / n_kv_heads;
+    const size_t esz = dtype == SEMSHARE_BF16 ? 2 : 4;
+    size_t off = 0;
+    p.off_q = off;
+    off = align256(off + (size_t)n_sel * n_q_heads * head_dim * esz);
+    p.off_rope = off;
+    if (dtype == SEMSHARE_BF16) off = align256(off + (size_t)n_sel * (head_dim / 2) * sizeof(float2));
+    p.off_dev = off;
+    off = align256(off + (size_t)n_sel * 2 * sizeof(float));
+    p.rows_per_tile = dtype == SEMSHARE_BF16 ? 128 / G : 1;
+    p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
+    p.chunk = (int32_t)((n_tok + 63) / 64 * 64);
+    p.n_chunks = 1;
+    if (dtype == SEMSHARE_BF16 && n_sel > 0) {
+        // split the key range when there are too few (tile, kv head) items to
+        // fill the chip; each chunk keeps >= 256 keys
+        const int64_t items = p.n_tiles * n_kv_heads;
+        int64_t want = (1024 + items - 1) / items;
+        const int64_t cap = (n_tok + 255) / 256;
+        if (want > cap) want = cap;
+        if (want < 1) want = 1;
+        const int64_t per = (n_tok + want - 1) / want;
+        p.chunk = (int32_t)((per + 63) / 64 * 64);
+        p.n_chunks = (int32_t)((n_tok + p.chunk - 1) / p.chunk);
+        if (p.n_chunks < 1) p.n_chunks = 1;
+    }
+    p.off_part_o = off;
+    p.off_part_ml = off;
+    if (p.n_chunks > 1) {
+        const size_t items = (size_t)p.n_tiles * n_kv_heads * p.n_chunks;
+        off = align256(off + items * 128 * head_dim * sizeof(float));
+        p.off_part_ml = off;
+        off = align256(off + items * 128 * 2 * sizeof(float) + (size_t)p.n_tiles * n_kv_heads * sizeof(int32_t));
+    }
+    p.total = off;
+    return p;
+}
+
+hipError_t launch_partial_prefill_bf16(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s) {
+    unsigned char* ws = static_cast<unsigned char*>(a.workspace);
+    uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + p.off_q);
+    float2* rope = reinterpret_cast<float2*>(ws + p.off_rope);
+    float* dev_sums = a.deviation_out ? reinterpret_cast<float*>(ws + p.off_dev) : nullptr;
+    const int32_t half_d = a.head_dim / 2;
+
+    {
+        const int64_t n = a.n_sel * half_d;
+        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sel_pos, a.n_sel,
+                           a.n_tok, half_d, log2(a.rope_base), rope, dev_sums);
+    }
+    {
+        GemmArgs g{};
+        g.x = static_cast<const uint16_t*>(a.x_sel);
+        g.pos = a.sel_pos;
+        g.w[0] = static_cast<const uint16_t*>(a.wq);
+        g.w[1] = static_cast<const uint16_t*>(a.wk);
+        g.w[2] = static_cast<const uint16_t*>(a.wv);
+        g.seg_cols[0] = a.n_q_heads * a.head_dim;
+        g.seg_cols[1] = g.seg_cols[2] = a.n_kv_heads * a.head_dim;
+        g.seg_tiles[0] = a.out ? g.seg_cols[0] / GBN : 0;
+        g.seg_tiles[1] = g.seg_tiles[2] = g.seg_cols[1] / GBN;
+        g.n_nt = g.seg_tiles[0] + g.seg_tiles[1] + g.seg_tiles[2];
+        g.n_mt = (int32_t)((a.n_sel + GBM - 1) / GBM);
+        g.n_sel = a.n_sel;
+        g.n_tok = a.n_tok;
+        g.hidden = a.hidden;
+        g.D = a.head_dim;
+        g.q_out = q_ws;
+        g.kv[0] = static_cast<uint16_t*>(a.k_cache);
+        g.kv[1] = static_cast<uint16_t*>(a.v_cache);
+        g.rope = rope;
+        g.dev_sums = dev_sums;
+        const int64_t per_xcd = (g.n_nt + 7) / 8;
+        const unsigned grid = (unsigned)(8 * per_xcd * g.n_mt);
+        hipLaunchKernelGGL(qkv_gemm_kernel, dim3(grid), dim3(256), 0, s, g);
+    }
+    if (a.deviation_out)
+        hipLaunchKernelGGL(dev_final_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_sums,
+                           a.deviation_out, a.n_sel);
+    if (a.out) {
+        AttnArgs t{};
+        t.q = q_ws;
+        t.pos = a.sel_pos;
+        t.k_cache = static_cast<const uint16_t*>(a.k_cache);
+        t.v_cache = static_cast<const uint16_t*>(a.v_cache);
+        t.out = static_cast<uint16_t*>(a.out);
+        t.part_o = reinterpret_cast<float*>(ws + p.off_part_o);
+        t.part_ml = reinterpret_cast<float*>(ws + p.off_part_ml);
+        t.n_used = reinterpret_cast<int32_t*>(ws + p.off_part_ml + (size_t)p.n_tiles * a.n_kv_heads * p.n_chunks * 128 * 2 * sizeof(float));
+        t.n_sel = a.n_sel;
+        t.n_tok = a.n_tok;
+        t.Hq = a.n_q_heads;
+        t.Hkv = a.n_kv_heads;
+        t.G = a.n_q_heads / a.n_kv_heads;
+        t.R = p.rows_per_tile;
+        t.n_tiles = (int32_t)p.n_tiles;
+        t.chunk = p.chunk;
+        t.n_chunks = p.n_chunks;
+        t.cl2 = a.sm_scale * kLog2e;
+        if (a.head_dim == 128) return launch_attention<128>(t, s);
+        return launch_attention<64>(t, s);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace semshare

@@ -1,0 +1,109 @@
+// High-deviation token selection (Section 3 Insight 1, Section 4.2): the
+// n_sel positions of largest deviation, ties to the lower position, emitted
+// in ascending order.
+//
+// One 1024-thread workgroup.  For non-negative floats the bit pattern orders
+// like the value, so a 4-pass, 8-bit-digit radix select over the bits finds
+// the threshold value T with count(> T) < n_sel <= count(>= T).  A final pass
+// walks the positions in order and keeps every value > T plus the first
+// (n_sel - count(> T)) values == T, compacting with block-wide prefix sums,
+// which yields the ascending output directly.
+#include "semshare_internal.h"
+
+namespace semshare {
+namespace {
+
+constexpr int kT = 1024;
+constexpr int kWaves = kT / 64;
+
+__device__ __forceinline__ uint32_t key_of(float f) {
+    return f == 0.0f ? 0u : __float_as_uint(f);  // -0 sorts with +0
+}
+
+// Exclusive block-wide prefix sum of two counters at once; returns totals.
+__device__ __forceinline__ void block_scan2(uint32_t a, uint32_t b, uint32_t& ea, uint32_t& eb,
+                                            uint32_t& ta, uint32_t& tb, uint32_t (*sw)[2]) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t ia = a, ib = b;  // inclusive wave scan
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t na = __shfl_up(ia, o), nb = __shfl_up(ib, o);
+        if (lane >= o) { ia += na; ib += nb; }
+    }
+    if (lane == 63) { sw[wave][0] = ia; sw[wave][1] = ib; }
+    __syncthreads();
+    uint32_t pa = 0, pb = 0, sa = 0, sb = 0;
+    for (int w = 0; w < kWaves; ++w) {
+        const uint32_t xa = sw[w][0], xb = sw[w][1];
+        if (w < wave) { pa += xa; pb += xb; }
+        sa += xa;
+        sb += xb;
+    }
+    ea = pa + ia - a;
+    eb = pb + ib - b;
+    ta = sa;
+    tb = sb;
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ sigma, int32_t n_tok,
+                                                    int32_t n_sel, int32_t* __restrict__ out) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t s_digit, s_need;
+    __shared__ uint32_t sw[kWaves][2];
+    const int tid = threadIdx.x;
+
+    uint32_t prefix = 0, hi_mask = 0, need = (uint32_t)n_sel;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += kT) hist[i] = 0;
+        __syncthreads();
+        for (int32_t i = tid; i < n_tok; i += kT) {
+            const uint32_t u = key_of(sigma[i]);
+            if ((u & hi_mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            uint32_t cum = 0, digit = 0, nd = need;
+            for (int b = 255; b >= 0; --b) {
+                const uint32_t h = hist[b];
+                if (cum + h >= need) { digit = (uint32_t)b; nd = need - cum; break; }
+                cum += h;
+            }
+            s_digit = digit;
+            s_need = nd;
+        }
+        __syncthreads();
+        prefix |= s_digit << shift;
+        hi_mask |= 255u << shift;
+        need = s_need;
+        __syncthreads();
+    }
+    const uint32_t thr = prefix;  // the n_sel-th largest key; `need` of its copies are taken
+
+    uint32_t base = 0, eq_taken = 0;
+    for (int32_t c0 = 0; c0 < n_tok; c0 += kT) {
+        const int32_t i = c0 + tid;
+        const uint32_t u = i < n_tok ? key_of(sigma[i]) : 0u;
+        const uint32_t gt = i < n_tok && u > thr;
+        const uint32_t eq = i < n_tok && u == thr;
+        uint32_t e_eq, e_dummy, t_eq, t_dummy;
+        block_scan2(eq, 0u, e_eq, e_dummy, t_eq, t_dummy, sw);
+        const uint32_t take = gt || (eq && eq_taken + e_eq < need);
+        uint32_t e_take, e_d2, t_take, t_d2;
+        block_scan2(take, 0u, e_take, e_d2, t_take, t_d2, sw);
+        if (take) out[base + e_take] = i;
+        base += t_take;
+        eq_taken += t_eq;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
+                                   int32_t* sel_pos, hipStream_t s) {
+    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kT), 0, s, sigma, (int32_t)n_tok, (int32_t)n_sel,
+                       sel_pos);
+    return hipGetLastError();
+}
+
+}  // namespace semshare

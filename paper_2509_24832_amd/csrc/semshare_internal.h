@@ -1,0 +1,115 @@
+// Internal declarations shared by the HIP kernels and the C ABI layer of
+// libsemshare.so.  gfx950 (CDNA4) only: 64-wide wavefronts, MFMA matrix
+// cores, 160 KB of LDS per CU, 8 XCDs with one L2 each.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "semshare.h"
+
+namespace semshare {
+
+// ------------------------------------------------------------ bf16 helpers
+// bf16 is handled as raw 16-bit patterns; widening is a shift (exact) and
+// narrowing rounds to nearest even through the native conversion.
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    __bf16 b = (__bf16)f;
+    return __builtin_bit_cast(uint16_t, b);
+}
+
+// Two floats -> packed bf16 pair (lo in bits 0..15).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// RoPE angle m * theta reduced to [-pi, pi] in fp64 (two-constant
+// Cody-Waite reduction).
+__device__ __forceinline__ double rope_reduced_angle(double m, double theta) {
+    const double a = m * theta;
+    const double n = rint(a * 0.15915494309189535);  // 1 / (2 pi)
+    double r = fma(-n, 6.283185307179586, a);         // 2 pi, high part
+    return fma(-n, 2.4492935982947064e-16, r);        // 2 pi - high part
+}
+
+// sin and cos of the RoPE angle m * theta: fp32 sincos of the reduced angle's
+// fp32 head, corrected to first order by its fp32 tail (the head alone would
+// carry up to 1.2e-7 rad of rounding error).
+__device__ __forceinline__ void rope_sincos(double m, double theta, float* s, float* c) {
+    const double r = rope_reduced_angle(m, theta);
+    const float hi = (float)r;
+    const float lo = (float)(r - (double)hi);
+    float sh, ch;
+    sincosf(hi, &sh, &ch);
+    *s = fmaf(ch, lo, sh);
+    *c = fmaf(-sh, lo, ch);
+}
+
+// ---------------------------------------------------------------- launchers
+// Every launcher assumes validated arguments and returns the launch status.
+
+hipError_t launch_rope_embed(const void* x, void* y, int64_t n_tok, int32_t dim, int64_t pos0,
+                             double base, int dtype, hipStream_t s);
+
+hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok,
+                             int32_t dim, int32_t n_bits, int dtype, hipStream_t s);
+
+hipError_t launch_match(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
+                        int32_t n_words, int32_t* idx, int32_t* dist, hipStream_t s);
+
+hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_t* idx,
+                              int64_t n_tgt, int64_t n_ref, void* dst_a, void* dst_b,
+                              int32_t n_layers, int64_t row_bytes, hipStream_t s);
+
+hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
+                                   int32_t* sel_pos, hipStream_t s);
+
+struct PrefillArgs {
+    const void* x_sel;
+    const int32_t* sel_pos;
+    int64_t n_sel;
+    const void* wq;
+    const void* wk;
+    const void* wv;
+    void* k_cache;
+    void* v_cache;
+    int64_t n_tok;
+    int32_t hidden, n_q_heads, n_kv_heads, head_dim;
+    double rope_base;
+    float sm_scale;
+    void* out;
+    float* deviation_out;
+    void* workspace;
+    size_t workspace_bytes;
+    int dtype;
+};
+
+// Partition of the partial-prefill workspace (offsets in bytes).
+struct PrefillPlan {
+    int32_t rows_per_tile;  // selected rows per attention tile (128 / G)
+    int64_t n_tiles;        // attention row tiles
+    int32_t chunk;          // keys per split-KV chunk (multiple of 64)
+    int32_t n_chunks;       // ceil(n_tok / chunk)
+    size_t off_q, off_rope, off_dev, off_part_o, off_part_ml, total;
+};
+
+PrefillPlan plan_partial_prefill(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, int dtype);
+
+hipError_t launch_partial_prefill_bf16(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s);
+hipError_t launch_partial_prefill_f32(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s);
+
+}  // namespace semshare

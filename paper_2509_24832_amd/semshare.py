@@ -1,0 +1,265 @@
+"""ctypes binding of libsemshare.so (include/semshare.h).
+
+Argument marshalling only: torch provides device memory and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.
+There is no fallback: if the library is missing or a call fails, an
+exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import List, Optional, Tuple
+
+import torch  # loaded first so the library binds to the same HIP runtime
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsemshare.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "semshare.h")
+
+OK, E_INVAL, E_UNSUPPORTED, E_DEVICE = 0, -1, -2, -3
+FP32, BF16 = 0, 1
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class SemShareError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"semshare status {status}: {message}")
+        self.status = status
+        self.message = message
+
+
+def declared_symbols() -> List[str]:
+    """Every function the C header declares."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\**\s+\**(semshare_\w+)\s*\(", text, re.M)))
+
+
+def load() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2509_24832_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I32, F64, F32, SZ = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
+                                 ctypes.c_float, ctypes.c_size_t)
+    sig = {
+        "semshare_last_error": (ctypes.c_char_p, []),
+        "semshare_version": (I32, []),
+        "semshare_rope_embed": (I32, [P, P, I64, I32, I64, F64, I32, P]),
+        "semshare_lsh_encode": (I32, [P, P, P, I64, I32, I32, I32, P]),
+        "semshare_match": (I32, [P, I64, P, I64, I32, P, P, P]),
+        "semshare_gather_kv": (I32, [P, P, P, I64, I64, P, P, I32, I32, I32, I32, P]),
+        "semshare_partial_prefill": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, F32,
+                                           P, P, P, SZ, I32, P]),
+        "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
+        "semshare_select_recompute": (I32, [P, I64, I64, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def version() -> int:
+    return int(load().semshare_version())
+
+
+def last_error() -> str:
+    return load().semshare_last_error().decode()
+
+
+def _call(fn_name: str, *args) -> None:
+    lib = load()
+    st = getattr(lib, fn_name)(*args)
+    if st != OK:
+        raise SemShareError(int(st), lib.semshare_last_error().decode())
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return FP32
+    raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32")
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    return t
+
+
+# ----------------------------------------------------------------- the calls
+
+def rope_embed(x: torch.Tensor, out: Optional[torch.Tensor] = None, pos0: int = 0,
+               base: float = 10000.0) -> torch.Tensor:
+    """RoPE of every row of x [n_tok, dim] (row r at position pos0 + r)."""
+    _dev(x, "x")
+    if x.dim() != 2:
+        raise ValueError("x must be [n_tok, dim]")
+    y = torch.empty_like(x) if out is None else _dev(out, "out", x.dtype)
+    if y.shape != x.shape:
+        raise ValueError("out shape mismatch")
+    _call("semshare_rope_embed", _ptr(x), _ptr(y), x.shape[0], x.shape[1], int(pos0), float(base), _dt(x),
+          _stream())
+    return y
+
+
+def lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Sign-bit LSH codes [n_tok, n_bits/64] (int64 tensor holding the u64 words)."""
+    _dev(x, "x")
+    _dev(planes, "planes", x.dtype)
+    if x.dim() != 2 or planes.dim() != 2 or planes.shape[1] != x.shape[1]:
+        raise ValueError("x [n_tok, dim] and planes [n_bits, dim] required")
+    n_bits = planes.shape[0]
+    codes = (torch.empty((x.shape[0], max(n_bits // 64, 1)), dtype=torch.int64, device=x.device)
+             if out is None else _dev(out, "out", torch.int64))
+    _call("semshare_lsh_encode", _ptr(x), _ptr(planes), _ptr(codes), x.shape[0], x.shape[1], n_bits, _dt(x),
+          _stream())
+    return codes
+
+
+def match(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, idx: Optional[torch.Tensor] = None,
+          dist: Optional[torch.Tensor] = None, want_dist: bool = True) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Top-1 Hamming match of target codes against reference codes."""
+    _dev(tgt_codes, "tgt_codes", torch.int64)
+    _dev(ref_codes, "ref_codes", torch.int64)
+    if tgt_codes.dim() != 2 or ref_codes.dim() != 2 or tgt_codes.shape[1] != ref_codes.shape[1]:
+        raise ValueError("codes must be [n, n_words] with equal n_words")
+    n_tgt = tgt_codes.shape[0]
+    if idx is None:
+        idx = torch.empty(n_tgt, dtype=torch.int32, device=tgt_codes.device)
+    _dev(idx, "idx", torch.int32)
+    if want_dist and dist is None:
+        dist = torch.empty(n_tgt, dtype=torch.int32, device=tgt_codes.device)
+    if dist is not None:
+        _dev(dist, "dist", torch.int32)
+    _call("semshare_match", _ptr(tgt_codes), n_tgt, _ptr(ref_codes), ref_codes.shape[0], tgt_codes.shape[1],
+          _ptr(idx), _ptr(dist), _stream())
+    return idx, dist
+
+
+def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Tensor,
+              out_k: Optional[torch.Tensor] = None, out_v: Optional[torch.Tensor] = None):
+    """out[l][t] = ref[l][idx[t]]; ref_* [L, n_ref, Hkv, D] -> out_* [L, n_tgt, Hkv, D]."""
+    _dev(ref_k, "ref_k")
+    _dev(idx, "idx", torch.int32)
+    if ref_k.dim() != 4:
+        raise ValueError("ref_k must be [L, n_ref, Hkv, D]")
+    L, n_ref, hkv, d = ref_k.shape
+    n_tgt = idx.shape[0]
+    shape = (L, n_tgt, hkv, d)
+    if out_k is None:
+        out_k = torch.empty(shape, dtype=ref_k.dtype, device=ref_k.device)
+    _dev(out_k, "out_k", ref_k.dtype)
+    if ref_v is not None:
+        _dev(ref_v, "ref_v", ref_k.dtype)
+        if ref_v.shape != ref_k.shape:
+            raise ValueError("ref_v shape mismatch")
+        if out_v is None:
+            out_v = torch.empty(shape, dtype=ref_k.dtype, device=ref_k.device)
+        _dev(out_v, "out_v", ref_k.dtype)
+    else:
+        out_v = None
+    if tuple(out_k.shape) != shape or (out_v is not None and tuple(out_v.shape) != shape):
+        raise ValueError("output shape mismatch")
+    _call("semshare_gather_kv", _ptr(ref_k), _ptr(ref_v), _ptr(idx), n_tgt, n_ref, _ptr(out_k), _ptr(out_v), L,
+          hkv, d, _dt(ref_k), _stream())
+    return out_k, out_v
+
+
+def gather_rows(src: torch.Tensor, idx: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Plain row gather out[t] = src[idx[t]] of a [n_ref, width] tensor."""
+    _dev(src, "src")
+    if src.dim() != 2:
+        raise ValueError("src must be [n_ref, width]")
+    if out is None:
+        out = torch.empty((idx.shape[0], src.shape[1]), dtype=src.dtype, device=src.device)
+    o, _ = gather_kv(src.view(1, src.shape[0], 1, src.shape[1]), None, idx,
+                     out_k=out.view(1, idx.shape[0], 1, src.shape[1]))
+    return out
+
+
+def partial_prefill_workspace_bytes(n_sel: int, n_tok: int, hidden: int, n_q_heads: int, n_kv_heads: int,
+                                    head_dim: int, dtype: torch.dtype) -> int:
+    code = BF16 if dtype == torch.bfloat16 else FP32
+    return int(load().semshare_partial_prefill_workspace(n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim,
+                                                         code))
+
+
+def partial_prefill(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tensor], wk: torch.Tensor,
+                    wv: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, n_q_heads: int,
+                    n_kv_heads: int, rope_base: float = 10000.0, sm_scale: float = 0.0,
+                    out: Optional[torch.Tensor] = None, want_out: bool = True,
+                    deviation: Optional[torch.Tensor] = None, want_deviation: bool = False,
+                    workspace: Optional[torch.Tensor] = None):
+    """One layer of partial prefill; updates k_cache/v_cache rows sel_pos in place.
+    Returns (out [n_sel, Hq, D] or None, deviation [n_sel] or None)."""
+    _dev(x_sel, "x_sel")
+    dt = x_sel.dtype
+    _dev(sel_pos, "sel_pos", torch.int32)
+    for name, t in (("wk", wk), ("wv", wv), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, name, dt)
+    n_sel, hidden = x_sel.shape
+    n_tok = k_cache.shape[0]
+    head_dim = k_cache.shape[-1]
+    if k_cache.numel() != n_tok * n_kv_heads * head_dim or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [n_tok, n_kv_heads, head_dim]")
+    if sel_pos.shape[0] != n_sel:
+        raise ValueError("sel_pos length must equal x_sel rows")
+    if want_out:
+        if wq is None:
+            raise ValueError("wq required for the attention output")
+        _dev(wq, "wq", dt)
+        if out is None:
+            out = torch.empty((n_sel, n_q_heads, head_dim), dtype=dt, device=x_sel.device)
+        _dev(out, "out", dt)
+    else:
+        out = None
+    if want_deviation:
+        if deviation is None:
+            deviation = torch.empty(n_sel, dtype=torch.float32, device=x_sel.device)
+        _dev(deviation, "deviation", torch.float32)
+    else:
+        deviation = None
+    need = partial_prefill_workspace_bytes(n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim, dt)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x_sel.device)
+    _dev(workspace, "workspace", torch.uint8)
+    _call("semshare_partial_prefill", _ptr(x_sel), _ptr(sel_pos), n_sel, _ptr(wq) if want_out else None, _ptr(wk),
+          _ptr(wv), _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim,
+          float(rope_base), float(sm_scale), _ptr(out), _ptr(deviation), _ptr(workspace), workspace.numel(),
+          _dt(x_sel), _stream())
+    return out, deviation
+
+
+def select_recompute(sigma: torch.Tensor, n_sel: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The n_sel positions of largest deviation (ties: lower position), ascending."""
+    _dev(sigma, "sigma", torch.float32)
+    if out is None:
+        out = torch.empty(n_sel, dtype=torch.int32, device=sigma.device)
+    _dev(out, "out", torch.int32)
+    _call("semshare_select_recompute", _ptr(sigma), sigma.numel(), int(n_sel), _ptr(out), _stream())
+    return out

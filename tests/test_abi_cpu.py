@@ -1,0 +1,159 @@
+"""The C-ABI library loads on a GPU-less host, exports every symbol the header
+declares, and rejects bad arguments on the host before enqueuing anything
+(no call here reaches a kernel launch).  CPU only."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import paper_2509_24832_amd as ss
+from paper_2509_24832_amd import semshare as b
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+FAKE_ODD = 0x1008  # 8-byte but not 16-byte aligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ss.load()
+
+
+def test_header_declares_the_five_calls():
+    syms = ss.declared_symbols()
+    for name in ("semshare_rope_embed", "semshare_lsh_encode", "semshare_match", "semshare_gather_kv",
+                 "semshare_partial_prefill"):
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for name in ss.declared_symbols():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_library_targets_gfx950_only(tmp_path):
+    fb = tmp_path / "fatbin.bin"
+    # an explicit output file keeps objcopy from rewriting the library in place
+    subprocess.run(["objcopy", "--dump-section", f".hip_fatbin={fb}", b.LIB_PATH, str(tmp_path / "copy.so")],
+                   check=True)
+    out = subprocess.run(["/opt/rocm/llvm/bin/clang-offload-bundler", "--list", "--type=o", f"--input={fb}"],
+                         capture_output=True, text=True, check=True)
+    targets = [t for t in out.stdout.split() if "amdgcn" in t]
+    assert targets and all(t.endswith("gfx950") for t in targets)
+
+
+def test_version(lib):
+    assert ss.version() == 10000
+
+
+def _st(fn, *args):
+    return getattr(ss.load(), fn)(*args)
+
+
+def test_rope_validation(lib):
+    assert _st("semshare_rope_embed", FAKE, FAKE, 4, 7, 0, 1e4, 1, None) == b.E_INVAL  # odd dim
+    assert "even" in ss.last_error()
+    assert _st("semshare_rope_embed", FAKE, FAKE, 4, 8, 0, -1.0, 1, None) == b.E_INVAL  # base
+    assert _st("semshare_rope_embed", FAKE, FAKE, 4, 8, -1, 1e4, 1, None) == b.E_INVAL  # pos0
+    assert _st("semshare_rope_embed", FAKE, FAKE, 4, 8, 0, 1e4, 7, None) == b.E_INVAL  # dtype
+    assert _st("semshare_rope_embed", None, None, 4, 8, 0, 1e4, 1, None) == b.E_INVAL  # null
+    assert _st("semshare_rope_embed", None, None, 0, 8, 0, 1e4, 1, None) == b.OK  # empty
+    assert ss.last_error() == ""
+
+
+def test_lsh_validation(lib):
+    assert _st("semshare_lsh_encode", FAKE, FAKE, FAKE, 10, 64, 96, 1, None) == b.E_INVAL  # n_bits
+    assert _st("semshare_lsh_encode", FAKE, FAKE, FAKE, 10, 100, 64, 1, None) == b.E_UNSUPPORTED  # bf16 dim
+    assert _st("semshare_lsh_encode", FAKE, FAKE, FAKE, 10, 6, 64, 0, None) == b.E_UNSUPPORTED  # fp32 dim
+    assert _st("semshare_lsh_encode", FAKE_ODD, FAKE, FAKE, 10, 64, 64, 1, None) == b.E_INVAL  # alignment
+    assert _st("semshare_lsh_encode", None, FAKE, FAKE, 10, 64, 64, 1, None) == b.E_INVAL
+    assert _st("semshare_lsh_encode", None, None, None, 0, 64, 64, 1, None) == b.OK
+
+
+def test_match_validation(lib):
+    assert _st("semshare_match", FAKE, 4, FAKE, 4, 0, FAKE, None, None) == b.E_INVAL  # n_words
+    assert _st("semshare_match", FAKE, 4, FAKE, 4, 5, FAKE, None, None) == b.E_INVAL
+    assert _st("semshare_match", FAKE, 4, FAKE, 0, 2, FAKE, None, None) == b.E_INVAL  # empty reference
+    assert _st("semshare_match", FAKE, 4, FAKE, 1 << 23, 2, FAKE, None, None) == b.E_UNSUPPORTED
+    assert _st("semshare_match", FAKE, 4, FAKE, 4, 2, None, None, None) == b.E_INVAL  # null idx
+    assert _st("semshare_match", None, 0, None, 4, 2, None, None, None) == b.OK
+
+
+def test_gather_validation(lib):
+    args = dict(n_tgt=4, n_ref=4, L=2, h=8, d=128, dt=1)
+    assert _st("semshare_gather_kv", FAKE, FAKE, FAKE, 4, 4, FAKE, None, 2, 8, 128, 1, None) == b.E_INVAL  # v pair
+    assert _st("semshare_gather_kv", FAKE, None, FAKE, 4, 4, FAKE, None, 2, 1, 3, 1, None) == b.E_UNSUPPORTED  # 6 B rows
+    assert _st("semshare_gather_kv", FAKE_ODD, None, FAKE, 4, 4, FAKE, None, 2, 8, 128, 1, None) == b.E_INVAL
+    assert _st("semshare_gather_kv", FAKE, None, None, 4, 4, FAKE, None, 2, 8, 128, 1, None) == b.E_INVAL
+    assert _st("semshare_gather_kv", FAKE, None, FAKE, 0, 4, FAKE, None, 2, 8, 128, 1, None) == b.OK
+    assert _st("semshare_gather_kv", FAKE, None, FAKE, 4, 4, FAKE, None, 0, 8, 128, 1, None) == b.OK
+    del args
+
+
+def _pp(n_sel=8, n_tok=16, hidden=256, hq=8, hkv=2, d=128, base=1e4, scale=0.0, out=FAKE, dev=None,
+        ws=FAKE, ws_bytes=1 << 30, dt=1, xsel=FAKE, pos=FAKE, wq=FAKE):
+    return _st("semshare_partial_prefill", xsel, pos, n_sel, wq, FAKE, FAKE, FAKE, FAKE, n_tok, hidden, hq, hkv, d,
+               base, scale, out, dev, ws, ws_bytes, dt, None)
+
+
+def test_partial_prefill_validation(lib):
+    assert _pp(n_sel=17, n_tok=16) == b.E_INVAL  # n_sel > n_tok
+    assert _pp(hq=6, hkv=4) == b.E_INVAL  # heads not divisible
+    assert _pp(d=96) == b.E_UNSUPPORTED  # bf16 head_dim
+    assert _pp(d=7) == b.E_INVAL  # odd head_dim
+    assert _pp(hidden=100) == b.E_UNSUPPORTED
+    assert _pp(hq=3 * 2, hkv=2) == b.E_UNSUPPORTED  # G = 3 does not divide 128
+    assert _pp(hkv=1, hq=1, d=64) == b.E_UNSUPPORTED  # kv row of 64 is not a 128-column tile
+    assert _pp(d=256, dt=0) == b.E_UNSUPPORTED  # fp32 head_dim limit
+    assert _pp(n_tok=9000, n_sel=8, dt=0) == b.E_UNSUPPORTED
+    assert _pp(base=0.0) == b.E_INVAL
+    assert _pp(scale=-1.0) == b.E_INVAL
+    assert _pp(ws_bytes=16) == b.E_INVAL and "workspace" in ss.last_error()
+    assert _pp(ws=FAKE + 16) == b.E_INVAL  # workspace alignment
+    assert _pp(wq=None) == b.E_INVAL  # out requested without wq
+    assert _pp(xsel=FAKE_ODD) == b.E_INVAL
+    assert _pp(pos=None) == b.E_INVAL
+    assert _pp(n_sel=0, xsel=None, pos=None) == b.OK
+
+
+def test_partial_prefill_workspace_sizes(lib):
+    W = ss.load().semshare_partial_prefill_workspace
+    assert W(8, 16, 256, 8, 2, 128, 7) == 0 and W(8, 16, 256, 6, 4, 128, 1) == 0
+    small = W(256, 1024, 4096, 32, 8, 128, 1)
+    # q (256*32*128*2) + rope table + deviation + split-KV partials
+    assert small >= 256 * 4096 * 2 + 256 * 64 * 8
+    full = W(5120, 5120, 4096, 32, 8, 128, 1)
+    assert full >= 5120 * 4096 * 2
+    assert W(1280, 5120, 4096, 32, 8, 128, 1) > W(1280, 5120, 4096, 32, 8, 128, 1) - 1
+
+
+def test_select_validation(lib):
+    assert _st("semshare_select_recompute", FAKE, 10, 11, FAKE, None) == b.E_INVAL
+    assert _st("semshare_select_recompute", FAKE, (1 << 20) + 1, 5, FAKE, None) == b.E_UNSUPPORTED
+    assert _st("semshare_select_recompute", FAKE, 10, 0, None, None) == b.OK
+
+
+def test_binding_requires_device_tensors():
+    import torch
+    x = torch.zeros(4, 8)
+    with pytest.raises(ValueError):
+        ss.rope_embed(x)
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(b, "_lib", None)
+    monkeypatch.setattr(b, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        b.load()
+
+
+def test_product_package_never_imports_the_oracle():
+    pkg = os.path.dirname(b.__file__)
+    for root, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(root, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text and "orc_" not in text, f

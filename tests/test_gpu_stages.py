@@ -1,0 +1,200 @@
+"""GPU parity of the RoPE, LSH, match, gather and select kernels against the
+oracle, each stage fed the oracle's (or the generator's) inputs.  Integer
+results are compared bit for bit; floating-point results within the
+tolerances derived in the design notes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import paper_2509_24832_amd as ss
+import workloads
+from workloads import CONFIGS
+
+from helpers import (announce, bf16_ulp, bf16_ulp_distance, code_mismatch_ok, dev, dev_codes, dev_i32, host,
+                     host_codes)
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------------- RoPE
+
+@pytest.mark.parametrize("cid,n_tok,dim,pos0", [
+    (0, 512, 256, 0),          # tiny fp32 config
+    (0, 37, 6, 3),             # ragged: width not a multiple of 8 (scalar path)
+    (1, 1024, 4096, 0),        # one Llama-3-8B-shaped prompt
+    (1, 64, 4096, 32700),      # positions near 32k: fp64 angle reduction matters
+    (1, 5, 10, 0),             # tiny bf16, scalar path
+])
+def test_rope_embed_matches_oracle(cid, n_tok, dim, pos0):
+    cfg = CONFIGS[cid]
+    announce(f"rope cfg{cid} n_tok={n_tok} dim={dim} pos0={pos0}")
+    x = workloads.make_rows(cfg, n_tok, dim, tag=1)
+    y = host(ss.rope_embed(dev(x, cfg.dtype), pos0=pos0))
+    # fp32 rotation error: sin/cos within ~1 ulp plus two roundings, <= 4e-7 (|x0| + |x1|)
+    scale = np.abs(x[:, 0::2]).repeat(2, axis=1) + np.abs(x[:, 1::2]).repeat(2, axis=1)
+    ref = orc.rope_embed(x, pos0=pos0, dtype=cfg.dtype)
+    err = np.abs(y - ref)
+    if cfg.dtype == "bf16":
+        # both sides round once to bf16: at most one bf16 spacing apart beyond the fp32 error
+        assert np.all(err <= bf16_ulp(ref) + 4e-7 * scale)
+        assert (bf16_ulp_distance(y, ref) > 0).mean() < 1e-3
+    else:
+        assert np.all(err <= 4e-7 * scale + 1e-30)
+
+
+def test_rope_embed_in_place_and_identity_at_zero():
+    cfg = CONFIGS[1]
+    x = workloads.make_rows(cfg, 16, 128, tag=2)
+    t = dev(x, "bf16")
+    announce("rope in place")
+    ss.rope_embed(t, out=t, pos0=0)
+    # row 0 sits at position 0: unchanged; others match the oracle
+    y = host(t)
+    assert np.array_equal(y[0], x[0])
+    ref = orc.rope_embed(x, dtype="bf16")
+    scale = np.abs(x[:, 0::2]).repeat(2, axis=1) + np.abs(x[:, 1::2]).repeat(2, axis=1)
+    assert np.all(np.abs(y - ref) <= bf16_ulp(ref) + 4e-7 * scale)
+
+
+# ----------------------------------------------------------------------- LSH
+
+@pytest.mark.parametrize("cid,n_tok,dim,n_bits", [
+    (0, 512, 256, 64),
+    (0, 77, 132, 128),        # ragged rows, fp32 dim not a multiple of 64
+    (1, 1024, 4096, 128),
+    (1, 1000, 4096, 64),      # ragged (not a multiple of 32 rows)
+    (3, 300, 4096, 256),      # bank code length
+    (1, 33, 64, 128),         # single K chunk
+])
+def test_lsh_encode_matches_oracle(cid, n_tok, dim, n_bits):
+    cfg = CONFIGS[cid]
+    announce(f"lsh cfg{cid} n_tok={n_tok} dim={dim} n_bits={n_bits}")
+    # fed the oracle's RoPE output, as the path does
+    x = orc.rope_embed(workloads.make_rows(cfg, n_tok, dim, tag=3), dtype=cfg.dtype).astype(np.float32)
+    planes = workloads.make_planes(cfg, n_bits=n_bits, dim=dim)
+    codes = host_codes(ss.lsh_encode(dev(x, cfg.dtype), dev(planes, cfg.dtype)))
+    ref = orc.lsh_encode(x, planes)
+    proj = orc.lsh_project(x, planes)
+    flips, outside = code_mismatch_ok(codes, ref, proj, x.astype(np.float64), planes.astype(np.float64))
+    assert outside == 0, f"{flips} flips, {outside} outside the 1e-5 band"
+    assert flips <= max(2, n_tok * n_bits // 20000)
+
+
+def test_lsh_zero_rows_give_zero_codes():
+    cfg = CONFIGS[1]
+    x = np.zeros((40, 128), np.float32)
+    planes = workloads.make_planes(cfg, n_bits=128, dim=128)
+    announce("lsh zero rows")
+    assert not host_codes(ss.lsh_encode(dev(x, "bf16"), dev(planes, "bf16"))).any()
+
+
+# --------------------------------------------------------------------- match
+
+@pytest.mark.parametrize("n_tgt,n_ref,n_words", [
+    (512, 512, 1),
+    (1024, 1024, 2),
+    (1000, 777, 2),       # ragged both ways
+    (130, 1, 2),          # single reference
+    (5, 70000, 4),        # many splits, tiny target
+    (4096, 4096, 4),
+    (300, 2048, 3),
+])
+def test_match_matches_oracle(n_tgt, n_ref, n_words):
+    cfg = CONFIGS[1]
+    announce(f"match n_tgt={n_tgt} n_ref={n_ref} W={n_words}")
+    tgt = workloads.make_codes(cfg, n_tgt, n_words, tag=n_tgt)
+    ref = workloads.make_codes(cfg, n_ref, n_words, tag=n_ref + 1)
+    # plant exact and near matches plus duplicates so ties are exercised
+    k = min(n_tgt, n_ref) // 3
+    ref[:k] = tgt[:k]
+    if n_ref > 2 * k + 1 and k:
+        ref[k:2 * k] = tgt[:k]  # duplicates at higher indices: lowest index must win
+    idx, dist = ss.match(dev_codes(tgt), dev_codes(ref))
+    ri, rd = orc.match(tgt, ref)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), ri)
+    assert np.array_equal(dist.cpu().numpy(), rd)
+
+
+def test_match_bank_shape():
+    # one 4096-token target against 16 references of 4096 tokens (256-bit codes)
+    cfg = CONFIGS[3]
+    announce("match bank 4096 x 65536 W=4")
+    tgt = workloads.make_codes(cfg, 4096, 4, tag=11)
+    ref = workloads.make_codes(cfg, 16 * 4096, 4, tag=12)
+    ref[5 * 4096 + np.arange(0, 4096, 7)] = tgt[np.arange(0, 4096, 7)]
+    idx, dist = ss.match(dev_codes(tgt), dev_codes(ref))
+    ri, rd = orc.match(tgt, ref)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), ri) and np.array_equal(dist.cpu().numpy(), rd)
+
+
+def test_match_identical_prompts_self_match_and_no_dist():
+    cfg = CONFIGS[2]
+    c = workloads.make_codes(cfg, 5120, 2, tag=3)
+    announce("match identical 5120")
+    idx, dist = ss.match(dev_codes(c), dev_codes(c), want_dist=False)
+    assert dist is None
+    assert np.array_equal(idx.cpu().numpy(), np.arange(5120))
+
+
+def test_match_complement_distance():
+    cfg = CONFIGS[1]
+    c = workloads.make_codes(cfg, 64, 2, tag=4)
+    announce("match complement")
+    idx, dist = ss.match(dev_codes(c[:1]), dev_codes(~c[:1]))
+    assert dist.cpu().numpy()[0] == 128 and idx.cpu().numpy()[0] == 0
+
+
+# -------------------------------------------------------------------- gather
+
+@pytest.mark.parametrize("cid,L,n_ref,n_tgt", [(0, 2, 512, 512), (1, 3, 1024, 1000), (2, 2, 5120, 5120)])
+def test_gather_kv_bitwise(cid, L, n_ref, n_tgt):
+    cfg = CONFIGS[cid]
+    announce(f"gather cfg{cid} L={L} n_ref={n_ref} n_tgt={n_tgt}")
+    k, v = workloads.make_cache(cfg, L, n_ref, tag=cid)
+    idx = np.random.default_rng(cid).integers(0, n_ref, n_tgt).astype(np.int32)
+    ok, ov = ss.gather_kv(dev(k, cfg.dtype), dev(v, cfg.dtype), dev_i32(idx))
+    assert np.array_equal(host(ok), orc.gather_rows(k, idx))
+    assert np.array_equal(host(ov), orc.gather_rows(v, idx))
+
+
+def test_gather_identity_k_only_and_out_of_range():
+    cfg = CONFIGS[1]
+    k, _ = workloads.make_cache(cfg, 2, 64, tag=5)
+    announce("gather identity / k-only / out of range")
+    tk = dev(k, "bf16")
+    ok, ov = ss.gather_kv(tk, None, dev_i32(np.arange(64)))
+    assert ov is None and np.array_equal(host(ok), k)
+    idx = np.array([0, -1, 63, 64, 1 << 30, 5], np.int32)
+    ok, _ = ss.gather_kv(tk, None, dev_i32(idx))
+    got = host(ok)
+    for t, j in enumerate(idx):
+        exp = k[:, j] if 0 <= j < 64 else np.zeros_like(k[:, 0])
+        assert np.array_equal(got[:, t], exp)
+
+
+def test_gather_rows_wide():
+    cfg = CONFIGS[1]
+    x = workloads.make_rows(cfg, 300, 4096, tag=6)  # 8 KB rows
+    idx = np.random.default_rng(6).integers(0, 300, 111).astype(np.int32)
+    announce("gather rows 8KB")
+    assert np.array_equal(host(ss.gather_rows(dev(x, "bf16"), dev_i32(idx))), x[idx])
+
+
+# -------------------------------------------------------------------- select
+
+@pytest.mark.parametrize("n_tok,n_sel,levels", [
+    (5120, 1280, 0), (5120, 512, 0), (5120, 2560, 7), (300, 300, 0), (300, 1, 3), (1000, 999, 2),
+    (32768, 3277, 50), (17, 5, 1),
+])
+def test_select_recompute_matches_oracle(n_tok, n_sel, levels):
+    rng = np.random.default_rng(n_tok + n_sel)
+    if levels:
+        sigma = rng.integers(0, levels, n_tok).astype(np.float32)  # many ties
+    else:
+        sigma = (rng.random(n_tok) * 50).astype(np.float32)
+    announce(f"select n_tok={n_tok} n_sel={n_sel} levels={levels}")
+    got = ss.select_recompute(torch.from_numpy(sigma).cuda(), n_sel).cpu().numpy()
+    assert np.array_equal(got, orc.select_recompute(sigma, n_sel))
