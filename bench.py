@@ -1,0 +1,325 @@
+#!/usr/bin/env python3
+"""Benchmark of the SemShareKV hot path on one MI355X.
+
+One step = one pass of the whole path for one 5120-token target prompt against
+a cached 5120-token reference prompt, Llama-3-8B attention shape (32 layers,
+hidden 4096, 32 query / 8 kv heads, head_dim 128), bf16:
+  RoPE-embed of the target embeddings -> 128-bit sign LSH -> top-1 Hamming
+  match against the reference codes -> gather of the matched reference K/V
+  rows for all 32 layers -> layer 0: full recompute with KV deviation ->
+  high-deviation token selection (recompute fraction f) -> layers 1..31:
+  partial prefill of the selected tokens over the assembled cache.
+The reference side (its RoPE/LSH codes and its own K/V cache) is prepared
+once before timing, as at cache-insert time.  Inputs are seeded synthetic
+data resident in HBM before the timed region starts.
+
+    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--frac 0.25]
+
+Prints one JSON line (see the keys below).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--frac", type=float, default=0.25, help="recompute fraction of the headline line")
+    ap.add_argument("--sweep", default="0.10,0.25,0.50", help="recompute fractions also timed ('' to skip)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
+    return ap.parse_args()
+
+
+class Path:
+    """Device buffers and the step of the hot path (config: 32 Llama-3-8B-shaped layers, 5k tokens)."""
+
+    def __init__(self, torch, ss, cfg):
+        import numpy as np
+
+        import workloads
+        self.torch, self.ss, self.cfg = torch, ss, cfg
+        dev = "cuda"
+        bf = torch.bfloat16
+        T, d, L = cfg.n_tok, cfg.dim, cfg.n_layers
+        hq, hkv, D = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+        self.T, self.d, self.L, self.hq, self.hkv, self.D = T, d, L, hq, hkv, D
+
+        def up(a):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev).to(bf).contiguous()
+
+        pair = workloads.make_prompt_pair(cfg)
+        self.e_ref = up(pair.e_ref)
+        self.e_tgt = up(pair.e_tgt)
+        self.planes = up(workloads.make_planes(cfg))
+        # per-layer Wq/Wk/Wv ~ N(0, 0.02), drawn on the device from a seeded generator
+        g = torch.Generator(device=dev)
+        self.w = []
+        for l in range(L):
+            g.manual_seed(1000 * (cfg.cid + 1) + l)
+            wq = (torch.randn((hq * D, d), generator=g, device=dev) * 0.02).to(bf)
+            wk = (torch.randn((hkv * D, d), generator=g, device=dev) * 0.02).to(bf)
+            wv = (torch.randn((hkv * D, d), generator=g, device=dev) * 0.02).to(bf)
+            self.w.append((wq, wk, wv))
+        # reference side, prepared once (insert time): codes and its own K/V cache
+        self.allpos = torch.arange(T, dtype=torch.int32, device=dev)
+        e_ref_rot = ss.rope_embed(self.e_ref)
+        self.codes_ref = ss.lsh_encode(e_ref_rot, self.planes)
+        self.ref_k = torch.zeros((L, T, hkv, D), dtype=bf, device=dev)
+        self.ref_v = torch.zeros_like(self.ref_k)
+        for l in range(L):
+            ss.qkv_rope(self.e_ref, self.allpos, None, self.w[l][1], self.w[l][2], self.ref_k[l], self.ref_v[l], hq,
+                        hkv, want_q=False)
+        # target-side buffers
+        self.e_rot = torch.empty_like(self.e_tgt)
+        self.codes_t = torch.empty_like(self.codes_ref)
+        self.idx = torch.empty(T, dtype=torch.int32, device=dev)
+        self.dist = torch.empty(T, dtype=torch.int32, device=dev)
+        self.asm_k = torch.empty_like(self.ref_k)
+        self.asm_v = torch.empty_like(self.ref_v)
+        self.q_full = torch.empty((T, hq, D), dtype=bf, device=dev)
+        self.out_full = torch.empty_like(self.q_full)
+        self.sigma = torch.empty(T, dtype=torch.float32, device=dev)
+        ws = max(ss.qkv_rope_workspace_bytes(T, hkv, D, bf),
+                 ss.prefill_attention_workspace_bytes(T, T, hq, hkv, D, bf))
+        self.set_frac(0.25, ws_hint=ws)
+
+    def set_frac(self, frac, ws_hint=0):
+        torch, ss = self.torch, self.ss
+        bf = torch.bfloat16
+        self.frac = frac
+        self.n_sel = self.cfg.n_sel(frac)
+        n = self.n_sel
+        self.sel = torch.empty(n, dtype=torch.int32, device="cuda")
+        self.x_sel = torch.empty((n, self.d), dtype=bf, device="cuda")
+        self.q_sel = torch.empty((n, self.hq, self.D), dtype=bf, device="cuda")
+        self.out_sel = torch.empty_like(self.q_sel)
+        need = max(ws_hint,
+                   ss.qkv_rope_workspace_bytes(self.T, self.hkv, self.D, bf),
+                   ss.prefill_attention_workspace_bytes(self.T, self.T, self.hq, self.hkv, self.D, bf),
+                   ss.prefill_attention_workspace_bytes(n, self.T, self.hq, self.hkv, self.D, bf))
+        self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+
+    def step(self, mark=None):
+        """One pass of the hot path.  mark(name) records a boundary event when given."""
+        ss = self.ss
+        m = mark or (lambda name: None)
+        hq, hkv = self.hq, self.hkv
+        m("start")
+        ss.rope_embed(self.e_tgt, out=self.e_rot)
+        m("rope")
+        ss.lsh_encode(self.e_rot, self.planes, out=self.codes_t)
+        m("lsh")
+        ss.match(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
+        m("match")
+        ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
+        m("gather")
+        wq, wk, wv = self.w[0]
+        ss.qkv_rope(self.e_tgt, self.allpos, wq, wk, wv, self.asm_k[0], self.asm_v[0], hq, hkv, q_out=self.q_full,
+                    deviation=self.sigma, want_deviation=True, workspace=self.ws)
+        m("qkv0")
+        ss.prefill_attention(self.q_full, self.allpos, self.asm_k[0], self.asm_v[0], hkv, out=self.out_full,
+                             workspace=self.ws)
+        m("attn0")
+        ss.select_recompute(self.sigma, self.n_sel, out=self.sel)
+        m("select")
+        ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
+        m("xsel")
+        for l in range(1, self.L):
+            wq, wk, wv = self.w[l]
+            ss.qkv_rope(self.x_sel, self.sel, wq, wk, wv, self.asm_k[l], self.asm_v[l], hq, hkv, q_out=self.q_sel,
+                        workspace=self.ws)
+            m("qkv")
+            ss.prefill_attention(self.q_sel, self.sel, self.asm_k[l], self.asm_v[l], hkv, out=self.out_sel,
+                                 workspace=self.ws)
+            m("attn")
+
+
+def time_steps(torch, path, steps, warmup, instrument):
+    """Times `steps` steps after `warmup` untimed ones.  With instrument, a
+    HIP event pair brackets every call (on the stream the kernels run on) and
+    per-stage durations are returned as well."""
+    for _ in range(warmup):
+        path.step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    marks = []
+
+    def mark(name):
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record(stream)
+        marks.append((name, ev))
+
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for _ in range(steps):
+        path.step(mark if instrument else None)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_time(t1)
+    stages = {}
+    if instrument:
+        for (_, a), (name, b) in zip(marks[:-1], marks[1:]):
+            if name == "start":
+                continue
+            stages.setdefault(name, []).append(a.elapsed_time(b))
+    return total_ms / steps, wall / steps * 1e3, stages
+
+
+def attention_flops(sel_pos, hq, D):
+    """4 * D * Hq * sum_s (p_s + 1): QK^T and PV multiply-adds of causal attention."""
+    return 4.0 * D * hq * float((sel_pos.astype("float64") + 1.0).sum())
+
+
+def cpu_baseline(cfg, frac, budget_s):
+    """The oracle, as it stands, on a bounded sample of one step: each stage is
+    run on a slice of its rows and scaled by work to the full step."""
+    import numpy as np
+
+    import oracle as orc
+    import workloads
+    T, d, L, hq, hkv, D = cfg.n_tok, cfg.dim, cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    n_sel = cfg.n_sel(frac)
+    rng = np.random.default_rng(0)
+    pair = workloads.make_prompt_pair(cfg)
+    planes = workloads.make_planes(cfg)
+    w = workloads.make_weights(cfg, 0)
+    k, v = workloads.make_cache(cfg, 1, T)
+    k, v = k[0].reshape(T, -1), v[0].reshape(T, -1)
+    sel = workloads.make_sel_pos(cfg, T, n_sel)
+    est = {}
+    # sample sizes chosen so the whole sample costs about budget_s on 16 threads
+    scale = max(budget_s / 15.0, 0.05)
+    nr = max(16, int(256 * scale))
+    t = time.perf_counter(); e = orc.rope_embed(pair.e_tgt[:nr], dtype="bf16"); est["rope"] = (time.perf_counter() - t) * T / nr
+    t = time.perf_counter(); c = orc.lsh_encode(e, planes); est["lsh"] = (time.perf_counter() - t) * T / nr
+    cr = orc.lsh_encode(orc.rope_embed(pair.e_ref[:nr], dtype="bf16"), planes)
+    codes_ref = np.tile(cr, (T // nr + 1, 1))[:T]
+    t = time.perf_counter(); orc.match(c, codes_ref); est["match"] = (time.perf_counter() - t) * T / nr
+    idx = rng.integers(0, T, T).astype(np.int32)
+    rows16 = rng.integers(0, 2**16, size=(1, T, hkv * D), dtype=np.uint16)  # one layer's K, bf16 bit patterns
+    t = time.perf_counter(); orc.gather_rows(rows16, idx); est["gather"] = (time.perf_counter() - t) * 2 * L
+    nq = max(4, int(16 * scale))
+    rows = np.sort(rng.choice(n_sel, nq, replace=False))
+    t = time.perf_counter()
+    orc.qkv_rows(pair.e_tgt[sel[rows]], sel[rows], w.wq, w.wk, w.wv, hq, hkv, D, dtype="bf16")
+    per_row_qkv = (time.perf_counter() - t) / nq
+    q, _, _ = orc.qkv_rows(pair.e_tgt[sel[rows]], sel[rows], w.wq, w.wk, w.wv, hq, hkv, D, dtype="bf16", want_kv=False)
+    t = time.perf_counter()
+    orc.attention_rows(q, sel[rows], k, v, hq, hkv, D, dtype="bf16")
+    per_key_attn = (time.perf_counter() - t) / float((sel[rows] + 1).sum())
+    est["qkv0"] = per_row_qkv * T
+    est["attn0"] = per_key_attn * T * (T + 1) / 2
+    est["select"] = 0.0
+    est["qkv"] = per_row_qkv * n_sel * (L - 1)
+    est["attn"] = per_key_attn * float((sel + 1).sum()) * (L - 1)
+    total = sum(est.values())
+    sample = (f"oracle on {nr} of {T} rows for RoPE/LSH/match, 1 of {2 * L} gathered layer tensors, {nq} selected "
+              f"rows for QKV and attention; each stage scaled by its work to one full step (f={frac}), extrapolated")
+    return {"value": T / total, "unit": "tokens/s", "cores": orc.num_threads(), "kind": "oracle", "sample": sample,
+            "est_step_s": total, "est_stage_s": {k2: round(v2, 3) for k2, v2 in est.items()}}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: every box here has one GPU and "
+              "this build has no multi-GPU path (see the sharding notes in DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2509_24832_amd as ss
+    from workloads import CONFIGS
+
+    torch.cuda.set_device(0)
+    cfg = CONFIGS[2]
+    path = Path(torch, ss, cfg)
+
+    # headline: plain timed region
+    path.set_frac(args.frac)
+    ms, wall_ms, _ = time_steps(torch, path, args.steps, args.warmup, instrument=False)
+    # per-call durations: the same steps with an event pair around every call
+    ms_i, _, stages = time_steps(torch, path, args.steps, 1, instrument=True)
+    sel_h = path.sel.cpu().numpy()
+    T, L, hq, hkv, D, d = path.T, path.L, path.hq, path.hkv, path.D, path.d
+    n_sel = path.n_sel
+
+    def avg(name):
+        v = stages.get(name, [])
+        return sum(v) / len(v) if v else float("nan")
+
+    attn_flops = attention_flops(sel_h, hq, D)
+    qkv_flops = 2.0 * n_sel * (hq + 2 * hkv) * D * d
+    attn_ms, qkv_ms = avg("attn"), avg("qkv")
+    gather_bytes = 2.0 * 2 * L * T * hkv * D * 2  # read + write, K and V
+    gather_ms = avg("gather")
+    match_ms = avg("match")
+    pp_ms = (avg("qkv0") + avg("attn0") + (L - 1) * (attn_ms + qkv_ms))
+    units = {
+        "attention": ("mfma", attn_flops / (attn_ms * 1e-3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s", attn_ms),
+        "qkv_gemm": ("mfma", qkv_flops / (qkv_ms * 1e-3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s", qkv_ms),
+    }
+    dom = max(units, key=lambda k: units[k][4])
+    bound, achieved, peak, unit, dur = units[dom]
+    res = {
+        "metric": "partial-prefill tokens/s + LSH match token-pairs/s at 5k tokens, Llama-3-8B shape",
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"5120-token target vs 5120-token cached reference, 32 Llama-3-8B-shaped attention "
+                               f"layers (hidden 4096, 32q/8kv heads, head_dim 128), 128-bit LSH, recompute "
+                               f"fraction {args.frac}", "n_tok": T, "layers": L, "recompute_frac": args.frac,
+                   "n_recompute": n_sel},
+        "partial_prefill_tokens_per_s": T / (pp_ms * 1e-3),
+        "match_token_pairs_per_s": T * T / (match_ms * 1e-3),
+        "stage_ms": {k: round(sum(v) / len(v), 4) for k, v in stages.items()},
+        "instrumented_ms_per_step": ms_i,
+        "wall_ms_per_step": wall_ms,
+        "gather": {"GB/s": gather_bytes / (gather_ms * 1e-3) / 1e9, "frac_of_hbm": gather_bytes / (gather_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS},
+        "attention_TFLOPs": units["attention"][1],
+        "qkv_gemm_TFLOPs": units["qkv_gemm"][1],
+        "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": None},
+    }
+    if args.sweep:
+        sweep = {}
+        for f in [float(x) for x in args.sweep.split(",") if x]:
+            path.set_frac(f)
+            m_f, _, _ = time_steps(torch, path, max(3, args.steps // 2), 2, instrument=False)
+            sweep[f"{f:.2f}"] = {"ms_per_step": m_f, "tokens_per_s": T / (m_f * 1e-3)}
+        res["recompute_sweep"] = sweep
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, args.frac, args.cpu_budget_s)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -122,7 +122,8 @@ semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const
  *  2. If deviation_out != NULL: deviation_out[i] = ||K_cache[p] - k||_2 +
  *     ||V_cache[p] - v||_2 over the row's n_kv_heads*head_dim entries, against
  *     the row held before step 3 (KV deviation, Appendix A.4), with k and v
- *     as rounded to dtype.
+ *     as rounded to dtype.  The sums are formed in a fixed order, so the
+ *     result is reproducible bit for bit.
  *  3. Cache rows sel_pos[i] are overwritten with k (post-RoPE) and v.
  *  4. If out != NULL: for every selected row and query head h,
  *     out = softmax_{j <= p}(q_h . K[j][h/G] * sm_scale) V[j][h/G] over the
@@ -157,6 +158,47 @@ semshare_status_t semshare_partial_prefill(
 size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t hidden,
                                           int32_t n_q_heads, int32_t n_kv_heads,
                                           int32_t head_dim, semshare_dtype_t dtype);
+
+/*
+ * Step 1 of semshare_partial_prefill on its own (same kernels): steps 1-3
+ * above -- projection, RoPE, deviation and the scatter of k/v into the
+ * cache rows sel_pos -- writing the RoPE'd q to q_out instead of attending.
+ *   q_out      [n_sel][n_q_heads][head_dim] dtype, or NULL (K/V only; wq may
+ *              then be NULL too).
+ *   workspace  at least semshare_qkv_rope_workspace() bytes, 256-byte
+ *              aligned (may be NULL when that size is 0).
+ *   Other arguments and limits as for semshare_partial_prefill.
+ */
+semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, int64_t n_sel,
+                                    const void* wq, const void* wk, const void* wv, void* k_cache,
+                                    void* v_cache, int64_t n_tok, int32_t hidden, int32_t n_q_heads,
+                                    int32_t n_kv_heads, int32_t head_dim, double rope_base,
+                                    void* q_out, float* deviation_out, void* workspace,
+                                    size_t workspace_bytes, semshare_dtype_t dtype, void* stream);
+size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim,
+                                   semshare_dtype_t dtype);
+
+/*
+ * Step 2 of semshare_partial_prefill on its own (same kernels): causal
+ * grouped-query attention of the selected rows over the cache (step 4
+ * above), for q as semshare_qkv_rope writes it.  Keys j <= sel_pos[i] of kv
+ * head h / G are attended; rows with a position outside [0, n_tok) are not
+ * written.
+ *   q          [n_sel][n_q_heads][head_dim] dtype (RoPE'd)
+ *   out        [n_sel][n_q_heads][head_dim] dtype
+ *   workspace  at least semshare_prefill_attention_workspace() bytes,
+ *              256-byte aligned (split-KV partial results; may be NULL when
+ *              that size is 0).
+ */
+semshare_status_t semshare_prefill_attention(const void* q, const int32_t* sel_pos, int64_t n_sel,
+                                             const void* k_cache, const void* v_cache,
+                                             int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                                             int32_t head_dim, float sm_scale, void* out,
+                                             void* workspace, size_t workspace_bytes,
+                                             semshare_dtype_t dtype, void* stream);
+size_t semshare_prefill_attention_workspace(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
+                                            int32_t n_kv_heads, int32_t head_dim,
+                                            semshare_dtype_t dtype);
 
 /*
  * High-deviation token selection (Section 3 Insight 1; Section 4.2): the

@@ -5,5 +5,6 @@ include/semshare.h); ``semshare`` is its thin ctypes binding.
 """
 from .semshare import (  # noqa: F401
     BF16, FP32, SemShareError, declared_symbols, gather_kv, gather_rows, last_error, load, lsh_encode, match,
-    partial_prefill, partial_prefill_workspace_bytes, rope_embed, select_recompute, version,
+    partial_prefill, partial_prefill_workspace_bytes, prefill_attention, prefill_attention_workspace_bytes,
+    qkv_rope, qkv_rope_workspace_bytes, rope_embed, select_recompute, version,
 )

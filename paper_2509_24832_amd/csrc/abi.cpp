@@ -114,35 +114,26 @@ semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const
                     "gather_kv launch");
 }
 
-size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t hidden,
-                                          int32_t n_q_heads, int32_t n_kv_heads,
-                                          int32_t head_dim, semshare_dtype_t dtype) {
-    if (!dtype_ok(dtype) || n_sel < 0 || n_tok < 0 || hidden <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 ||
-        head_dim <= 0 || n_q_heads % n_kv_heads)
-        return 0;
-    return semshare::plan_partial_prefill(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
-}
+}  // extern "C"
 
-semshare_status_t semshare_partial_prefill(
-    const void* x_sel, const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
-    const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
-    int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base, float sm_scale,
-    void* out, float* deviation_out, void* workspace, size_t workspace_bytes,
-    semshare_dtype_t dtype, void* stream) {
-    const char* fn = "partial_prefill";
+namespace {
+
+// Shape checks shared by the partial-prefill calls.  Returns SEMSHARE_OK or
+// the failing status (message already set).
+semshare_status_t check_prefill_shapes(const char* fn, int64_t n_sel, int64_t n_tok, int32_t hidden,
+                                       int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                       semshare_dtype_t dtype, bool need_hidden) {
     if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "%s: unknown dtype %d", fn, dtype);
     if (n_sel < 0 || n_tok < 0) return fail(SEMSHARE_E_INVAL, "%s: negative size", fn);
     if (n_sel > n_tok) return fail(SEMSHARE_E_INVAL, "%s: n_sel (%lld) > n_tok (%lld)", fn, (long long)n_sel, (long long)n_tok);
-    if (hidden <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0)
+    if ((need_hidden && hidden <= 0) || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0)
         return fail(SEMSHARE_E_INVAL, "%s: sizes must be > 0", fn);
     if (n_q_heads % n_kv_heads) return fail(SEMSHARE_E_INVAL, "%s: n_q_heads %% n_kv_heads != 0", fn);
     if (head_dim & 1) return fail(SEMSHARE_E_INVAL, "%s: head_dim must be even", fn);
-    if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
-    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", fn);
     if (n_tok > (int64_t(1) << 30) || (int64_t)n_kv_heads * head_dim * n_tok > (int64_t(1) << 40))
         return fail(SEMSHARE_E_UNSUPPORTED, "%s: cache too large", fn);
     const int32_t G = n_q_heads / n_kv_heads;
-    if (hidden % 64) return fail(SEMSHARE_E_UNSUPPORTED, "%s: hidden %% 64 != 0", fn);
+    if (need_hidden && hidden % 64) return fail(SEMSHARE_E_UNSUPPORTED, "%s: hidden %% 64 != 0", fn);
     if (dtype == SEMSHARE_BF16) {
         if (head_dim != 128 && head_dim != 64)
             return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 supports head_dim 64 or 128 (got %d)", fn, head_dim);
@@ -153,25 +144,142 @@ semshare_status_t semshare_partial_prefill(
         if (head_dim > 128) return fail(SEMSHARE_E_UNSUPPORTED, "%s: fp32 supports head_dim <= 128", fn);
         if (n_tok > 8192) return fail(SEMSHARE_E_UNSUPPORTED, "%s: fp32 path supports n_tok <= 8192", fn);
     }
+    return SEMSHARE_OK;
+}
+
+struct PrefillLayout {
+    size_t off_q, off_qkv, off_attn, total;
+};
+
+PrefillLayout prefill_layout(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                             int32_t head_dim, semshare_dtype_t dtype) {
+    auto a256 = [](size_t x) { return (x + 255) & ~size_t(255); };
+    PrefillLayout l{};
+    l.off_q = 0;
+    l.off_qkv = a256((size_t)n_sel * n_q_heads * head_dim * dtype_size(dtype));
+    l.off_attn = l.off_qkv + semshare::qkv_workspace_bytes(n_sel, n_kv_heads, head_dim, dtype);
+    l.total = l.off_attn + semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
+    return l;
+}
+
+semshare_status_t check_workspace(const char* fn, const void* ws, size_t have, size_t need) {
+    if (need == 0) return SEMSHARE_OK;
+    if (!ws || have < need)
+        return fail(SEMSHARE_E_INVAL, "%s: workspace of %zu bytes is smaller than the %zu required", fn, have, need);
+    if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(SEMSHARE_E_INVAL, "%s: workspace not 256-byte aligned", fn);
+    return SEMSHARE_OK;
+}
+
+float default_scale(float sm_scale, int32_t head_dim) {
+    return sm_scale > 0.0f ? sm_scale : (float)(1.0 / std::sqrt((double)head_dim));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim, semshare_dtype_t dtype) {
+    if (!dtype_ok(dtype) || n_sel < 0 || n_kv_heads <= 0 || head_dim <= 0) return 0;
+    return semshare::qkv_workspace_bytes(n_sel, n_kv_heads, head_dim, dtype);
+}
+
+size_t semshare_prefill_attention_workspace(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
+                                            int32_t n_kv_heads, int32_t head_dim, semshare_dtype_t dtype) {
+    if (!dtype_ok(dtype) || n_sel < 0 || n_tok < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0 ||
+        n_q_heads % n_kv_heads)
+        return 0;
+    return semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
+}
+
+size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t hidden,
+                                          int32_t n_q_heads, int32_t n_kv_heads,
+                                          int32_t head_dim, semshare_dtype_t dtype) {
+    if (!dtype_ok(dtype) || n_sel < 0 || n_tok < 0 || hidden <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 ||
+        head_dim <= 0 || n_q_heads % n_kv_heads)
+        return 0;
+    return prefill_layout(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
+}
+
+semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, int64_t n_sel,
+                                    const void* wq, const void* wk, const void* wv, void* k_cache,
+                                    void* v_cache, int64_t n_tok, int32_t hidden, int32_t n_q_heads,
+                                    int32_t n_kv_heads, int32_t head_dim, double rope_base, void* q_out,
+                                    float* deviation_out, void* workspace, size_t workspace_bytes,
+                                    semshare_dtype_t dtype, void* stream) {
+    const char* fn = "qkv_rope";
+    semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim, dtype, true);
+    if (st != SEMSHARE_OK) return st;
+    if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
     if (n_sel == 0) return ok();
-    if (!x_sel || !sel_pos || !wk || !wv || !k_cache || !v_cache)
-        return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (!x_sel || !sel_pos || !wk || !wv || !k_cache || !v_cache) return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (q_out && !wq) return fail(SEMSHARE_E_INVAL, "%s: wq is NULL but q_out is requested", fn);
+    if (!aligned16(x_sel) || !aligned16(wk) || !aligned16(wv) || !aligned16(k_cache) || !aligned16(v_cache) ||
+        (q_out && (!aligned16(wq) || !aligned16(q_out))))
+        return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
+    st = check_workspace(fn, workspace, workspace_bytes, semshare::qkv_workspace_bytes(n_sel, n_kv_heads, head_dim, dtype));
+    if (st != SEMSHARE_OK) return st;
+    const semshare::QkvArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden, n_q_heads,
+                              n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace};
+    hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_qkv_bf16(a, (hipStream_t)stream)
+                                          : semshare::launch_qkv_f32(a, (hipStream_t)stream);
+    return from_hip(e, "qkv_rope launch");
+}
+
+semshare_status_t semshare_prefill_attention(const void* q, const int32_t* sel_pos, int64_t n_sel,
+                                             const void* k_cache, const void* v_cache, int64_t n_tok,
+                                             int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                             float sm_scale, void* out, void* workspace,
+                                             size_t workspace_bytes, semshare_dtype_t dtype, void* stream) {
+    const char* fn = "prefill_attention";
+    semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, 0, n_q_heads, n_kv_heads, head_dim, dtype, false);
+    if (st != SEMSHARE_OK) return st;
+    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", fn);
+    if (n_sel == 0) return ok();
+    if (!q || !sel_pos || !k_cache || !v_cache || !out) return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+        return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
+    const semshare::AttnPlan plan = semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
+    st = check_workspace(fn, workspace, workspace_bytes, plan.total);
+    if (st != SEMSHARE_OK) return st;
+    const semshare::AttnCall a{q, sel_pos, n_sel, k_cache, v_cache, n_tok, n_q_heads, n_kv_heads, head_dim,
+                               default_scale(sm_scale, head_dim), out, workspace};
+    hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_attention_bf16(a, plan, (hipStream_t)stream)
+                                          : semshare::launch_attention_f32(a, plan, (hipStream_t)stream);
+    return from_hip(e, "prefill_attention launch");
+}
+
+semshare_status_t semshare_partial_prefill(
+    const void* x_sel, const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
+    const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
+    int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base, float sm_scale,
+    void* out, float* deviation_out, void* workspace, size_t workspace_bytes,
+    semshare_dtype_t dtype, void* stream) {
+    const char* fn = "partial_prefill";
+    semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim, dtype, true);
+    if (st != SEMSHARE_OK) return st;
+    if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
+    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", fn);
+    if (n_sel == 0) return ok();
+    if (!x_sel || !sel_pos || !wk || !wv || !k_cache || !v_cache) return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
     if (out && !wq) return fail(SEMSHARE_E_INVAL, "%s: wq is NULL but out is requested", fn);
     if (!aligned16(x_sel) || !aligned16(wk) || !aligned16(wv) || !aligned16(k_cache) || !aligned16(v_cache) ||
         (out && (!aligned16(wq) || !aligned16(out))))
         return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
-    const semshare::PrefillPlan plan =
-        semshare::plan_partial_prefill(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
-    if (!workspace || workspace_bytes < plan.total)
-        return fail(SEMSHARE_E_INVAL, "%s: workspace of %zu bytes is smaller than the %zu required", fn,
-                    workspace_bytes, plan.total);
-    if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(SEMSHARE_E_INVAL, "%s: workspace not 256-byte aligned", fn);
-    semshare::PrefillArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden,
-                            n_q_heads, n_kv_heads, head_dim, rope_base,
-                            sm_scale > 0.0f ? sm_scale : (float)(1.0 / std::sqrt((double)head_dim)),
-                            out, deviation_out, workspace, workspace_bytes, dtype};
-    hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_partial_prefill_bf16(a, plan, (hipStream_t)stream)
-                                          : semshare::launch_partial_prefill_f32(a, plan, (hipStream_t)stream);
+    const PrefillLayout lay = prefill_layout(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
+    st = check_workspace(fn, workspace, workspace_bytes, lay.total);
+    if (st != SEMSHARE_OK) return st;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    void* q_ws = out ? ws + lay.off_q : nullptr;
+    const semshare::QkvArgs qa{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden, n_q_heads,
+                               n_kv_heads, head_dim, rope_base, q_ws, deviation_out, ws + lay.off_qkv};
+    hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_qkv_bf16(qa, (hipStream_t)stream)
+                                          : semshare::launch_qkv_f32(qa, (hipStream_t)stream);
+    if (e != hipSuccess || !out) return from_hip(e, "partial_prefill launch");
+    const semshare::AttnPlan plan = semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
+    const semshare::AttnCall aa{q_ws, sel_pos, n_sel, k_cache, v_cache, n_tok, n_q_heads, n_kv_heads, head_dim,
+                                default_scale(sm_scale, head_dim), out, ws + lay.off_attn};
+    e = dtype == SEMSHARE_BF16 ? semshare::launch_attention_bf16(aa, plan, (hipStream_t)stream)
+                               : semshare::launch_attention_f32(aa, plan, (hipStream_t)stream);
     return from_hip(e, "partial_prefill launch");
 }
 

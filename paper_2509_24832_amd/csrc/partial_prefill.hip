@@ -36,8 +36,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // ------------------------------------------------------------------ prep
 
 __global__ void prep_kernel(const int32_t* __restrict__ pos, int64_t n_sel, int64_t n_tok,
-                            int32_t half_d, double log2_base, float2* __restrict__ rope,
-                            float* __restrict__ dev_sums) {
+                            int32_t half_d, double log2_base, float2* __restrict__ rope) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n_sel * half_d) {
         const int64_t m = i / half_d;
@@ -49,12 +48,20 @@ __global__ void prep_kernel(const int32_t* __restrict__ pos, int64_t n_sel, int6
         rope_sincos((double)p, theta, &s, &c);
         rope[i] = make_float2(c, s);
     }
-    if (dev_sums && i < n_sel * 2) dev_sums[i] = 0.0f;
 }
 
-__global__ void dev_final_kernel(const float* __restrict__ sums, float* __restrict__ dev, int64_t n_sel) {
+// sigma = sqrt(sum dK^2) + sqrt(sum dV^2) from per-tile partial sums
+// parts[(m * 2 + t) * n_parts + j], summed in a fixed order (deterministic).
+__global__ void dev_final_kernel(const float* __restrict__ parts, float* __restrict__ dev, int64_t n_sel,
+                                 int32_t n_parts) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n_sel) dev[i] = sqrtf(sums[2 * i]) + sqrtf(sums[2 * i + 1]);
+    if (i >= n_sel) return;
+    float sk = 0.0f, sv = 0.0f;
+    for (int32_t j = 0; j < n_parts; ++j) {
+        sk += parts[(2 * i) * n_parts + j];
+        sv += parts[(2 * i + 1) * n_parts + j];
+    }
+    dev[i] = sqrtf(sk) + sqrtf(sv);
 }
 
 // ------------------------------------------------------------------ QKV GEMM
@@ -78,7 +85,7 @@ struct GemmArgs {
     uint16_t* q_out;        // [n_sel][Hq*D]
     uint16_t* kv[2];        // k_cache, v_cache [n_tok][Hkv*D]
     const float2* rope;     // [n_sel][D/2]
-    float* dev_sums;        // [n_sel][2] or null
+    float* dev_parts;       // [n_sel][2][Hkv*D/128] squared-difference sums, or null
 };
 
 __device__ __forceinline__ void gemm_load_regs(const uint16_t* p, u32x4_t (&r)[4]) {
@@ -225,7 +232,7 @@ __global__ __launch_bounds__(256, 2) void qkv_gemm_kernel(GemmArgs g) {
                 *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
             } else if (p >= 0 && p < g.n_tok) {
                 uint16_t* dst = kvseg + (int64_t)p * seg_cols + n;
-                if (g.dev_sums) {
+                if (g.dev_parts) {
                     const u32x4_t old = *reinterpret_cast<const u32x4_t*>(dst);
                     const uint32_t ow[4] = {old.x, old.y, old.z, old.w};
                     const uint32_t nw[4] = {packed.x, packed.y, packed.z, packed.w};
@@ -239,13 +246,14 @@ __global__ __launch_bounds__(256, 2) void qkv_gemm_kernel(GemmArgs g) {
                 *reinterpret_cast<u32x4_t*>(dst) = packed;
             }
         }
-        if (g.dev_sums && seg > 0) {
+        if (g.dev_parts && seg > 0) {
             // the 16 threads of one tile row are 16 consecutive lanes
             dsum += __shfl_xor(dsum, 8, 16);
             dsum += __shfl_xor(dsum, 4, 16);
             dsum += __shfl_xor(dsum, 2, 16);
             dsum += __shfl_xor(dsum, 1, 16);
-            if (cg == 0 && m < g.n_sel && dsum != 0.0f) atomicAdd(g.dev_sums + 2 * m + (seg - 1), dsum);
+            const int n_parts = seg_cols / GBN;
+            if (cg == 0 && m < g.n_sel) g.dev_parts[(2 * m + (seg - 1)) * n_parts + nt] = dsum;
         }
     }
 }
@@ -552,18 +560,24 @@ hipError_t launch_attention(const AttnArgs& args, hipStream_t s) {
 
 }  // namespace
 
-PrefillPlan plan_partial_prefill(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
-                                 int32_t n_kv_heads, int32_t head_dim, int dtype) {
-    PrefillPlan p{};
+size_t qkv_workspace_dev_offset(int64_t n_sel, int32_t head_dim, int dtype) {
+    return dtype == SEMSHARE_BF16 ? align256((size_t)n_sel * (head_dim / 2) * sizeof(float2)) : 0;
+}
+
+int32_t qkv_dev_parts(int32_t n_kv_heads, int32_t head_dim, int dtype) {
+    const int32_t cols = n_kv_heads * head_dim;
+    return dtype == SEMSHARE_BF16 ? cols / GBN : cols / 2;
+}
+
+size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim, int dtype) {
+    return qkv_workspace_dev_offset(n_sel, head_dim, dtype) +
+           align256((size_t)n_sel * 2 * qkv_dev_parts(n_kv_heads, head_dim, dtype) * sizeof(float));
+}
+
+AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                        int32_t head_dim, int dtype) {
+    AttnPlan p{};
     const int32_t G = n_q_heads / n_kv_heads;
-    const size_t esz = dtype == SEMSHARE_BF16 ? 2 : 4;
-    size_t off = 0;
-    p.off_q = off;
-    off = align256(off + (size_t)n_sel * n_q_heads * head_dim * esz);
-    p.off_rope = off;
-    if (dtype == SEMSHARE_BF16) off = align256(off + (size_t)n_sel * (head_dim / 2) * sizeof(float2));
-    p.off_dev = off;
-    off = align256(off + (size_t)n_sel * 2 * sizeof(float));
     p.rows_per_tile = dtype == SEMSHARE_BF16 ? 128 / G : 1;
     p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
     p.chunk = (int32_t)((n_tok + 63) / 64 * 64);
@@ -581,83 +595,84 @@ PrefillPlan plan_partial_prefill(int64_t n_sel, int64_t n_tok, int32_t n_q_heads
         p.n_chunks = (int32_t)((n_tok + p.chunk - 1) / p.chunk);
         if (p.n_chunks < 1) p.n_chunks = 1;
     }
-    p.off_part_o = off;
-    p.off_part_ml = off;
+    size_t off = 0;
+    p.off_part_o = p.off_part_ml = p.off_used = 0;
     if (p.n_chunks > 1) {
         const size_t items = (size_t)p.n_tiles * n_kv_heads * p.n_chunks;
-        off = align256(off + items * 128 * head_dim * sizeof(float));
+        off = align256(items * 128 * head_dim * sizeof(float));
         p.off_part_ml = off;
-        off = align256(off + items * 128 * 2 * sizeof(float) + (size_t)p.n_tiles * n_kv_heads * sizeof(int32_t));
+        off = align256(off + items * 128 * 2 * sizeof(float));
+        p.off_used = off;
+        off = align256(off + (size_t)p.n_tiles * n_kv_heads * sizeof(int32_t));
     }
     p.total = off;
     return p;
 }
 
-hipError_t launch_partial_prefill_bf16(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s) {
+hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     unsigned char* ws = static_cast<unsigned char*>(a.workspace);
-    uint16_t* q_ws = reinterpret_cast<uint16_t*>(ws + p.off_q);
-    float2* rope = reinterpret_cast<float2*>(ws + p.off_rope);
-    float* dev_sums = a.deviation_out ? reinterpret_cast<float*>(ws + p.off_dev) : nullptr;
+    float2* rope = reinterpret_cast<float2*>(ws);
+    float* dev_parts = a.deviation_out
+                           ? reinterpret_cast<float*>(ws + qkv_workspace_dev_offset(a.n_sel, a.head_dim, SEMSHARE_BF16))
+                           : nullptr;
     const int32_t half_d = a.head_dim / 2;
-
     {
         const int64_t n = a.n_sel * half_d;
         hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sel_pos, a.n_sel,
-                           a.n_tok, half_d, log2(a.rope_base), rope, dev_sums);
+                           a.n_tok, half_d, log2(a.rope_base), rope);
     }
-    {
-        GemmArgs g{};
-        g.x = static_cast<const uint16_t*>(a.x_sel);
-        g.pos = a.sel_pos;
-        g.w[0] = static_cast<const uint16_t*>(a.wq);
-        g.w[1] = static_cast<const uint16_t*>(a.wk);
-        g.w[2] = static_cast<const uint16_t*>(a.wv);
-        g.seg_cols[0] = a.n_q_heads * a.head_dim;
-        g.seg_cols[1] = g.seg_cols[2] = a.n_kv_heads * a.head_dim;
-        g.seg_tiles[0] = a.out ? g.seg_cols[0] / GBN : 0;
-        g.seg_tiles[1] = g.seg_tiles[2] = g.seg_cols[1] / GBN;
-        g.n_nt = g.seg_tiles[0] + g.seg_tiles[1] + g.seg_tiles[2];
-        g.n_mt = (int32_t)((a.n_sel + GBM - 1) / GBM);
-        g.n_sel = a.n_sel;
-        g.n_tok = a.n_tok;
-        g.hidden = a.hidden;
-        g.D = a.head_dim;
-        g.q_out = q_ws;
-        g.kv[0] = static_cast<uint16_t*>(a.k_cache);
-        g.kv[1] = static_cast<uint16_t*>(a.v_cache);
-        g.rope = rope;
-        g.dev_sums = dev_sums;
-        const int64_t per_xcd = (g.n_nt + 7) / 8;
-        const unsigned grid = (unsigned)(8 * per_xcd * g.n_mt);
-        hipLaunchKernelGGL(qkv_gemm_kernel, dim3(grid), dim3(256), 0, s, g);
-    }
+    GemmArgs g{};
+    g.x = static_cast<const uint16_t*>(a.x_sel);
+    g.pos = a.sel_pos;
+    g.w[0] = static_cast<const uint16_t*>(a.wq);
+    g.w[1] = static_cast<const uint16_t*>(a.wk);
+    g.w[2] = static_cast<const uint16_t*>(a.wv);
+    g.seg_cols[0] = a.n_q_heads * a.head_dim;
+    g.seg_cols[1] = g.seg_cols[2] = a.n_kv_heads * a.head_dim;
+    g.seg_tiles[0] = a.q_out ? g.seg_cols[0] / GBN : 0;
+    g.seg_tiles[1] = g.seg_tiles[2] = g.seg_cols[1] / GBN;
+    g.n_nt = g.seg_tiles[0] + g.seg_tiles[1] + g.seg_tiles[2];
+    g.n_mt = (int32_t)((a.n_sel + GBM - 1) / GBM);
+    g.n_sel = a.n_sel;
+    g.n_tok = a.n_tok;
+    g.hidden = a.hidden;
+    g.D = a.head_dim;
+    g.q_out = static_cast<uint16_t*>(a.q_out);
+    g.kv[0] = static_cast<uint16_t*>(a.k_cache);
+    g.kv[1] = static_cast<uint16_t*>(a.v_cache);
+    g.rope = rope;
+    g.dev_parts = dev_parts;
+    const int64_t per_xcd = (g.n_nt + 7) / 8;
+    hipLaunchKernelGGL(qkv_gemm_kernel, dim3((unsigned)(8 * per_xcd * g.n_mt)), dim3(256), 0, s, g);
     if (a.deviation_out)
-        hipLaunchKernelGGL(dev_final_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_sums,
-                           a.deviation_out, a.n_sel);
-    if (a.out) {
-        AttnArgs t{};
-        t.q = q_ws;
-        t.pos = a.sel_pos;
-        t.k_cache = static_cast<const uint16_t*>(a.k_cache);
-        t.v_cache = static_cast<const uint16_t*>(a.v_cache);
-        t.out = static_cast<uint16_t*>(a.out);
-        t.part_o = reinterpret_cast<float*>(ws + p.off_part_o);
-        t.part_ml = reinterpret_cast<float*>(ws + p.off_part_ml);
-        t.n_used = reinterpret_cast<int32_t*>(ws + p.off_part_ml + (size_t)p.n_tiles * a.n_kv_heads * p.n_chunks * 128 * 2 * sizeof(float));
-        t.n_sel = a.n_sel;
-        t.n_tok = a.n_tok;
-        t.Hq = a.n_q_heads;
-        t.Hkv = a.n_kv_heads;
-        t.G = a.n_q_heads / a.n_kv_heads;
-        t.R = p.rows_per_tile;
-        t.n_tiles = (int32_t)p.n_tiles;
-        t.chunk = p.chunk;
-        t.n_chunks = p.n_chunks;
-        t.cl2 = a.sm_scale * kLog2e;
-        if (a.head_dim == 128) return launch_attention<128>(t, s);
-        return launch_attention<64>(t, s);
-    }
+        hipLaunchKernelGGL(dev_final_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_parts,
+                           a.deviation_out, a.n_sel, qkv_dev_parts(a.n_kv_heads, a.head_dim, SEMSHARE_BF16));
     return hipGetLastError();
+}
+
+hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream_t s) {
+    unsigned char* ws = static_cast<unsigned char*>(a.workspace);
+    AttnArgs t{};
+    t.q = static_cast<const uint16_t*>(a.q);
+    t.pos = a.sel_pos;
+    t.k_cache = static_cast<const uint16_t*>(a.k_cache);
+    t.v_cache = static_cast<const uint16_t*>(a.v_cache);
+    t.out = static_cast<uint16_t*>(a.out);
+    t.part_o = reinterpret_cast<float*>(ws + p.off_part_o);
+    t.part_ml = reinterpret_cast<float*>(ws + p.off_part_ml);
+    t.n_used = reinterpret_cast<int32_t*>(ws + p.off_used);
+    t.n_sel = a.n_sel;
+    t.n_tok = a.n_tok;
+    t.Hq = a.n_q_heads;
+    t.Hkv = a.n_kv_heads;
+    t.G = a.n_q_heads / a.n_kv_heads;
+    t.R = p.rows_per_tile;
+    t.n_tiles = (int32_t)p.n_tiles;
+    t.chunk = p.chunk;
+    t.n_chunks = p.n_chunks;
+    t.cl2 = a.sm_scale * kLog2e;
+    if (a.head_dim == 128) return launch_attention<128>(t, s);
+    return launch_attention<64>(t, s);
 }
 
 }  // namespace semshare

@@ -16,11 +16,6 @@
 namespace semshare {
 namespace {
 
-__global__ void zero_f32_kernel(float* p, int64_t n) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0.0f;
-}
-
 struct QkvF32Args {
     const float* x;
     const int32_t* pos;
@@ -32,7 +27,7 @@ struct QkvF32Args {
     double log2_base;
     float* q_out;
     float* kv[2];
-    float* dev_sums;
+    float* dev_parts;  // [n_sel][2][Hkv*D/2] squared differences per pair, or null
 };
 
 __global__ __launch_bounds__(256) void qkv_f32_kernel(QkvF32Args a, int32_t pairs_per_row) {
@@ -78,19 +73,30 @@ __global__ __launch_bounds__(256) void qkv_f32_kernel(QkvF32Args a, int32_t pair
         q[1] = y1;
         return;
     }
-    if (p < 0 || p >= a.n_tok) return;
+    float* part = a.dev_parts ? a.dev_parts + (2 * m + (seg - 1)) * (int64_t)(nkv / 2) + c / 2 : nullptr;
+    if (p < 0 || p >= a.n_tok) {
+        if (part) *part = 0.0f;
+        return;
+    }
     float* dst = (seg == 1 ? a.kv[0] : a.kv[1]) + (int64_t)p * seg_cols + c;
-    if (a.dev_sums) {
+    if (part) {
         const float d0 = dst[0] - y0, d1 = dst[1] - y1;
-        atomicAdd(a.dev_sums + 2 * m + (seg - 1), d0 * d0 + d1 * d1);
+        *part = d0 * d0 + d1 * d1;
     }
     dst[0] = y0;
     dst[1] = y1;
 }
 
-__global__ void dev_final_f32_kernel(const float* __restrict__ sums, float* __restrict__ dev, int64_t n_sel) {
+__global__ void dev_final_f32_kernel(const float* __restrict__ parts, float* __restrict__ dev, int64_t n_sel,
+                                     int32_t n_parts) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n_sel) dev[i] = sqrtf(sums[2 * i]) + sqrtf(sums[2 * i + 1]);
+    if (i >= n_sel) return;
+    float sk = 0.0f, sv = 0.0f;
+    for (int32_t j = 0; j < n_parts; ++j) {
+        sk += parts[(2 * i) * n_parts + j];
+        sv += parts[(2 * i + 1) * n_parts + j];
+    }
+    dev[i] = sqrtf(sk) + sqrtf(sv);
 }
 
 constexpr int kAttnThreads = 128;
@@ -156,13 +162,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_f32_kernel(const float* __r
 
 }  // namespace
 
-hipError_t launch_partial_prefill_f32(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s) {
+hipError_t launch_qkv_f32(const QkvArgs& a, hipStream_t s) {
     unsigned char* ws = static_cast<unsigned char*>(a.workspace);
-    float* q_ws = reinterpret_cast<float*>(ws + p.off_q);
-    float* dev_sums = a.deviation_out ? reinterpret_cast<float*>(ws + p.off_dev) : nullptr;
-    if (dev_sums)
-        hipLaunchKernelGGL(zero_f32_kernel, dim3((unsigned)((2 * a.n_sel + 255) / 256)), dim3(256), 0, s, dev_sums,
-                           2 * a.n_sel);
+    float* dev_parts = a.deviation_out
+                           ? reinterpret_cast<float*>(ws + qkv_workspace_dev_offset(a.n_sel, a.head_dim, SEMSHARE_FP32))
+                           : nullptr;
     QkvF32Args q{};
     q.x = static_cast<const float*>(a.x_sel);
     q.pos = a.sel_pos;
@@ -171,29 +175,33 @@ hipError_t launch_partial_prefill_f32(const PrefillArgs& a, const PrefillPlan& p
     q.w[2] = static_cast<const float*>(a.wv);
     q.seg_cols[0] = a.n_q_heads * a.head_dim;
     q.seg_cols[1] = q.seg_cols[2] = a.n_kv_heads * a.head_dim;
-    q.first_seg = a.out ? 0 : 1;
+    q.first_seg = a.q_out ? 0 : 1;
     q.n_sel = a.n_sel;
     q.n_tok = a.n_tok;
     q.hidden = a.hidden;
     q.D = a.head_dim;
     q.log2_base = log2(a.rope_base);
-    q.q_out = q_ws;
+    q.q_out = static_cast<float*>(a.q_out);
     q.kv[0] = static_cast<float*>(a.k_cache);
     q.kv[1] = static_cast<float*>(a.v_cache);
-    q.dev_sums = dev_sums;
-    const int32_t cols = (a.out ? q.seg_cols[0] : 0) + 2 * q.seg_cols[1];
+    q.dev_parts = dev_parts;
+    const int32_t cols = (a.q_out ? q.seg_cols[0] : 0) + 2 * q.seg_cols[1];
     const int32_t pairs = cols / 2;
     const int64_t n = a.n_sel * pairs;
     hipLaunchKernelGGL(qkv_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, q, pairs);
-    if (dev_sums)
-        hipLaunchKernelGGL(dev_final_f32_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_sums,
-                           a.deviation_out, a.n_sel);
-    if (a.out) {
-        const size_t lds = (size_t)a.n_tok * sizeof(float);
-        hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)(a.n_sel * a.n_q_heads)), dim3(kAttnThreads), lds, s,
-                           q_ws, a.sel_pos, static_cast<const float*>(a.k_cache), static_cast<const float*>(a.v_cache),
-                           static_cast<float*>(a.out), a.n_tok, a.n_q_heads, a.n_kv_heads, a.head_dim, a.sm_scale);
-    }
+    if (dev_parts)
+        hipLaunchKernelGGL(dev_final_f32_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_parts,
+                           a.deviation_out, a.n_sel, qkv_dev_parts(a.n_kv_heads, a.head_dim, SEMSHARE_FP32));
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_f32(const AttnCall& a, const AttnPlan& p, hipStream_t s) {
+    (void)p;
+    const size_t lds = (size_t)a.n_tok * sizeof(float);
+    hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)(a.n_sel * a.n_q_heads)), dim3(kAttnThreads), lds, s,
+                       static_cast<const float*>(a.q), a.sel_pos, static_cast<const float*>(a.k_cache),
+                       static_cast<const float*>(a.v_cache), static_cast<float*>(a.out), a.n_tok, a.n_q_heads,
+                       a.n_kv_heads, a.head_dim, a.sm_scale);
     return hipGetLastError();
 }
 

@@ -77,7 +77,9 @@ hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_
 hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
                                    int32_t* sel_pos, hipStream_t s);
 
-struct PrefillArgs {
+// Step 1 of a partial-prefill layer: q/k/v projection, RoPE, deviation and
+// the scatter of k/v into the cache.
+struct QkvArgs {
     const void* x_sel;
     const int32_t* sel_pos;
     int64_t n_sel;
@@ -89,27 +91,43 @@ struct PrefillArgs {
     int64_t n_tok;
     int32_t hidden, n_q_heads, n_kv_heads, head_dim;
     double rope_base;
+    void* q_out;           // [n_sel][Hq][D] or null (K/V only)
+    float* deviation_out;  // [n_sel] or null
+    void* workspace;       // qkv_workspace_bytes()
+};
+
+// Step 2: causal GQA attention of the selected rows over the cache.
+struct AttnCall {
+    const void* q;
+    const int32_t* sel_pos;
+    int64_t n_sel;
+    const void* k_cache;
+    const void* v_cache;
+    int64_t n_tok;
+    int32_t n_q_heads, n_kv_heads, head_dim;
     float sm_scale;
     void* out;
-    float* deviation_out;
-    void* workspace;
-    size_t workspace_bytes;
-    int dtype;
+    void* workspace;  // plan_attention().total bytes
 };
 
-// Partition of the partial-prefill workspace (offsets in bytes).
-struct PrefillPlan {
-    int32_t rows_per_tile;  // selected rows per attention tile (128 / G)
-    int64_t n_tiles;        // attention row tiles
+// Work decomposition and workspace partition of the attention step.
+struct AttnPlan {
+    int32_t rows_per_tile;  // selected rows per tile (128 / G for bf16)
+    int64_t n_tiles;
     int32_t chunk;          // keys per split-KV chunk (multiple of 64)
-    int32_t n_chunks;       // ceil(n_tok / chunk)
-    size_t off_q, off_rope, off_dev, off_part_o, off_part_ml, total;
+    int32_t n_chunks;       // ceil(n_tok / chunk); 1 = no split
+    size_t off_part_o, off_part_ml, off_used, total;
 };
 
-PrefillPlan plan_partial_prefill(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
-                                 int32_t n_kv_heads, int32_t head_dim, int dtype);
+size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim, int dtype);
+size_t qkv_workspace_dev_offset(int64_t n_sel, int32_t head_dim, int dtype);
+int32_t qkv_dev_parts(int32_t n_kv_heads, int32_t head_dim, int dtype);
+AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                        int32_t head_dim, int dtype);
 
-hipError_t launch_partial_prefill_bf16(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s);
-hipError_t launch_partial_prefill_f32(const PrefillArgs& a, const PrefillPlan& p, hipStream_t s);
+hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s);
+hipError_t launch_qkv_f32(const QkvArgs& a, hipStream_t s);
+hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream_t s);
+hipError_t launch_attention_f32(const AttnCall& a, const AttnPlan& p, hipStream_t s);
 
 }  // namespace semshare

@@ -59,6 +59,10 @@ def load() -> ctypes.CDLL:
                                            P, P, P, SZ, I32, P]),
         "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
         "semshare_select_recompute": (I32, [P, I64, I64, P, P]),
+        "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
+        "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32]),
+        "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
+        "semshare_prefill_attention_workspace": (SZ, [I64, I64, I32, I32, I32, I32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -253,6 +257,81 @@ def partial_prefill(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[tor
           float(rope_base), float(sm_scale), _ptr(out), _ptr(deviation), _ptr(workspace), workspace.numel(),
           _dt(x_sel), _stream())
     return out, deviation
+
+
+def qkv_rope_workspace_bytes(n_sel: int, n_kv_heads: int, head_dim: int, dtype: torch.dtype) -> int:
+    return int(load().semshare_qkv_rope_workspace(n_sel, n_kv_heads, head_dim,
+                                                  BF16 if dtype == torch.bfloat16 else FP32))
+
+
+def prefill_attention_workspace_bytes(n_sel: int, n_tok: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                                      dtype: torch.dtype) -> int:
+    return int(load().semshare_prefill_attention_workspace(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim,
+                                                           BF16 if dtype == torch.bfloat16 else FP32))
+
+
+def _workspace(need: int, given: Optional[torch.Tensor], like: torch.Tensor) -> Optional[torch.Tensor]:
+    if given is not None:
+        return _dev(given, "workspace", torch.uint8)
+    if need == 0:
+        return None
+    return torch.empty(need, dtype=torch.uint8, device=like.device)
+
+
+def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tensor], wk: torch.Tensor,
+             wv: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int,
+             rope_base: float = 10000.0, q_out: Optional[torch.Tensor] = None, want_q: bool = True,
+             deviation: Optional[torch.Tensor] = None, want_deviation: bool = False,
+             workspace: Optional[torch.Tensor] = None):
+    """Projection + RoPE + deviation + cache scatter of the selected rows.
+    Returns (q [n_sel, Hq, D] or None, deviation [n_sel] or None)."""
+    _dev(x_sel, "x_sel")
+    dt = x_sel.dtype
+    _dev(sel_pos, "sel_pos", torch.int32)
+    for name, t in (("wk", wk), ("wv", wv), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, name, dt)
+    n_sel, hidden = x_sel.shape
+    n_tok, head_dim = k_cache.shape[0], k_cache.shape[-1]
+    if k_cache.numel() != n_tok * n_kv_heads * head_dim or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [n_tok, n_kv_heads, head_dim]")
+    if want_q:
+        _dev(wq, "wq", dt)
+        if q_out is None:
+            q_out = torch.empty((n_sel, n_q_heads, head_dim), dtype=dt, device=x_sel.device)
+        _dev(q_out, "q_out", dt)
+    else:
+        q_out = None
+    if want_deviation and deviation is None:
+        deviation = torch.empty(n_sel, dtype=torch.float32, device=x_sel.device)
+    if not want_deviation:
+        deviation = None
+    ws = _workspace(qkv_rope_workspace_bytes(n_sel, n_kv_heads, head_dim, dt), workspace, x_sel)
+    _call("semshare_qkv_rope", _ptr(x_sel), _ptr(sel_pos), n_sel, _ptr(wq) if want_q else None, _ptr(wk), _ptr(wv),
+          _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, float(rope_base),
+          _ptr(q_out), _ptr(deviation), _ptr(ws), 0 if ws is None else ws.numel(), _dt(x_sel), _stream())
+    return q_out, deviation
+
+
+def prefill_attention(q: torch.Tensor, sel_pos: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                      n_kv_heads: int, sm_scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Causal GQA attention of the selected rows (q [n_sel, Hq, D]) over the cache."""
+    _dev(q, "q")
+    dt = q.dtype
+    _dev(sel_pos, "sel_pos", torch.int32)
+    _dev(k_cache, "k_cache", dt)
+    _dev(v_cache, "v_cache", dt)
+    n_sel, n_q_heads, head_dim = q.shape
+    n_tok = k_cache.shape[0]
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out", dt)
+    ws = _workspace(prefill_attention_workspace_bytes(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dt),
+                    workspace, q)
+    _call("semshare_prefill_attention", _ptr(q), _ptr(sel_pos), n_sel, _ptr(k_cache), _ptr(v_cache), n_tok,
+          n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out), _ptr(ws), 0 if ws is None else ws.numel(),
+          _dt(q), _stream())
+    return out
 
 
 def select_recompute(sigma: torch.Tensor, n_sel: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:

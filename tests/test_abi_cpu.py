@@ -157,3 +157,25 @@ def test_product_package_never_imports_the_oracle():
             if f.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(root, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text and "orc_" not in text, f
+
+
+def test_split_call_validation(lib):
+    L = ss.load()
+    assert L.semshare_qkv_rope(FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 256, 8, 2, 128, 1e4, FAKE, None, FAKE,
+                               1 << 30, 1, None) == b.E_INVAL  # n_sel > n_tok
+    assert L.semshare_qkv_rope(FAKE, FAKE, 8, None, FAKE, FAKE, FAKE, FAKE, 16, 256, 8, 2, 128, 1e4, FAKE, None, FAKE,
+                               1 << 30, 1, None) == b.E_INVAL  # q requested without wq
+    assert L.semshare_qkv_rope(FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 16, 256, 8, 2, 128, 1e4, FAKE, None, FAKE,
+                               0, 1, None) == b.E_INVAL  # workspace too small
+    assert L.semshare_prefill_attention(FAKE, FAKE, 8, FAKE, FAKE, 16, 8, 2, 96, 0.0, FAKE, FAKE, 1 << 30, 1,
+                                        None) == b.E_UNSUPPORTED
+    assert L.semshare_prefill_attention(FAKE, FAKE, 8, FAKE, FAKE, 16, 8, 2, 128, -2.0, FAKE, FAKE, 1 << 30, 1,
+                                        None) == b.E_INVAL
+    assert L.semshare_prefill_attention(FAKE, FAKE, 8, FAKE, FAKE, 16, 8, 2, 128, 0.0, None, FAKE, 1 << 30, 1,
+                                        None) == b.E_INVAL
+    assert L.semshare_prefill_attention(None, None, 0, None, None, 16, 8, 2, 128, 0.0, None, None, 0, 1, None) == b.OK
+    # composition: the partial-prefill workspace covers q plus both steps
+    W = L.semshare_partial_prefill_workspace(1280, 5120, 4096, 32, 8, 128, 1)
+    assert W >= 1280 * 32 * 128 * 2 + L.semshare_qkv_rope_workspace(1280, 8, 128, 1) + \
+        L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1)
+    assert L.semshare_prefill_attention_workspace(5120, 5120, 32, 8, 128, 1) == 0  # no split needed at full length

@@ -178,3 +178,25 @@ def test_config2_layer_sampled_rows():
     check_cache_rows("bf16", kc_g, kc_r, k, sel, x_all[sel], w.wk, True)
     check_cache_rows("bf16", vc_g, vc_r, v, sel, x_all[sel], w.wv, False)
     np.testing.assert_allclose(sig_g, sig_r, rtol=1e-3)
+
+
+def test_split_calls_equal_partial_prefill():
+    """semshare_qkv_rope followed by semshare_prefill_attention runs the same
+    kernels as semshare_partial_prefill: identical outputs, caches and deviation."""
+    cfg = CONFIGS[1]
+    n_tok, hidden, hq, hkv, d = 700, 512, 16, 4, 128
+    x_all, w, k, v, sel = _case(cfg, n_tok, hidden, hq, hkv, d, 200, tag=8)
+    dt = cfg.dtype
+    announce("split calls vs partial_prefill")
+    xs, ps = dev(x_all[sel], dt), dev_i32(sel)
+    wq, wk, wv = dev(w.wq, dt), dev(w.wk, dt), dev(w.wv, dt)
+    k1, v1, k2, v2 = dev(k, dt), dev(v, dt), dev(k, dt), dev(v, dt)
+    out1, dev1 = ss.partial_prefill(xs, ps, wq, wk, wv, k1, v1, hq, hkv, want_deviation=True)
+    q, dev2 = ss.qkv_rope(xs, ps, wq, wk, wv, k2, v2, hq, hkv, want_deviation=True)
+    out2 = ss.prefill_attention(q, ps, k2, v2, hkv)
+    for a, b in ((out1, out2), (dev1, dev2), (k1, k2), (v1, v2)):
+        assert torch.equal(a, b)
+    # and the q written by the projection step is the oracle's within the derived bound
+    qr, _, _ = orc.qkv_rows(x_all[sel], sel, w.wq, w.wk, w.wv, hq, hkv, d, dtype="bf16", want_kv=False)
+    b = rotated_pair_bound(fp32_dot_error_bound(x_all[sel], w.wq), d) + 1e-6 * np.abs(qr)
+    assert np.all(np.abs(host(q).reshape(len(sel), -1) - qr) <= bf16_ulp(qr) + b)
