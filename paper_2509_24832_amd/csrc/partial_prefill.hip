@@ -288,6 +288,14 @@ struct AttnLds {
     static constexpr int kVItems = 16 * (D / 8);              // (key quad, d group) items
 };
 
+typedef float f32x8_t __attribute__((ext_vector_type(8)));
+
+// Running-max slack of the online softmax, in log2 units: the output
+// accumulators are rescaled only when a column's maximum grows by more than
+// this, so probabilities stay <= 2^8 (exact enough in bf16 and fp32) and the
+// 64-register rescale is skipped on almost every tile.
+constexpr float kRescaleSlack = 8.0f;
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
     using L = AttnLds<D>;
@@ -298,7 +306,7 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
     uint16_t* Vt = reinterpret_cast<uint16_t*>(smem + L::kBytes);
 
     const int b = blockIdx.x;
-    const int g = b % a.Hkv;
+    const int g = b % a.Hkv;  // kv head: with 8 kv heads, one per XCD (its K/V stay in that L2)
     const int jj = b / a.Hkv;
     const int tile = a.n_tiles - 1 - jj / a.n_chunks;  // longest (latest) tiles first
     const int chunk_id = jj % a.n_chunks;
@@ -341,37 +349,58 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
     // Q^T operand: lane half h holds d in [h*D/2, h*D/2 + D/2)
     bf16x8_t qf[D / 16];
     {
-        const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(a.q + ((p_l >= 0 ? row : 0) * a.Hq + head) * (int64_t)D + half * (D / 2));
+        const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(a.q + ((p_l >= 0 ? row : 0) * a.Hq + head) * (int64_t)D +
+                                                             half * (D / 2));
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) {
-            u32x4_t w = p_l >= 0 ? qp[s] : u32x4_t{0u, 0u, 0u, 0u};
+            const u32x4_t w = p_l >= 0 ? qp[s] : u32x4_t{0u, 0u, 0u, 0u};
             qf[s] = __builtin_bit_cast(bf16x8_t, w);
         }
     }
 
-    const int64_t row_stride = (int64_t)a.Hkv * D;  // elements between consecutive keys
+    // Per-thread global offsets (elements) of its K/V tile loads, relative to
+    // the tile's first key; consecutive keys are row_stride elements apart.
+    const int32_t row_stride = a.Hkv * D;
     const uint16_t* kbase = a.k_cache + (int64_t)g * D;
     const uint16_t* vbase = a.v_cache + (int64_t)g * D;
     const int32_t last_key = (int32_t)a.n_tok - 1;
+    int32_t k_key[L::kKLoads], k_off[L::kKLoads];
+#pragma unroll
+    for (int i = 0; i < L::kKLoads; ++i) {
+        const int item = i * 256 + tid;
+        k_key[i] = item / L::kChunksPerKey;
+        k_off[i] = k_key[i] * row_stride + (item % L::kChunksPerKey) * 8;
+    }
+    // V: thread -> (key quad kq = tid % 16, d group dg = tid / 16): the
+    // transposed LDS writes of a wave then cover every bank exactly twice.
+    const bool v_owner = tid < L::kVItems;
+    const int v_kq = tid & 15, v_dg = tid >> 4;
+    const int32_t v_off = 4 * v_kq * row_stride + v_dg * 8;
 
     u32x4_t rk[L::kKLoads];
     u32x4_t rv[4];
-    const bool v_owner = tid < L::kVItems;
-    const int v_dg = tid % (D / 8), v_kq = tid / (D / 8);
-
     auto load_regs = [&](int32_t k0) {
+        const int64_t base = (int64_t)k0 * row_stride;
+        if (k0 + KT <= (int32_t)a.n_tok) {
 #pragma unroll
-        for (int i = 0; i < L::kKLoads; ++i) {
-            const int item = i * 256 + tid;
-            const int key = item / L::kChunksPerKey, ch = item % L::kChunksPerKey;
-            const int32_t kk = min(k0 + key, last_key);
-            rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + kk * row_stride + ch * 8);
-        }
-        if (v_owner) {
+            for (int i = 0; i < L::kKLoads; ++i) rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + base + k_off[i]);
+            if (v_owner) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int32_t kk = min(k0 + 4 * v_kq + i, last_key);
-                rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + kk * row_stride + v_dg * 8);
+                for (int i = 0; i < 4; ++i)
+                    rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + base + v_off + i * row_stride);
+            }
+        } else {  // tail tile: clamp rows past the end (their scores are masked)
+#pragma unroll
+            for (int i = 0; i < L::kKLoads; ++i) {
+                const int32_t kk = min(k0 + k_key[i], last_key);
+                rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + (int64_t)kk * row_stride + (k_off[i] - k_key[i] * row_stride));
+            }
+            if (v_owner) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int32_t kk = min(k0 + 4 * v_kq + i, last_key);
+                    rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + (int64_t)kk * row_stride + v_dg * 8);
+                }
             }
         }
     };
@@ -380,24 +409,20 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < L::kKLoads; ++i) {
             const int item = i * 256 + tid;
-            const int key = item / L::kChunksPerKey, ch = item % L::kChunksPerKey;
-            *reinterpret_cast<u32x4_t*>(kb + key * L::KLD + ch * 8) = rk[i];
+            *reinterpret_cast<u32x4_t*>(kb + k_key[i] * L::KLD + (item % L::kChunksPerKey) * 8) = rk[i];
         }
         if (v_owner) {
-            uint16_t* vb = Vt + buf * D * L::VLD;
-            const uint32_t w0[4] = {rv[0].x, rv[0].y, rv[0].z, rv[0].w};
-            const uint32_t w1[4] = {rv[1].x, rv[1].y, rv[1].z, rv[1].w};
-            const uint32_t w2[4] = {rv[2].x, rv[2].y, rv[2].z, rv[2].w};
-            const uint32_t w3[4] = {rv[3].x, rv[3].y, rv[3].z, rv[3].w};
+            uint16_t* vb = Vt + buf * D * L::VLD + (8 * v_dg) * L::VLD + 4 * v_kq;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                u32x2_t lo, hi;  // d = 8*dg + 2e (lo halves) and 2e+1 (hi halves), keys 4kq..4kq+3
-                lo.x = __builtin_amdgcn_perm(w1[e], w0[e], 0x05040100u);
-                lo.y = __builtin_amdgcn_perm(w3[e], w2[e], 0x05040100u);
-                hi.x = __builtin_amdgcn_perm(w1[e], w0[e], 0x07060302u);
-                hi.y = __builtin_amdgcn_perm(w3[e], w2[e], 0x07060302u);
-                *reinterpret_cast<u32x2_t*>(vb + (8 * v_dg + 2 * e) * L::VLD + 4 * v_kq) = lo;
-                *reinterpret_cast<u32x2_t*>(vb + (8 * v_dg + 2 * e + 1) * L::VLD + 4 * v_kq) = hi;
+                // d = 8*dg + 2e (low halves) and 2e+1 (high halves), keys 4kq .. 4kq+3
+                u32x2_t lo, hi;
+                lo.x = __builtin_amdgcn_perm(rv[1][e], rv[0][e], 0x05040100u);
+                lo.y = __builtin_amdgcn_perm(rv[3][e], rv[2][e], 0x05040100u);
+                hi.x = __builtin_amdgcn_perm(rv[1][e], rv[0][e], 0x07060302u);
+                hi.y = __builtin_amdgcn_perm(rv[3][e], rv[2][e], 0x07060302u);
+                *reinterpret_cast<u32x2_t*>(vb + (2 * e) * L::VLD) = lo;
+                *reinterpret_cast<u32x2_t*>(vb + (2 * e + 1) * L::VLD) = hi;
             }
         }
     };
@@ -438,45 +463,48 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
                     if (key > p_l || key >= kend) sacc[mb][v] = -INFINITY;
                 }
         }
-        float mx = sacc[0][0];
+        float mx = fmaxf(sacc[0][0], sacc[0][1]);
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+        for (int v = 2; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[0][v], sacc[0][v + 1]));
 #pragma unroll
-            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[mb][v]);
+        for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[1][v], sacc[1][v + 1]));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * cl2);
-        const float mc = m_new * cl2;
+        if (__any((m_new - m_run) * cl2 > kRescaleSlack)) {  // rare: the first tile, then big jumps only
+            const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * cl2);
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
+        }
+        const float mc = m_run * cl2;
         float lsum = 0.0f;
+        bf16x8_t pb[4];
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+        for (int s = 0; s < 4; ++s) {  // keys 16s .. 16s+15 of the tile (permuted, see below)
+            f32x8_t pv;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mb][v], cl2, -mc));
-                sacc[mb][v] = pv;
-                lsum += pv;
+            for (int e = 0; e < 8; ++e) {
+                const float x = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], cl2, -mc));
+                pv[e] = x;
+                lsum += x;
             }
-        l_run = l_run * alpha + lsum;
-        m_run = m_new;
-#pragma unroll
-        for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
+            pb[s] = __builtin_convertvector(pv, bf16x8_t);
+        }
+        l_run += lsum;
 
+        // O^T += V^T P^T.  MFMA k index 8h+e of step s is key 16s + 8(e/4) + 4h + e%4:
+        // exactly the keys this lane's P values (above) belong to.
         const uint16_t* vb = Vt + buf * D * L::VLD;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {  // 16 keys per MFMA k-step
-            const int mb = s >> 1, v0 = 8 * (s & 1);
-            bf16x8_t pb;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) pb[e] = (__bf16)sacc[mb][v0 + e];
+        for (int s = 0; s < 4; ++s) {
 #pragma unroll
             for (int i = 0; i < D / 32; ++i) {
                 const uint16_t* vr = vb + (32 * i + l32) * L::VLD + 16 * s + 4 * half;
                 const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
                 const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 8);
                 const u32x4_t w = u32x4_t{lo.x, lo.y, hi.x, hi.y};
-                oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, w), pb, oacc[i], 0, 0, 0);
+                oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, w), pb[s], oacc[i], 0, 0, 0);
             }
         }
         if (more) store_lds(buf ^ 1);
@@ -507,20 +535,22 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int d0 = 32 * i + 8 * r + 4 * half;
-                *reinterpret_cast<float4*>(po + d0) =
-                    make_float4(oacc[i][4 * r], oacc[i][4 * r + 1], oacc[i][4 * r + 2], oacc[i][4 * r + 3]);
+                *reinterpret_cast<f32x4_t*>(po + d0) =
+                    f32x4_t{oacc[i][4 * r], oacc[i][4 * r + 1], oacc[i][4 * r + 2], oacc[i][4 * r + 3]};
             }
         if (half == 0) *reinterpret_cast<float2*>(a.part_ml + (item * 128 + col) * 2) = make_float2(m_run, l_tot);
     }
 }
 
+// Log-sum-exp merge of split-KV partial results: one workgroup per
+// (tile, kv head); thread t owns column t/2 and half of its head dim.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t tg = blockIdx.x / 32;  // tile * Hkv + g
-    const int col = (blockIdx.x % 32) * 4 + wave;
+    const int64_t tg = blockIdx.x;  // tile * Hkv + g
     const int32_t nu = a.n_used[tg];
     if (nu <= 1) return;
+    const int tid = threadIdx.x;
+    const int col = tid >> 1, dh = tid & 1;
     const int tile = (int)(tg / a.Hkv), g = (int)(tg % a.Hkv);
     const int row_local = col % a.R, head_local = col / a.R;
     const int64_t row = (int64_t)tile * a.R + row_local;
@@ -529,23 +559,29 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     if (p < 0 || p >= a.n_tok) return;
     const int head = g * a.G + head_local;
     const int64_t item0 = tg * a.n_chunks;
+    constexpr int PER = D / 2;
     float M = -1.0e30f;
     for (int c = 0; c < nu; ++c) M = fmaxf(M, a.part_ml[((item0 + c) * 128 + col) * 2]);
-    constexpr int PER = D / 64;
-    float acc[PER] = {};
+    f32x4_t acc[PER / 4];
+#pragma unroll
+    for (int e = 0; e < PER / 4; ++e) acc[e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float Lsum = 0.0f;
     for (int c = 0; c < nu; ++c) {
         const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((item0 + c) * 128 + col) * 2);
         const float w = __builtin_amdgcn_exp2f((ml.x - M) * a.cl2);
         Lsum += w * ml.y;
-        const float* po = a.part_o + ((item0 + c) * 128 + col) * D + PER * lane;
+        const f32x4_t* po = reinterpret_cast<const f32x4_t*>(a.part_o + ((item0 + c) * 128 + col) * D + dh * PER);
 #pragma unroll
-        for (int e = 0; e < PER; ++e) acc[e] += w * po[e];
+        for (int e = 0; e < PER / 4; ++e) acc[e] += w * po[e];
     }
     const float inv = 1.0f / Lsum;
-    uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D + PER * lane;
+    u32x4_t* op = reinterpret_cast<u32x4_t*>(a.out + (row * a.Hq + head) * (int64_t)D + dh * PER);
 #pragma unroll
-    for (int e = 0; e < PER; ++e) op[e] = f32_to_bf16(acc[e] * inv);
+    for (int e = 0; e < PER / 8; ++e) {
+        const f32x4_t x0 = acc[2 * e] * inv, x1 = acc[2 * e + 1] * inv;
+        op[e] = u32x4_t{pack_bf16x2(x0[0], x0[1]), pack_bf16x2(x0[2], x0[3]), pack_bf16x2(x1[0], x1[1]),
+                        pack_bf16x2(x1[2], x1[3])};
+    }
 }
 
 template <int D>
@@ -553,8 +589,7 @@ hipError_t launch_attention(const AttnArgs& args, hipStream_t s) {
     const unsigned grid = (unsigned)((int64_t)args.n_tiles * args.Hkv * args.n_chunks);
     hipLaunchKernelGGL(attention_kernel<D>, dim3(grid), dim3(256), 0, s, args);
     if (args.n_chunks > 1)
-        hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)((int64_t)args.n_tiles * args.Hkv * 32)), dim3(256), 0, s,
-                           args);
+        hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)((int64_t)args.n_tiles * args.Hkv)), dim3(256), 0, s, args);
     return hipGetLastError();
 }
 
