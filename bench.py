@@ -95,7 +95,7 @@ class Path:
         self.q_full = torch.empty((T, hq, D), dtype=bf, device=dev)
         self.out_full = torch.empty_like(self.q_full)
         self.sigma = torch.empty(T, dtype=torch.float32, device=dev)
-        ws = max(ss.qkv_rope_workspace_bytes(T, hkv, D, bf),
+        ws = max(ss.qkv_rope_workspace_bytes(T, hq, hkv, D, bf),
                  ss.prefill_attention_workspace_bytes(T, T, hq, hkv, D, bf))
         self.set_frac(0.25, ws_hint=ws)
 
@@ -110,7 +110,7 @@ class Path:
         self.q_sel = torch.empty((n, self.hq, self.D), dtype=bf, device="cuda")
         self.out_sel = torch.empty_like(self.q_sel)
         need = max(ws_hint,
-                   ss.qkv_rope_workspace_bytes(self.T, self.hkv, self.D, bf),
+                   ss.qkv_rope_workspace_bytes(self.T, self.hq, self.hkv, self.D, bf),
                    ss.prefill_attention_workspace_bytes(self.T, self.T, self.hq, self.hkv, self.D, bf),
                    ss.prefill_attention_workspace_bytes(n, self.T, self.hq, self.hkv, self.D, bf))
         self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")

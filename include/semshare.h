@@ -175,8 +175,8 @@ semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, i
                                     int32_t n_kv_heads, int32_t head_dim, double rope_base,
                                     void* q_out, float* deviation_out, void* workspace,
                                     size_t workspace_bytes, semshare_dtype_t dtype, void* stream);
-size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim,
-                                   semshare_dtype_t dtype);
+size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads,
+                                   int32_t head_dim, semshare_dtype_t dtype);
 
 /*
  * Step 2 of semshare_partial_prefill on its own (same kernels): causal

@@ -157,7 +157,7 @@ PrefillLayout prefill_layout(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, in
     PrefillLayout l{};
     l.off_q = 0;
     l.off_qkv = a256((size_t)n_sel * n_q_heads * head_dim * dtype_size(dtype));
-    l.off_attn = l.off_qkv + semshare::qkv_workspace_bytes(n_sel, n_kv_heads, head_dim, dtype);
+    l.off_attn = l.off_qkv + semshare::qkv_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dtype);
     l.total = l.off_attn + semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
     return l;
 }
@@ -178,9 +178,10 @@ float default_scale(float sm_scale, int32_t head_dim) {
 
 extern "C" {
 
-size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim, semshare_dtype_t dtype) {
-    if (!dtype_ok(dtype) || n_sel < 0 || n_kv_heads <= 0 || head_dim <= 0) return 0;
-    return semshare::qkv_workspace_bytes(n_sel, n_kv_heads, head_dim, dtype);
+size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                   semshare_dtype_t dtype) {
+    if (!dtype_ok(dtype) || n_sel < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return 0;
+    return semshare::qkv_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dtype);
 }
 
 size_t semshare_prefill_attention_workspace(int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
@@ -216,7 +217,7 @@ semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, i
     if (!aligned16(x_sel) || !aligned16(wk) || !aligned16(wv) || !aligned16(k_cache) || !aligned16(v_cache) ||
         (q_out && (!aligned16(wq) || !aligned16(q_out))))
         return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
-    st = check_workspace(fn, workspace, workspace_bytes, semshare::qkv_workspace_bytes(n_sel, n_kv_heads, head_dim, dtype));
+    st = check_workspace(fn, workspace, workspace_bytes, semshare::qkv_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dtype));
     if (st != SEMSHARE_OK) return st;
     const semshare::QkvArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden, n_q_heads,
                               n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace};

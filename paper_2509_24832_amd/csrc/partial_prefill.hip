@@ -5,12 +5,7 @@
 //  1. prep        RoPE (cos, sin) table for the selected positions, one entry
 //                 per (row, pair) shared by all heads and by q and k; zeroes
 //                 the deviation sums.
-//  2. qkv_gemm    [n_sel, hidden] x [Wq;Wk;Wv]^T on v_mfma_f32_32x32x16_bf16,
-//                 128x128x64 tiles, LDS double buffering.  Epilogue through an
-//                 fp32 LDS tile: RoPE of q/k pairs, bf16 rounding, q to the
-//                 workspace, k/v scattered into the cache rows sel_pos (after
-//                 reading the old row for the deviation sums).  Tiles are
-//                 mapped XCD-major so the M tiles of one weight tile share an L2.
+//  2. qkv_gemm    projection + RoPE + deviation + cache scatter (qkv_gemm.hip).
 //  3. dev_final   sigma = sqrt(sum dK^2) + sqrt(sum dV^2).
 //  4. attention   flash-style causal GQA attention of the selected rows over
 //                 the assembled cache.  A workgroup owns one kv head and 128
@@ -62,200 +57,6 @@ __global__ void dev_final_kernel(const float* __restrict__ parts, float* __restr
         sv += parts[(2 * i + 1) * n_parts + j];
     }
     dev[i] = sqrtf(sk) + sqrtf(sv);
-}
-
-// ------------------------------------------------------------------ QKV GEMM
-
-constexpr int GBM = 128, GBN = 128, GBK = 64;
-constexpr int GLDA = GBK + 8;   // bf16 per LDS operand row (144 B: conflict-free 16-B reads)
-constexpr int GLDC = GBN + 8;   // floats per LDS epilogue row
-constexpr int kGemmOperandBytes = 2 * (GBM + GBN) * GLDA * 2;
-constexpr int kGemmEpilogueBytes = GBM * GLDC * 4;
-constexpr int kGemmLdsBytes = kGemmOperandBytes > kGemmEpilogueBytes ? kGemmOperandBytes : kGemmEpilogueBytes;
-
-struct GemmArgs {
-    const uint16_t* x;      // [n_sel][hidden]
-    const int32_t* pos;     // [n_sel]
-    const uint16_t* w[3];   // Wq, Wk, Wv  (rows = output features)
-    int32_t seg_tiles[3];   // n-tiles per segment (0 for q in K/V-only mode)
-    int32_t seg_cols[3];    // output columns per segment
-    int32_t n_nt, n_mt;
-    int64_t n_sel, n_tok;
-    int32_t hidden, D;
-    uint16_t* q_out;        // [n_sel][Hq*D]
-    uint16_t* kv[2];        // k_cache, v_cache [n_tok][Hkv*D]
-    const float2* rope;     // [n_sel][D/2]
-    float* dev_parts;       // [n_sel][2][Hkv*D/128] squared-difference sums, or null
-};
-
-__device__ __forceinline__ void gemm_load_regs(const uint16_t* p, u32x4_t (&r)[4]) {
-    const u32x4_t* q = reinterpret_cast<const u32x4_t*>(p);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) r[i] = q[i];
-}
-
-__device__ __forceinline__ void gemm_store_lds(uint16_t* p, const u32x4_t (&r)[4]) {
-    u32x4_t* q = reinterpret_cast<u32x4_t*>(p);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) q[i] = r[i];
-}
-
-__global__ __launch_bounds__(256, 2) void qkv_gemm_kernel(GemmArgs g) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[kGemmLdsBytes];
-    uint16_t* As = reinterpret_cast<uint16_t*>(smem);
-    uint16_t* Bs = As + 2 * GBM * GLDA;
-
-    // XCD-major tile order: workgroup b runs on XCD b % 8; all M tiles of one
-    // N (weight) tile go to the same XCD, consecutively.
-    const int b = blockIdx.x;
-    const int xcd = b & 7;
-    const int j = b >> 3;
-    const int n_idx = xcd + 8 * (j / g.n_mt);
-    const int m_idx = j % g.n_mt;
-    if (n_idx >= g.n_nt) return;
-    int seg = 0, nt = n_idx;
-    if (nt >= g.seg_tiles[0]) {
-        nt -= g.seg_tiles[0];
-        seg = 1;
-        if (nt >= g.seg_tiles[1]) { nt -= g.seg_tiles[1]; seg = 2; }
-    }
-    const uint16_t* wseg = seg == 0 ? g.w[0] : (seg == 1 ? g.w[1] : g.w[2]);
-    uint16_t* kvseg = seg == 2 ? g.kv[1] : g.kv[0];
-    const int seg_cols = seg == 0 ? g.seg_cols[0] : g.seg_cols[1];
-    const int64_t m0 = (int64_t)m_idx * GBM;
-    const int32_t ncol0 = nt * GBN;  // first column within the segment
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int half = lane >> 5, l32 = lane & 31;
-    const int wm = wave >> 1, wn = wave & 1;
-
-    // global -> register assignment: 2 threads per row, 64 B each
-    const int lrow = tid >> 1, lk = (tid & 1) * 32;
-    int64_t arow = m0 + lrow;
-    if (arow > g.n_sel - 1) arow = g.n_sel - 1;  // tail rows: computed, never stored
-    const uint16_t* a_src = g.x + arow * g.hidden + lk;
-    const uint16_t* b_src = wseg + (int64_t)(ncol0 + lrow) * g.hidden + lk;
-    const int lds_off = lrow * GLDA + lk;
-
-    f32x16_t acc[2][2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int k = 0; k < 2; ++k) acc[i][k] = f32x16_t{};
-
-    u32x4_t ra[4], rb[4];
-    gemm_load_regs(a_src, ra);
-    gemm_load_regs(b_src, rb);
-    gemm_store_lds(As + lds_off, ra);
-    gemm_store_lds(Bs + lds_off, rb);
-    __syncthreads();
-
-    const int nk = g.hidden / GBK;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            gemm_load_regs(a_src + (kt + 1) * GBK, ra);
-            gemm_load_regs(b_src + (kt + 1) * GBK, rb);
-        }
-        const uint16_t* Ab = As + buf * GBM * GLDA;
-        const uint16_t* Bb = Bs + buf * GBN * GLDA;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            bf16x8_t av[2], bv[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                av[i] = *reinterpret_cast<const bf16x8_t*>(Ab + (64 * wm + 32 * i + l32) * GLDA + 32 * half + 8 * s);
-                bv[i] = *reinterpret_cast<const bf16x8_t*>(Bb + (64 * wn + 32 * i + l32) * GLDA + 32 * half + 8 * s);
-            }
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int k = 0; k < 2; ++k)
-                    acc[i][k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[k], acc[i][k], 0, 0, 0);
-        }
-        if (more) {
-            gemm_store_lds(As + (buf ^ 1) * GBM * GLDA + lds_off, ra);
-            gemm_store_lds(Bs + (buf ^ 1) * GBN * GLDA + lds_off, rb);
-        }
-        __syncthreads();
-    }
-
-    // ---- epilogue: accumulators -> fp32 LDS tile
-    float* Cs = reinterpret_cast<float*>(smem);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int k = 0; k < 2; ++k)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int r = 64 * wm + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
-                const int c = 64 * wn + 32 * k + l32;
-                Cs[r * GLDC + c] = acc[i][k][v];
-            }
-    __syncthreads();
-
-    const int half_d = g.D / 2;
-#pragma unroll 1
-    for (int ps = 0; ps < (GBM * GBN / 8) / 256; ++ps) {
-        const int item = ps * 256 + tid;
-        const int r = item >> 4, cg = item & 15;
-        const int64_t m = m0 + r;
-        const int32_t n = ncol0 + 8 * cg;  // column within the segment
-        float v8[8];
-        {
-            const float4 c0 = *reinterpret_cast<const float4*>(Cs + r * GLDC + 8 * cg);
-            const float4 c1 = *reinterpret_cast<const float4*>(Cs + r * GLDC + 8 * cg + 4);
-            v8[0] = c0.x; v8[1] = c0.y; v8[2] = c0.z; v8[3] = c0.w;
-            v8[4] = c1.x; v8[5] = c1.y; v8[6] = c1.z; v8[7] = c1.w;
-        }
-        float dsum = 0.0f;
-        if (m < g.n_sel) {
-            const int32_t p = g.pos[m];
-            if (seg < 2) {  // RoPE on q and k: pairs (2k, 2k+1) within the head
-                const int32_t k0 = (n % g.D) >> 1;
-                const float2* cs = g.rope + m * half_d + k0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float2 t = cs[e];
-                    const float x0 = v8[2 * e], x1 = v8[2 * e + 1];
-                    v8[2 * e] = t.x * x0 - t.y * x1;
-                    v8[2 * e + 1] = t.y * x0 + t.x * x1;
-                }
-            }
-            u32x4_t packed;
-            packed.x = pack_bf16x2(v8[0], v8[1]);
-            packed.y = pack_bf16x2(v8[2], v8[3]);
-            packed.z = pack_bf16x2(v8[4], v8[5]);
-            packed.w = pack_bf16x2(v8[6], v8[7]);
-            if (seg == 0) {
-                *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
-            } else if (p >= 0 && p < g.n_tok) {
-                uint16_t* dst = kvseg + (int64_t)p * seg_cols + n;
-                if (g.dev_parts) {
-                    const u32x4_t old = *reinterpret_cast<const u32x4_t*>(dst);
-                    const uint32_t ow[4] = {old.x, old.y, old.z, old.w};
-                    const uint32_t nw[4] = {packed.x, packed.y, packed.z, packed.w};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float d0 = bf16_lo(ow[e]) - bf16_lo(nw[e]);
-                        const float d1 = bf16_hi(ow[e]) - bf16_hi(nw[e]);
-                        dsum += d0 * d0 + d1 * d1;
-                    }
-                }
-                *reinterpret_cast<u32x4_t*>(dst) = packed;
-            }
-        }
-        if (g.dev_parts && seg > 0) {
-            // the 16 threads of one tile row are 16 consecutive lanes
-            dsum += __shfl_xor(dsum, 8, 16);
-            dsum += __shfl_xor(dsum, 4, 16);
-            dsum += __shfl_xor(dsum, 2, 16);
-            dsum += __shfl_xor(dsum, 1, 16);
-            const int n_parts = seg_cols / GBN;
-            if (cg == 0 && m < g.n_sel) g.dev_parts[(2 * m + (seg - 1)) * n_parts + nt] = dsum;
-        }
-    }
 }
 
 // ------------------------------------------------------------------ attention
@@ -599,14 +400,14 @@ size_t qkv_workspace_dev_offset(int64_t n_sel, int32_t head_dim, int dtype) {
     return dtype == SEMSHARE_BF16 ? align256((size_t)n_sel * (head_dim / 2) * sizeof(float2)) : 0;
 }
 
-int32_t qkv_dev_parts(int32_t n_kv_heads, int32_t head_dim, int dtype) {
+int32_t qkv_dev_parts(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype) {
     const int32_t cols = n_kv_heads * head_dim;
-    return dtype == SEMSHARE_BF16 ? cols / GBN : cols / 2;
+    return dtype == SEMSHARE_BF16 ? cols / qkv_gemm_bn(n_q_heads, n_kv_heads, head_dim) : cols / 2;
 }
 
-size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim, int dtype) {
+size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype) {
     return qkv_workspace_dev_offset(n_sel, head_dim, dtype) +
-           align256((size_t)n_sel * 2 * qkv_dev_parts(n_kv_heads, head_dim, dtype) * sizeof(float));
+           align256((size_t)n_sel * 2 * qkv_dev_parts(n_q_heads, n_kv_heads, head_dim, dtype) * sizeof(float));
 }
 
 AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
@@ -656,6 +457,7 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sel_pos, a.n_sel,
                            a.n_tok, half_d, log2(a.rope_base), rope);
     }
+    const int32_t bn = qkv_gemm_bn(a.n_q_heads, a.n_kv_heads, a.head_dim);
     GemmArgs g{};
     g.x = static_cast<const uint16_t*>(a.x_sel);
     g.pos = a.sel_pos;
@@ -664,10 +466,10 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     g.w[2] = static_cast<const uint16_t*>(a.wv);
     g.seg_cols[0] = a.n_q_heads * a.head_dim;
     g.seg_cols[1] = g.seg_cols[2] = a.n_kv_heads * a.head_dim;
-    g.seg_tiles[0] = a.q_out ? g.seg_cols[0] / GBN : 0;
-    g.seg_tiles[1] = g.seg_tiles[2] = g.seg_cols[1] / GBN;
+    g.seg_tiles[0] = a.q_out ? g.seg_cols[0] / bn : 0;
+    g.seg_tiles[1] = g.seg_tiles[2] = g.seg_cols[1] / bn;
     g.n_nt = g.seg_tiles[0] + g.seg_tiles[1] + g.seg_tiles[2];
-    g.n_mt = (int32_t)((a.n_sel + GBM - 1) / GBM);
+    g.n_mt = (int32_t)((a.n_sel + 127) / 128);
     g.n_sel = a.n_sel;
     g.n_tok = a.n_tok;
     g.hidden = a.hidden;
@@ -677,11 +479,11 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     g.kv[1] = static_cast<uint16_t*>(a.v_cache);
     g.rope = rope;
     g.dev_parts = dev_parts;
-    const int64_t per_xcd = (g.n_nt + 7) / 8;
-    hipLaunchKernelGGL(qkv_gemm_kernel, dim3((unsigned)(8 * per_xcd * g.n_mt)), dim3(256), 0, s, g);
+    launch_qkv_gemm(g, bn, s);
     if (a.deviation_out)
         hipLaunchKernelGGL(dev_final_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_parts,
-                           a.deviation_out, a.n_sel, qkv_dev_parts(a.n_kv_heads, a.head_dim, SEMSHARE_BF16));
+                           a.deviation_out, a.n_sel,
+                           qkv_dev_parts(a.n_q_heads, a.n_kv_heads, a.head_dim, SEMSHARE_BF16));
     return hipGetLastError();
 }
 

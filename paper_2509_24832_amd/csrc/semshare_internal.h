@@ -122,9 +122,27 @@ struct AttnPlan {
     size_t off_part_o, off_part_ml, off_used, total;
 };
 
-size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_kv_heads, int32_t head_dim, int dtype);
+size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);
 size_t qkv_workspace_dev_offset(int64_t n_sel, int32_t head_dim, int dtype);
-int32_t qkv_dev_parts(int32_t n_kv_heads, int32_t head_dim, int dtype);
+int32_t qkv_dev_parts(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);
+
+// The bf16 projection GEMM (qkv_gemm.hip).
+struct GemmArgs {
+    const uint16_t* x;     // [n_sel][hidden]
+    const int32_t* pos;    // [n_sel]
+    const uint16_t* w[3];  // Wq, Wk, Wv (rows = output features)
+    int32_t seg_tiles[3];  // BN-wide column tiles per segment (0 for q in K/V-only mode)
+    int32_t seg_cols[3];   // output columns per segment
+    int32_t n_nt, n_mt;
+    int64_t n_sel, n_tok;
+    int32_t hidden, D;
+    uint16_t* q_out;       // [n_sel][Hq*D]
+    uint16_t* kv[2];       // k_cache, v_cache [n_tok][Hkv*D]
+    const float2* rope;    // [n_sel][D/2] (cos, sin)
+    float* dev_parts;      // [n_sel][2][Hkv*D/BN] squared-difference sums, or null
+};
+int32_t qkv_gemm_bn(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim);
+hipError_t launch_qkv_gemm(const GemmArgs& g, int32_t bn, hipStream_t s);
 AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
                         int32_t head_dim, int dtype);
 

@@ -60,7 +60,7 @@ def load() -> ctypes.CDLL:
         "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
         "semshare_select_recompute": (I32, [P, I64, I64, P, P]),
         "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
-        "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32]),
+        "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_prefill_attention_workspace": (SZ, [I64, I64, I32, I32, I32, I32]),
     }
@@ -259,8 +259,9 @@ def partial_prefill(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[tor
     return out, deviation
 
 
-def qkv_rope_workspace_bytes(n_sel: int, n_kv_heads: int, head_dim: int, dtype: torch.dtype) -> int:
-    return int(load().semshare_qkv_rope_workspace(n_sel, n_kv_heads, head_dim,
+def qkv_rope_workspace_bytes(n_sel: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                             dtype: torch.dtype) -> int:
+    return int(load().semshare_qkv_rope_workspace(n_sel, n_q_heads, n_kv_heads, head_dim,
                                                   BF16 if dtype == torch.bfloat16 else FP32))
 
 
@@ -305,7 +306,7 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
         deviation = torch.empty(n_sel, dtype=torch.float32, device=x_sel.device)
     if not want_deviation:
         deviation = None
-    ws = _workspace(qkv_rope_workspace_bytes(n_sel, n_kv_heads, head_dim, dt), workspace, x_sel)
+    ws = _workspace(qkv_rope_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dt), workspace, x_sel)
     _call("semshare_qkv_rope", _ptr(x_sel), _ptr(sel_pos), n_sel, _ptr(wq) if want_q else None, _ptr(wk), _ptr(wv),
           _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, float(rope_base),
           _ptr(q_out), _ptr(deviation), _ptr(ws), 0 if ws is None else ws.numel(), _dt(x_sel), _stream())

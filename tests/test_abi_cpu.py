@@ -176,6 +176,6 @@ def test_split_call_validation(lib):
     assert L.semshare_prefill_attention(None, None, 0, None, None, 16, 8, 2, 128, 0.0, None, None, 0, 1, None) == b.OK
     # composition: the partial-prefill workspace covers q plus both steps
     W = L.semshare_partial_prefill_workspace(1280, 5120, 4096, 32, 8, 128, 1)
-    assert W >= 1280 * 32 * 128 * 2 + L.semshare_qkv_rope_workspace(1280, 8, 128, 1) + \
+    assert W >= 1280 * 32 * 128 * 2 + L.semshare_qkv_rope_workspace(1280, 32, 8, 128, 1) + \
         L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1)
     assert L.semshare_prefill_attention_workspace(5120, 5120, 32, 8, 128, 1) == 0  # no split needed at full length
