@@ -34,13 +34,19 @@ COMMON_FLAGS = [
 ]
 
 
+# Per-source extra flags.  attention.hip: scores and probabilities are finite
+# or -inf by construction (masked keys), so NaN-preserving max is not needed;
+# without this every fmaxf operand is first quieted with an extra v_max.
+EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans"]}
+
+
 def sources() -> List[str]:
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
 
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *COMMON_FLAGS, "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *COMMON_FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), "-x", "hip", "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

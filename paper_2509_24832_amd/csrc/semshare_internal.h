@@ -115,10 +115,10 @@ struct AttnCall {
 
 // Work decomposition and workspace partition of the attention step.
 struct AttnPlan {
-    int32_t rows_per_tile;  // selected rows per tile (128 / G for bf16)
+    int32_t rows_per_tile;  // selected rows per tile (256 / G for bf16)
     int64_t n_tiles;
-    int32_t chunk;          // keys per split-KV chunk (multiple of 64)
-    int32_t n_chunks;       // ceil(n_tok / chunk); 1 = no split
+    int32_t split_units;    // target split-KV piece length in 64-key tiles
+    int32_t n_chunks;       // most pieces per (tile, kv head); 1 = no split
     size_t off_part_o, off_part_ml, off_used, total;
 };
 

@@ -178,4 +178,5 @@ def test_split_call_validation(lib):
     W = L.semshare_partial_prefill_workspace(1280, 5120, 4096, 32, 8, 128, 1)
     assert W >= 1280 * 32 * 128 * 2 + L.semshare_qkv_rope_workspace(1280, 32, 8, 128, 1) + \
         L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1)
-    assert L.semshare_prefill_attention_workspace(5120, 5120, 32, 8, 128, 1) == 0  # no split needed at full length
+    assert L.semshare_prefill_attention_workspace(256, 256, 32, 8, 128, 1) == 0  # short key range: never split
+    assert L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1) > 0  # few row tiles: split-KV
