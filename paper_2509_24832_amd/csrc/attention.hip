@@ -524,51 +524,52 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     }
 }
 
-// Log-sum-exp merge of an item's pieces, in piece order.  Thread (wave, lane)
-// reads exactly the partial values attention thread (wave, lane) wrote.
+// Log-sum-exp merge of an item's pieces, in piece order.  One workgroup per
+// (item, wave slice, column block): the 32 columns x D values that attention
+// wave `wave` held in block nb, laid out as [i][r][lane] f32x4 per piece, so
+// every load is a coalesced 1 KB row.  Thread t handles lane t % 64 and the
+// (i, r) pairs t / 64 + 4k.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     constexpr int kMd = D / 32;
-    const int64_t item = blockIdx.x;  // tile * Hkv + g
+    constexpr int kPer = kMd;  // (i, r) pairs per thread: 4 * kMd / 4
+    const int64_t item = blockIdx.x >> 3;  // tile * Hkv + g
+    const int wave = (blockIdx.x >> 1) & 3, nb = blockIdx.x & 1;
     const int32_t nu = a.n_used[item];
     if (nu <= 1) return;
     const int tile = (int)(item / a.Hkv), g = (int)(item % a.Hkv);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, q4 = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
+    const int col = 64 * wave + 32 * nb + l32;
+    const int64_t row = (int64_t)tile * a.R + col % a.R;
+    if (row >= a.n_sel) return;
+    const int32_t p = a.pos[row];
+    if (p < 0 || p >= a.n_tok) return;
+    const int head = g * a.G + col / a.R;
     const float cl2 = a.cl2;
+    const float2* ml = a.part_ml + item * a.n_chunks * NCOL + col;
+    float M = -1.0e30f;
+    for (int c = 0; c < nu; ++c) M = fmaxf(M, ml[c * NCOL].x);
+    float L = 0.0f;
+    f32x4_t o[kPer];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int col = 64 * wave + 32 * nb + l32;
-        const int64_t row = (int64_t)tile * a.R + col % a.R;
-        if (row >= a.n_sel) continue;
-        const int32_t p = a.pos[row];
-        if (p < 0 || p >= a.n_tok) continue;
-        const int head = g * a.G + col / a.R;
-        const float2* ml = a.part_ml + item * a.n_chunks * NCOL + col;
-        float M = -1.0e30f;
-        for (int c = 0; c < nu; ++c) M = fmaxf(M, ml[c * NCOL].x);
-        float L = 0.0f;
-        f32x4_t o[kMd * 4];
+    for (int k = 0; k < kPer; ++k) o[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < nu; ++c) {
+        const float2 mlc = ml[c * NCOL];
+        const float w = __builtin_amdgcn_exp2f((mlc.x - M) * cl2);
+        L += w * mlc.y;
+        const f32x4_t* po = a.part_o + (((item * a.n_chunks + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
 #pragma unroll
-        for (int j = 0; j < kMd * 4; ++j) o[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < nu; ++c) {
-            const float2 mlc = ml[c * NCOL];
-            const float w = __builtin_amdgcn_exp2f((mlc.x - M) * cl2);
-            L += w * mlc.y;
-            const f32x4_t* po = a.part_o + (((item * a.n_chunks + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
+        for (int k = 0; k < kPer; ++k) o[k] += w * po[(q4 + 4 * k) * 64];
+    }
+    const float inv = 1.0f / L;
+    uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D;
 #pragma unroll
-            for (int j = 0; j < kMd * 4; ++j) o[j] += w * po[j * 64];
-        }
-        const float inv = 1.0f / L;
-        uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D;
-#pragma unroll
-        for (int i = 0; i < kMd; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const f32x4_t x = o[i * 4 + r] * inv;
-                *reinterpret_cast<u32x2_t*>(op + 32 * i + 8 * r + 4 * half) =
-                    u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
-            }
+    for (int k = 0; k < kPer; ++k) {
+        const int ir = q4 + 4 * k, i = ir >> 2, r = ir & 3;
+        const f32x4_t x = o[k] * inv;
+        *reinterpret_cast<u32x2_t*>(op + 32 * i + 8 * r + 4 * half) =
+            u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
     }
 }
 
@@ -576,7 +577,7 @@ template <int D>
 hipError_t launch(const AttnArgs& args, hipStream_t s) {
     const int64_t items = (int64_t)args.n_tiles * args.Hkv;
     hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(items * args.n_chunks)), dim3(256), 0, s, args);
-    if (args.n_chunks > 1) hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)items), dim3(256), 0, s, args);
+    if (args.n_chunks > 1) hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)(items * 8)), dim3(256), 0, s, args);
     return hipGetLastError();
 }
 
