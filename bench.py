@@ -53,8 +53,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "f91effdbbe12307be5590b77722dbd00fa5b692a5a4ce4866e8a28ef52eecbbb",
-                "bytes_per_call": 132286231}
+ATTN_TRAFFIC = {"source_sha256": "6a19640b63574401baaded7604abe2401f0c3488f9e1fc3d2ae98d3a38cfb438",
+                "bytes_per_call": 194044788}
 
 
 def source_sha256(rel):

@@ -51,7 +51,7 @@ constexpr int kStages = 4;   // K/V ring depth
 constexpr float kSumLimit = 65536.0f;  // 2^16
 constexpr int kCUs = 256;        // compute units of the chip
 constexpr int kMinPieceKt = 4;   // shortest split-KV piece, in 64-key tiles
-constexpr double kSplitShares = 2.0;  // split-KV piece target, in CU shares of work
+constexpr double kSplitShares = 0.75;  // split-KV piece target, in CU shares of work
 
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -88,17 +88,26 @@ struct ACfg {
     static constexpr int kKs = D / 16;                 // k-steps of S^T
 };
 
-// 16 bytes per lane from global memory straight into LDS at lds_base +
-// 16 * lane (global_load_lds_dwordx4; M0 holds the wave-uniform base).
-// Issued as inline assembly on purpose: the compiler then does not treat the
-// transposing LDS reads that follow as dependent on these in-flight loads
-// (it would drain the whole ring with vmcnt(0) before each of them).  Stage
-// readiness is established explicitly instead (wait_vmcnt + ring_barrier),
-// and M0 is written only here in this kernel.
-__device__ __forceinline__ void g2lds(const void* g, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+// 16 bytes per lane from gbase + off (bytes, per lane) straight into LDS at
+// lds_base + 16 * lane (global_load_lds_dwordx4, M0 = the wave-uniform LDS
+// base, scalar base address + 32-bit lane offset).  Issued as inline assembly
+// on purpose: the compiler then does not treat the transposing LDS reads that
+// follow as dependent on these in-flight loads (it would drain the whole ring
+// with vmcnt(0) before each of them).  Stage readiness is established
+// explicitly instead (wait_vmcnt + ring_barrier), and M0 is written only here
+// in this kernel.
+__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
+    // the scalar operands are wave-uniform by construction; readfirstlane
+    // places them in scalar registers
+    // (readfirstlane returns int: both halves go through uint32_t so the low
+    // half is zero-extended, never sign-extended into the high half)
+    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                  :
-                 : "v"(g), "s"(lds_base)
+                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
                  : "memory", "m0");
 }
 
@@ -167,7 +176,7 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
         if (lane == 0) { s_pmin = mn; s_pmax = mx; }
     }
     __syncthreads();
-    const int32_t pmin = s_pmin, pmax = s_pmax;
+    const int32_t pmin = __builtin_amdgcn_readfirstlane(s_pmin), pmax = __builtin_amdgcn_readfirstlane(s_pmax);
     // this item's pieces: n_pieces runs of piece_kt whole tiles over [0, pmax]
     const int32_t item_kt = (pmax + KT) / KT;
     int32_t n_pieces = min((item_kt + a.split_units - 1) / a.split_units, a.n_chunks);
@@ -225,16 +234,39 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
         ld_vc[i] = 8 * (pc ^ (2 * (r & (C::kNch / 2 - 1))));
     }
     const uint32_t smem_base = lds_addr(smem);
-    auto issue = [&](int t) {
+    // Loads of one 64-key tile: scalar bases of its first key row, per-lane
+    // byte offsets of this wave's rows (clamped to the last key), LDS base.
+    struct TileLoads {
+        const uint16_t* kg;
+        const uint16_t* vg;
+        uint32_t off_k[C::kLoadsPerWave], off_v[C::kLoadsPerWave];
+        uint32_t lds;
+    };
+    auto prep_tile = [&](int t, TileLoads& d) {
         const int32_t key0 = kbeg + t * KT;
-        const uint32_t st = smem_base + (t % kStages) * C::kStage;
+        d.kg = kbase + (int64_t)key0 * row_stride;
+        d.vg = vbase + (int64_t)key0 * row_stride;
+        const int32_t lim = last_key - key0;
 #pragma unroll
         for (int i = 0; i < C::kLoadsPerWave; ++i) {
-            const int64_t kk = min(key0 + ld_row[i], last_key);
-            const uint32_t dst = __builtin_amdgcn_readfirstlane(st + (wave * C::kLoadsPerWave + i) * 1024);
-            g2lds(kbase + kk * row_stride + ld_kc[i], dst);
-            g2lds(vbase + kk * row_stride + ld_vc[i], dst + C::kTileBytes);
+            const uint32_t r = (uint32_t)min(ld_row[i], lim);
+            d.off_k[i] = (r * (uint32_t)row_stride + (uint32_t)ld_kc[i]) * 2u;
+            d.off_v[i] = (r * (uint32_t)row_stride + (uint32_t)ld_vc[i]) * 2u;
         }
+        d.lds = __builtin_amdgcn_readfirstlane(smem_base + (t % kStages) * C::kStage +
+                                               wave * C::kLoadsPerWave * 1024);
+    };
+    // load n of the tile (n in [0, kLoads)): K for even n, V for odd n, rows of load n/2
+    auto issue_one = [&](const TileLoads& d, int n) {
+        const int i = n >> 1;
+        if (n & 1) g2lds(d.vg, d.off_v[i], d.lds + i * 1024 + C::kTileBytes);
+        else g2lds(d.kg, d.off_k[i], d.lds + i * 1024);
+    };
+    auto issue = [&](int t) {
+        TileLoads d;
+        prep_tile(t, d);
+#pragma unroll
+        for (int n = 0; n < C::kLoads; ++n) issue_one(d, n);
     };
 
     // ---- LDS read offsets (bytes within a stage)
@@ -392,6 +424,8 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
             if (T + 1 < n_kt) wait_vmcnt<C::kLoads>();
             else wait_vmcnt<0>();
             ring_barrier();
+            // all loads of tile T+2 at once: spreading them over the MFMA slots
+            // costs more (each load holds up the in-order issue of its wave)
             if (T + 2 < n_kt) issue(T + 2);
         }
         if (!has_prev) {
@@ -400,59 +434,96 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
             s_mfma(kf, nxt);
             exp_pack(cur, pc, ts);
         } else {
-            // Steady state, in kKs fenced steps.  Step j: the K and V fragments
-            // of step j+2 are requested, S^T k-step j and PV step j run on the
-            // matrix cores for both column blocks, and 32/kKs of this lane's
-            // probabilities of sub-tile u are formed.  The fences fix this
-            // order, so LDS latency hides behind two steps of MFMAs and the
-            // exponentials run beside them.
-            constexpr int kSteps = C::kKs;  // == 2 * kMd PV steps
-            constexpr int kVals = 32 / kSteps;
+            // Steady state as a software pipeline of 4*kKs slots.  Slot k
+            // issues one MFMA, fenced off on its own: k%4 = 0, 1 are S^T
+            // k-step k/4 for column blocks 0, 1; k%4 = 2, 3 are PV step k/4.
+            // A fenced group of VALU work follows it: the scaled scores of
+            // this slot's values, the exponentials of the previous slot's, a
+            // bf16 pair conversion and a row-sum update further behind, and
+            // one LDS request for step k/4 + 2.  The strict alternation keeps
+            // the matrix pipe fed while the softmax arithmetic runs in its
+            // shadow, and no operation waits on its immediate predecessor.
+            constexpr int kSlots = 4 * C::kKs;
+            constexpr int kV = 32 / kSlots;  // probabilities formed per slot (1 or 2)
+            auto cvt_slot = [](int q) { return (2 * q + 1) / kV + 2; };
             const unsigned char* kb = stage_of(u + 1) + ((u + 1) & 1) * 32 * C::kRowBytes;
             const unsigned char* vb = stage_of(u - 1) + C::kTileBytes + ((u - 1) & 1) * 32 * C::kRowBytes;
-            auto rk = [&](int j) { return *reinterpret_cast<const bf16x8_t*>(kb + k_ro[j]); };
-            auto rv = [&](int j) {
-                const unsigned char* p0 = vb + (16 * (j / C::kMd)) * C::kRowBytes + v_ro[j % C::kMd];
-                const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0);
-                const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p0 + 8 * C::kRowBytes));
-                const u32x2_t wl = __builtin_bit_cast(u32x2_t, lo), wh = __builtin_bit_cast(u32x2_t, hi);
-                return __builtin_bit_cast(bf16x8_t, u32x4_t{wl[0], wl[1], wh[0], wh[1]});
+            // one address per K fragment and per V row block; the V half-steps
+            // are immediate offsets from it
+            const unsigned char* ka[C::kKs];
+            const unsigned char* va[C::kMd];
+#pragma unroll
+            for (int j = 0; j < C::kKs; ++j) ka[j] = kb + k_ro[j];
+#pragma unroll
+            for (int md = 0; md < C::kMd; ++md) va[md] = vb + v_ro[md];
+            auto rk = [&](int j) { return *reinterpret_cast<const bf16x8_t*>(ka[j]); };
+            auto rv = [&](int j, int hi) {
+                const unsigned char* p0 = va[j % C::kMd] + (16 * (j / C::kMd) + 8 * hi) * C::kRowBytes;
+                return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0));
             };
-            const float mc0 = m_run[0] * cl2, mc1 = m_run[1] * cl2;
+            const float mc[2] = {m_run[0] * cl2, m_run[1] * cl2};
             const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
-            u32x4_t pw[2][2];
+            float fv[32], ev[32];
+            uint32_t pw[16];
+            bf16x8_t kf[C::kKs];
+            u32x2_t vl[C::kKs], vh[C::kKs];
             ts[0] = ts[1] = 0.0f;
             nxt[0] = nxt[1] = f32x16_t{};
-            bf16x8_t kf[kSteps], vf[kSteps];
-            kf[0] = rk(0); vf[0] = rv(0);
-            kf[1] = rk(1); vf[1] = rv(1);
 #pragma unroll
-            for (int j = 0; j < kSteps; ++j) {
-                if (j + 2 < kSteps) { kf[j + 2] = rk(j + 2); vf[j + 2] = rv(j + 2); }
+            for (int j = 0; j < 2 && j < C::kKs; ++j) {
+                kf[j] = rk(j);
+                vl[j] = rv(j, 0);
+                vh[j] = rv(j, 1);
+            }
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
-                    nxt[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[j], qf[nb][j], nxt[nb], 0, 0, 0);
+            for (int k = 0; k < kSlots; ++k) {
+                const int j = k >> 2, kind = k & 3;
+                if (kind < 2) {
+                    nxt[kind] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[j], qf[kind][j], nxt[kind], 0, 0, 0);
+                } else {
+                    const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4_t{vl[j][0], vl[j][1], vh[j][0], vh[j][1]});
+                    f32x16_t& o = oacc[kind - 2][j % C::kMd];
+                    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pp[kind - 2][j / C::kMd], o, 0, 0, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if (j + 2 < C::kKs) {
+                    if (kind == 0) kf[j + 2] = rk(j + 2);
+                    if (kind == 1) vl[j + 2] = rv(j + 2, 0);
+                    if (kind == 2) vh[j + 2] = rv(j + 2, 1);
+                }
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
-                    oacc[nb][j % C::kMd] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        vf[j], pp[nb][j / C::kMd], oacc[nb][j % C::kMd], 0, 0, 0);
+                for (int v = 0; v < kV; ++v) {
+                    const int f = k * kV + v;  // value f: column block f/16, S^T register f%16
+                    fv[f] = fmaf(cur[f >> 4][f & 15], cl2, -mc[f >> 4]);
+                    if (k > 0) ev[f - kV] = __builtin_amdgcn_exp2f(fv[f - kV]);
+                }
 #pragma unroll
-                for (int x = 0; x < kVals; x += 2) {
-                    const int f = j * kVals + x;  // flat (nb, sp, e) index
-                    const int nb = f >> 4, sp = (f >> 3) & 1, e = f & 7;
-                    const float mc = nb ? mc1 : mc0;
-                    const float p0 = __builtin_amdgcn_exp2f(fmaf(cur[nb][8 * sp + e], cl2, -mc));
-                    const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[nb][8 * sp + e + 1], cl2, -mc));
-                    const bf16x2_t pk = __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t);
-                    pw[nb][sp][e >> 1] = __builtin_bit_cast(uint32_t, pk);
-                    ts[nb] = __builtin_amdgcn_fdot2_f32_bf16(pk, one, ts[nb], false);
+                for (int q = 0; q < 16; ++q) {
+                    if (cvt_slot(q) == k)
+                        pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
+                    if (cvt_slot(q) + 1 == k)
+                        ts[q >> 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[q]), one, ts[q >> 3], false);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
+            // drain: the last slot's exponentials, conversions and sums
+#pragma unroll
+            for (int f = (kSlots - 1) * kV; f < 32; ++f) ev[f] = __builtin_amdgcn_exp2f(fv[f]);
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                if (cvt_slot(q) >= kSlots)
+                    pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                if (cvt_slot(q) + 1 >= kSlots)
+                    ts[q >> 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[q]), one, ts[q >> 3], false);
+            // word q = (nb, sp, w) with q = 8 nb + 4 sp + w
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-                for (int sp = 0; sp < 2; ++sp) pc[nb][sp] = __builtin_bit_cast(bf16x8_t, pw[nb][sp]);
+                for (int sp = 0; sp < 2; ++sp)
+                    pc[nb][sp] = __builtin_bit_cast(bf16x8_t, u32x4_t{pw[8 * nb + 4 * sp], pw[8 * nb + 4 * sp + 1],
+                                                                      pw[8 * nb + 4 * sp + 2], pw[8 * nb + 4 * sp + 3]});
         }
         settle(cur, pc, ts);
         mask(u + 1, nxt);
@@ -596,15 +667,22 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
     p.n_chunks = 1;
     if (dtype == SEMSHARE_BF16 && n_sel > 0) {
         // Work estimate in 64-key tiles with the selected rows spread over the
-        // prompt (a tile's causal range then averages half of it).  Only items
-        // longer than twice one CU's share are cut (fewer, longer pieces keep
-        // the partial-result traffic low; measured best between 1.5x and 2x),
-        // never into pieces shorter than 4 tiles.
+        // prompt (a tile's causal range then averages half of it).  Items
+        // longer than 3/4 of one CU's share are cut into equal pieces (shorter
+        // pieces balance the CUs better but cost partial-result traffic and a
+        // prologue each; 3/4 measured best at 5k tokens), never shorter than
+        // 4 tiles.
         const double share = (double)p.n_tiles * n_kv_heads * (n_kt + 1) / 2.0 / kCUs;
         const int64_t su = std::max<int64_t>(kMinPieceKt, (int64_t)(share * kSplitShares));
         if (su < n_kt) {
             p.split_units = (int32_t)su;
             p.n_chunks = (int32_t)((n_kt + su - 1) / su);
+            // Items with fewer pieces leave their trailing chunk slots empty.
+            // At an even stride those empty workgroups line up with the
+            // dispatcher's round-robin over the shader engines of an XCD and
+            // the real ones all land on half of its CUs (measured 1.6x slower);
+            // an odd stride spreads them.
+            if (p.n_chunks % 2 == 0) p.n_chunks += 1;
         }
     }
     size_t off = 0;
