@@ -28,7 +28,8 @@
 // nothing can overflow; otherwise (the first sub-tile, where m is still
 // unset, and large upward jumps later) the sub-tile's true maximum becomes
 // the new m, O and l are rescaled and the probabilities formed again.  The
-// normaliser l sums the bf16-rounded p that the PV product consumes.
+// normaliser l sums the fp32 p (the PV product consumes them rounded to bf16;
+// a v_dot2c sum of the rounded pairs is a serial chain that cost ~20% here).
 //
 // Split-KV.  A (row tile, kv head) item whose causal key range is long
 // relative to the chip's share of work is cut into equal pieces of whole
@@ -129,14 +130,6 @@ __device__ __forceinline__ void ring_barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-}
-
-__device__ __forceinline__ float sum_bf16x8(bf16x8_t v, float acc) {
-    const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{v[2 * i], v[2 * i + 1]}, one, acc, false);
-    return acc;
 }
 
 template <int D>
@@ -363,7 +356,8 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[nb][8 * sp + e], cl2, -mc));
                 pb[nb][sp] = __builtin_convertvector(pv, bf16x8_t);
-                ts[nb] = sum_bf16x8(pb[nb][sp], ts[nb]);
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) ts[nb] += pv[e] + pv[e + 1];
             }
         }
     };
@@ -462,7 +456,6 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
                 return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0));
             };
             const float mc[2] = {m_run[0] * cl2, m_run[1] * cl2};
-            const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
             float fv[32], ev[32];
             uint32_t pw[16];
             bf16x8_t kf[C::kKs];
@@ -501,8 +494,7 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
                 for (int q = 0; q < 16; ++q) {
                     if (cvt_slot(q) == k)
                         pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
-                    if (cvt_slot(q) + 1 == k)
-                        ts[q >> 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[q]), one, ts[q >> 3], false);
+                    if (cvt_slot(q) + 1 == k) ts[q >> 3] += ev[2 * q] + ev[2 * q + 1];
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -515,8 +507,7 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
                     pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
 #pragma unroll
             for (int q = 0; q < 16; ++q)
-                if (cvt_slot(q) + 1 >= kSlots)
-                    ts[q >> 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[q]), one, ts[q >> 3], false);
+                if (cvt_slot(q) + 1 >= kSlots) ts[q >> 3] += ev[2 * q] + ev[2 * q + 1];
             // word q = (nb, sp, w) with q = 8 nb + 4 sp + w
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb)
