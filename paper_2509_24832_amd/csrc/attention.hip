@@ -31,12 +31,18 @@
 // normaliser l sums the fp32 p (the PV product consumes them rounded to bf16;
 // a v_dot2c sum of the rounded pairs is a serial chain that cost ~20% here).
 //
-// Split-KV.  A (row tile, kv head) item whose causal key range is long
-// relative to the chip's share of work is cut into equal pieces of whole
-// 64-key tiles (the piece count follows from the tile's largest position, so
-// short items stay whole); each piece writes its (m, l, O) to the workspace
-// in the order its registers hold them (coalesced), and a combine kernel
-// merges the pieces by log-sum-exp in piece order.
+// Work division (stream-K over keys).  The unit of work is one 64-key tile
+// of one row tile's causal range: a row tile whose largest valid position is
+// pmax has pmax/64 + 1 units, the same for every kv head.  A plan kernel lays
+// the row tiles end to end, each preceded by kSegCost units standing for the
+// fixed cost of starting it (W positions per head), and cuts the line into P
+// equal contiguous ranges, one workgroup (one CU) each, so the CUs finish
+// together whatever the mix of short and long causal ranges.  A workgroup
+// walks its range one segment (the part of a row tile inside it) at a time.  A row
+// tile inside a single range writes its output directly; the pieces of a row
+// tile that range boundaries cut write (m, l, O) in register order
+// (coalesced) to slots the plan assigns, and a combine kernel merges them by
+// log-sum-exp in piece order (deterministic).
 #include <algorithm>
 #include <climits>
 
@@ -51,8 +57,11 @@ constexpr int NCOL = 256;    // query columns per workgroup
 constexpr int kStages = 4;   // K/V ring depth
 constexpr float kSumLimit = 65536.0f;  // 2^16
 constexpr int kCUs = 256;        // compute units of the chip
-constexpr int kMinPieceKt = 4;   // shortest split-KV piece, in 64-key tiles
-constexpr double kSplitShares = 0.75;  // split-KV piece target, in CU shares of work
+constexpr int kPlanHdr = 4;      // plan header: W, ranges, split row tiles, slots used
+// Fixed cost of a segment (Q and first K/V loads before the key loop, the
+// output or partial-result stores after it) in units of one 64-key tile of
+// the key loop (measured ~14 us against ~2 us per unit at 256 columns x D 128).
+constexpr int32_t kSegCost = 6;
 
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -64,14 +73,18 @@ struct AttnArgs {
     const uint16_t* k_cache;  // [n_tok][Hkv][D]
     const uint16_t* v_cache;
     uint16_t* out;            // [n_sel][Hq][D]
-    f32x4_t* part_o;          // [items][n_chunks][NCOL * D / 4], register-native order
-    float2* part_ml;          // [items][n_chunks][NCOL]  (m, l)
-    int32_t* n_used;          // [items]: pieces of the item
+    f32x4_t* part_o;          // [Hkv][max_slots][NCOL * D / 4], register-native order
+    float2* part_ml;          // [Hkv][max_slots][NCOL]  (m, l)
+    // plan (int32): header [kPlanHdr] = W, ranges P', split row tiles, slots;
+    // ranges [P][4] = first unit, end unit, first row tile, piece index of
+    // its first segment; row tiles [n_tiles][8] = first unit, end unit, pmin,
+    // pmax, slot base, pieces, -, -; split row tiles [P]
+    int32_t* plan;
     int64_t n_sel, n_tok;
     int32_t Hq, Hkv, G, R;
     int32_t n_tiles;
-    int32_t split_units;      // target piece length in 64-key tiles
-    int32_t n_chunks;         // most pieces an item can have (grid dimension)
+    int32_t P;                // ranges (workgroups) per kv head
+    int32_t max_slots;        // partial-result slots per kv head
     float cl2;                // sm_scale * log2(e)
 };
 
@@ -132,82 +145,50 @@ __device__ __forceinline__ void ring_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// One segment: keys [kbeg, kend) of row tile `tile` for kv head g (kend <=
+// pmax + 1; pmin = the tile's smallest valid position).  slot < 0: the
+// segment is the whole causal range and writes the output; otherwise it
+// writes its (m, l, O) to partial-result slot `slot` of head g.
 template <int D>
-__global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
+__device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, const int g, const int tile,
+                                        const int32_t kbeg, const int32_t kend, const int32_t pmin, const int slot) {
     using C = ACfg<D>;
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[C::kLds];
-    __shared__ int32_t s_pos[NCOL];
-    __shared__ int32_t s_pmin, s_pmax;
-
-    const int b = blockIdx.x;
-    const int g = b % a.Hkv;  // kv head; with 8 kv heads each XCD serves one (its K/V stay in that L2)
-    const int jj = b / a.Hkv;
-    const int tile = a.n_tiles - 1 - jj / a.n_chunks;  // longest (latest) tiles first
-    const int chunk_id = jj % a.n_chunks;
-    const int tid = threadIdx.x, lane = tid & 63;
+    // the lane id through an opaque copy: nothing derived from it is hoisted
+    // out of the segment loop (it would stay live through the key loop)
+    int tid = (int)threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = lane >> 5, l32 = lane & 31;
 
-    if (tid < a.R) {
-        const int64_t r = (int64_t)tile * a.R + tid;
-        int32_t p = r < a.n_sel ? a.pos[r] : -1;
-        if (p < 0 || p >= a.n_tok) p = -1;
-        s_pos[tid] = p;
-    }
-    __syncthreads();
-    if (wave == 0) {
-        int32_t mn = INT_MAX, mx = -1;
-        for (int i = lane; i < a.R; i += 64) {
-            const int32_t p = s_pos[i];
-            if (p >= 0) { mn = min(mn, p); mx = max(mx, p); }
-        }
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) {
-            mn = min(mn, __shfl_xor(mn, o));
-            mx = max(mx, __shfl_xor(mx, o));
-        }
-        if (lane == 0) { s_pmin = mn; s_pmax = mx; }
-    }
-    __syncthreads();
-    const int32_t pmin = __builtin_amdgcn_readfirstlane(s_pmin), pmax = __builtin_amdgcn_readfirstlane(s_pmax);
-    // this item's pieces: n_pieces runs of piece_kt whole tiles over [0, pmax]
-    const int32_t item_kt = (pmax + KT) / KT;
-    int32_t n_pieces = min((item_kt + a.split_units - 1) / a.split_units, a.n_chunks);
-    const int32_t piece_kt = (item_kt + n_pieces - 1) / max(n_pieces, 1);
-    n_pieces = (item_kt + piece_kt - 1) / max(piece_kt, 1);
-    const int64_t item = (int64_t)tile * a.Hkv + g;
-    if (chunk_id == 0 && tid == 0 && a.n_chunks > 1) a.n_used[item] = pmax < 0 ? 0 : n_pieces;
-    const int32_t kbeg = chunk_id * piece_kt * KT;
-    const int32_t kend = min(kbeg + piece_kt * KT, pmax + 1);
-    if (pmax < 0 || kbeg >= kend) return;  // no row of the tile reaches this piece
-
-    // this lane's two query columns
-    int col[2], head[2];
+    // this lane's two query columns: column c of the tile is row c % R of
+    // it, query head g*G + c / R
     int64_t row[2];
     int32_t p_l[2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-        col[nb] = 64 * wave + 32 * nb + l32;
-        const int row_local = col[nb] % a.R;
-        row[nb] = (int64_t)tile * a.R + row_local;
-        head[nb] = g * a.G + col[nb] / a.R;
-        p_l[nb] = s_pos[row_local];
+        const int c = 64 * wave + 32 * nb + l32;
+        row[nb] = (int64_t)tile * a.R + c % a.R;
+        p_l[nb] = row[nb] < a.n_sel ? a.pos[row[nb]] : -1;  // checked below, after the Q loads are out
     }
-    // Q^T operands: lane half h holds d in [h*D/2, h*D/2 + D/2)
-    bf16x8_t qf[2][C::kKs];
+    // Q^T operands: lane half h holds d in [h*D/2, h*D/2 + D/2).  All loads
+    // are issued here, together with the positions; they move to the
+    // accumulation registers (zeroed for columns without a position) once
+    // the first K/V tile is on its way as well.
+    u32x4_t qv[2][C::kKs];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
+        const int c = 64 * wave + 32 * nb + l32;
         const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(
-            a.q + ((p_l[nb] >= 0 ? row[nb] : 0) * a.Hq + head[nb]) * (int64_t)D + half * (D / 2));
+            a.q + ((row[nb] < a.n_sel ? row[nb] : 0) * a.Hq + g * a.G + c / a.R) * (int64_t)D + half * (D / 2));
 #pragma unroll
-        for (int s = 0; s < C::kKs; ++s) {
-            const u32x4_t w = p_l[nb] >= 0 ? qp[s] : u32x4_t{0u, 0u, 0u, 0u};
-            qf[nb][s] = __builtin_bit_cast(bf16x8_t, w);
-            // kept in accumulation registers (MFMA reads its B operand from
-            // there), leaving the vector registers to K/V fragments and softmax
-            asm volatile("" : "+a"(qf[nb][s]));
-        }
+        for (int s = 0; s < C::kKs; ++s) qv[nb][s] = qp[s];
     }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+        if (p_l[nb] < 0 || p_l[nb] >= a.n_tok) p_l[nb] = -1;
+    bf16x8_t qf[2][C::kKs];
 
     // ---- direct-load sources.  Load i of this wave (per tensor) fills rows
     // [rpl*(wave*lpw + i), +rpl) of the tile; lane -> (row, physical chunk pc),
@@ -216,16 +197,6 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     const uint16_t* kbase = a.k_cache + (int64_t)g * D;
     const uint16_t* vbase = a.v_cache + (int64_t)g * D;
     const int32_t last_key = (int32_t)a.n_tok - 1;
-    int ld_row[C::kLoadsPerWave];
-    int32_t ld_kc[C::kLoadsPerWave], ld_vc[C::kLoadsPerWave];
-#pragma unroll
-    for (int i = 0; i < C::kLoadsPerWave; ++i) {
-        const int r = C::kRowsPerLoad * (wave * C::kLoadsPerWave + i) + lane / C::kNch;
-        const int pc = lane % C::kNch;
-        ld_row[i] = r;
-        ld_kc[i] = 8 * (pc ^ (r & (C::kNch - 1)));
-        ld_vc[i] = 8 * (pc ^ (2 * (r & (C::kNch / 2 - 1))));
-    }
     const uint32_t smem_base = lds_addr(smem);
     // Loads of one 64-key tile: scalar bases of its first key row, per-lane
     // byte offsets of this wave's rows (clamped to the last key), LDS base.
@@ -240,11 +211,17 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
         d.kg = kbase + (int64_t)key0 * row_stride;
         d.vg = vbase + (int64_t)key0 * row_stride;
         const int32_t lim = last_key - key0;
+        // recomputed from an opaque lane id at every tile (a few VALU
+        // operations) instead of being held through the key loop
+        int ln = (int)threadIdx.x & 63;
+        asm volatile("" : "+v"(ln));
+        const int pc = ln % C::kNch;
 #pragma unroll
         for (int i = 0; i < C::kLoadsPerWave; ++i) {
-            const uint32_t r = (uint32_t)min(ld_row[i], lim);
-            d.off_k[i] = (r * (uint32_t)row_stride + (uint32_t)ld_kc[i]) * 2u;
-            d.off_v[i] = (r * (uint32_t)row_stride + (uint32_t)ld_vc[i]) * 2u;
+            const int rw = C::kRowsPerLoad * (wave * C::kLoadsPerWave + i) + ln / C::kNch;
+            const uint32_t r = (uint32_t)min(rw, lim);
+            d.off_k[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (rw & (C::kNch - 1)))) * 2u;
+            d.off_v[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (2 * (rw & (C::kNch / 2 - 1))))) * 2u;
         }
         d.lds = __builtin_amdgcn_readfirstlane(smem_base + (t % kStages) * C::kStage +
                                                wave * C::kLoadsPerWave * 1024);
@@ -263,21 +240,27 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     };
 
     // ---- LDS read offsets (bytes within a stage)
-    // K (A operand of S^T): key row l32 of the sub-tile, logical chunk half*(D/16) + s
-    int k_ro[C::kKs];
-#pragma unroll
-    for (int s = 0; s < C::kKs; ++s)
-        k_ro[s] = l32 * C::kRowBytes + (((half * (C::kNch / 2) + s) ^ (l32 & (C::kNch - 1))) << 4);
+    // K (A operand of S^T): key row l32 of the sub-tile, logical chunk
+    // half*(D/16) + s, stored at chunk (half*(D/16) + s) ^ (l32 % (D/8)).
+    // With s < D/16 the XOR with s touches bits the half term leaves free, so
+    // step s is at k_ro0 ^ (s << 4).
+    const uint32_t k_ro0 = l32 * C::kRowBytes + (((half * (C::kNch / 2)) ^ (l32 & (C::kNch - 1))) << 4);
     // V^T via transpose reads: 16-lane group gq, lane m in it; rows 16*sp + 8*qh + 4*half + m/4,
-    // dims 32*md + 16*(gq%2) + 4*(m%4) .. +3
+    // dims 32*md + 16*(gq%2) + 4*(m%4) .. +3: chunk c = 4 md + c0 stored at
+    // c ^ (2 (row % (D/16))); md sits above c0 and the XOR is bitwise, so row
+    // block md is at v_ro0 ^ (md << 6).
     const int gq = lane >> 4, m16 = lane & 15;
     const int v_r = 4 * half + (m16 >> 2);  // row within an 8-row group (the swizzle depends on it only)
-    int v_ro[C::kMd];
-#pragma unroll
-    for (int md = 0; md < C::kMd; ++md) {
-        const int c = 4 * md + 2 * (gq & 1) + ((m16 & 3) >> 1);
-        v_ro[md] = v_r * C::kRowBytes + ((c ^ (2 * (v_r & (C::kNch / 2 - 1)))) << 4) + (m16 & 1) * 8;
-    }
+    const uint32_t v_ro0 = v_r * C::kRowBytes +
+                           (((2 * (gq & 1) + ((m16 & 3) >> 1)) ^ (2 * (v_r & (C::kNch / 2 - 1)))) << 4) + (m16 & 1) * 8;
+    // Stage and sub-tile bases are multiples of 1 KB, above every bit these
+    // XORs touch: (base + off0) ^ x == base + (off0 ^ x).
+    typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
+    auto k_frag = [](uint32_t kb0, int s) { return *(lds_bf16x8_t*)(uintptr_t)(kb0 ^ (uint32_t)(s << 4)); };
+    auto v_half = [](uint32_t vb0, int md, int row_off) {
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4_t*)(uintptr_t)((vb0 ^ (uint32_t)(md << 6)) + (uint32_t)row_off * C::kRowBytes));
+    };
 
     f32x16_t oacc[2][C::kMd];
 #pragma unroll
@@ -288,24 +271,23 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     const float cl2 = a.cl2;
 
     // Sub-tile u is half u%2 of the 64-key tile u/2 in ring stage (u/2) % kStages.
-    auto stage_of = [&](int u) { return smem + ((u >> 1) % kStages) * C::kStage; };
+    const uint32_t smem_lds = lds_addr(smem);
+    auto stage_of = [&](int u) { return smem_lds + ((u >> 1) % kStages) * C::kStage + (u & 1) * 32 * C::kRowBytes; };
     // K fragments of sub-tile u (A operand of S^T, k-step s)
     auto read_k = [&](int u, bf16x8_t (&kf)[C::kKs]) {
-        const unsigned char* kb = stage_of(u) + (u & 1) * 32 * C::kRowBytes;
+        const uint32_t kb0 = stage_of(u) + k_ro0;
 #pragma unroll
-        for (int s = 0; s < C::kKs; ++s) kf[s] = *reinterpret_cast<const bf16x8_t*>(kb + k_ro[s]);
+        for (int s = 0; s < C::kKs; ++s) kf[s] = k_frag(kb0, s);
     };
     // V^T fragments of sub-tile u (A operand of O^T, k-step sp, row block md)
     auto read_v = [&](int u, bf16x8_t (&vf)[2][C::kMd]) {
-        const unsigned char* vb = stage_of(u) + C::kTileBytes + (u & 1) * 32 * C::kRowBytes;
+        const uint32_t vb0 = stage_of(u) + C::kTileBytes + v_ro0;
 #pragma unroll
         for (int sp = 0; sp < 2; ++sp)
 #pragma unroll
             for (int md = 0; md < C::kMd; ++md) {
-                const unsigned char* p0 = vb + (16 * sp) * C::kRowBytes + v_ro[md];
-                const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0);
-                const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p0 + 8 * C::kRowBytes));
-                const u32x2_t wl = __builtin_bit_cast(u32x2_t, lo), wh = __builtin_bit_cast(u32x2_t, hi);
+                const u32x2_t wl = __builtin_bit_cast(u32x2_t, v_half(vb0, md, 16 * sp));
+                const u32x2_t wh = __builtin_bit_cast(u32x2_t, v_half(vb0, md, 16 * sp + 8));
                 vf[sp][md] = __builtin_bit_cast(bf16x8_t, u32x4_t{wl[0], wl[1], wh[0], wh[1]});
             }
     };
@@ -339,6 +321,10 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
                     if (8 * (v >> 2) + (v & 3) > lim) sacc[nb][v] = -INFINITY;
+                // applied here, back in the accumulation registers: left to
+                // the compiler the selects sink to the next sub-tile's reads
+                // and hold 32 lane masks in scalar registers meanwhile
+                asm volatile("" : "+a"(sacc[nb]));
             }
         }
     };
@@ -392,6 +378,19 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     const int n_sub = (kend - kbeg + 31) / 32;
     const int n_kt = (n_sub + 1) / 2;
     issue(0);
+    // The waits for the Q loads (placed by the compiler, which does not see
+    // the direct loads) also cover tile 0, needed next anyway; tiles 1 and 2
+    // are issued after them so that those waits do not cover them too.
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int s = 0; s < C::kKs; ++s) {
+            const u32x4_t w = p_l[nb] >= 0 ? qv[nb][s] : u32x4_t{0u, 0u, 0u, 0u};
+            qf[nb][s] = __builtin_bit_cast(bf16x8_t, w);
+            // kept in accumulation registers (MFMA reads its B operand from
+            // there), leaving the vector registers to K/V fragments and softmax
+            asm volatile("" : "+a"(qf[nb][s]));
+        }
     if (n_kt > 1) issue(1);
     if (n_kt > 2) issue(2);
     if (n_kt > 2) wait_vmcnt<2 * C::kLoads>();
@@ -440,20 +439,13 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
             constexpr int kSlots = 4 * C::kKs;
             constexpr int kV = 32 / kSlots;  // probabilities formed per slot (1 or 2)
             auto cvt_slot = [](int q) { return (2 * q + 1) / kV + 2; };
-            const unsigned char* kb = stage_of(u + 1) + ((u + 1) & 1) * 32 * C::kRowBytes;
-            const unsigned char* vb = stage_of(u - 1) + C::kTileBytes + ((u - 1) & 1) * 32 * C::kRowBytes;
-            // one address per K fragment and per V row block; the V half-steps
-            // are immediate offsets from it
-            const unsigned char* ka[C::kKs];
-            const unsigned char* va[C::kMd];
-#pragma unroll
-            for (int j = 0; j < C::kKs; ++j) ka[j] = kb + k_ro[j];
-#pragma unroll
-            for (int md = 0; md < C::kMd; ++md) va[md] = vb + v_ro[md];
-            auto rk = [&](int j) { return *reinterpret_cast<const bf16x8_t*>(ka[j]); };
+            const uint32_t kb0 = stage_of(u + 1) + k_ro0;
+            const uint32_t vb0 = stage_of(u - 1) + C::kTileBytes + v_ro0;
+            // addresses formed next to each read (the V half-steps are
+            // immediate offsets), so none stays live through the body
+            auto rk = [&](int j) { return k_frag(kb0, j); };
             auto rv = [&](int j, int hi) {
-                const unsigned char* p0 = va[j % C::kMd] + (16 * (j / C::kMd) + 8 * hi) * C::kRowBytes;
-                return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0));
+                return __builtin_bit_cast(u32x2_t, v_half(vb0, j % C::kMd, 16 * (j / C::kMd) + 8 * hi));
             };
             const float mc[2] = {m_run[0] * cl2, m_run[1] * cl2};
             float fv[32], ev[32];
@@ -553,8 +545,13 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     float l_tot[2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) l_tot[nb] = l_run[nb] + __shfl_xor(l_run[nb], 32);
+    // the columns' rows and heads, recomputed rather than held through the loop
+    int ln = (int)threadIdx.x & 63;
+    asm volatile("" : "+v"(ln));
+    auto col_of = [&](int nb) { return 64 * wave + 32 * nb + (ln & 31); };
     auto store_out = [&](int nb, const f32x16_t (&o)[C::kMd], float inv) {
-        uint16_t* op = a.out + (row[nb] * a.Hq + head[nb]) * (int64_t)D;
+        const int c = col_of(nb);
+        uint16_t* op = a.out + (((int64_t)tile * a.R + c % a.R) * a.Hq + g * a.G + c / a.R) * (int64_t)D;
 #pragma unroll
         for (int i = 0; i < C::kMd; ++i)
 #pragma unroll
@@ -565,41 +562,90 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
                 *reinterpret_cast<u32x2_t*>(op + 32 * i + 8 * r + 4 * half) = w;
             }
     };
-    if (n_pieces == 1) {
+    if (slot < 0) {
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb)
             if (p_l[nb] >= 0) store_out(nb, oacc[nb], 1.0f / l_tot[nb]);
         return;
     }
 
-    // split item: publish this piece's (m, l, O) in register order
+    // piece of a cut row tile: publish its (m, l, O) in register order
+    const int64_t sl = (int64_t)g * a.max_slots + slot;
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-        f32x4_t* po = a.part_o + (((item * a.n_chunks + chunk_id) * 4 + wave) * 2 + nb) * (C::kMd * 4 * 64) + lane;
+        f32x4_t* po = a.part_o + ((sl * 4 + wave) * 2 + nb) * (C::kMd * 4 * 64) + lane;
 #pragma unroll
         for (int i = 0; i < C::kMd; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
                 po[(i * 4 + r) * 64] = f32x4_t{oacc[nb][i][4 * r], oacc[nb][i][4 * r + 1], oacc[nb][i][4 * r + 2],
                                                oacc[nb][i][4 * r + 3]};
-        if (half == 0) a.part_ml[(item * a.n_chunks + chunk_id) * NCOL + col[nb]] = make_float2(m_run[nb], l_tot[nb]);
+        if (half == 0) a.part_ml[sl * NCOL + col_of(nb)] = make_float2(m_run[nb], l_tot[nb]);
     }
 }
 
-// Log-sum-exp merge of an item's pieces, in piece order.  One workgroup per
-// (item, wave slice, column block): the 32 columns x D values that attention
-// wave `wave` held in block nb, laid out as [i][r][lane] f32x4 per piece, so
-// every load is a coalesced 1 KB row.  Thread t handles lane t % 64 and the
-// (i, r) pairs t / 64 + 4k.
+// Plan entries are read as constant memory (the plan kernel wrote them before
+// this launch and nothing here writes them), so they come in by scalar loads.
+__device__ __forceinline__ int32_t sload(const int32_t* p) {
+    return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
+// Workgroup b serves kv head b % Hkv (with 8 kv heads each XCD serves one, so
+// its K/V stay in that XCD's L2) and walks range b / Hkv of the plan.
+template <int D>
+__global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[ACfg<D>::kLds];
+    const int b = blockIdx.x;
+    const int g = b % a.Hkv;
+    const int jw = b / a.Hkv;
+    const int32_t* hdr = a.plan;
+    if (jw >= sload(hdr + 1)) return;
+    const int32_t* rg = hdr + kPlanHdr + 4 * jw;
+    int32_t unit = sload(rg);
+    const int32_t hi = sload(rg + 1);
+    int t = sload(rg + 2);
+    int32_t piece = sload(rg + 3);
+    const int32_t* til = hdr + kPlanHdr + 4 * a.P;
+    for (; t < a.n_tiles; ++t, piece = 0) {
+        const int32_t* e = til + 8 * t;
+        const int32_t s0 = sload(e), s1 = sload(e + 1);
+        if (s1 <= s0) continue;  // no row of the tile has a valid position
+        const int32_t seg_lo = max(unit, s0), seg_hi = min(hi, s1);
+        if (seg_hi <= seg_lo) break;  // the range ends before the tile's units
+        const int32_t pmin = sload(e + 2), pmax = sload(e + 3), pbase = sload(e + 4), npc = sload(e + 5);
+        // the arguments and the head through opaque copies: what the segment
+        // derives from them is formed inside it, not held in scalar registers
+        // through the loop
+        auto kp = __builtin_amdgcn_kernarg_segment_ptr();
+        int gs = g;
+        asm volatile("" : "+s"(kp), "+s"(gs));
+        segment<D>(*(const AttnArgs*)kp, smem, gs, t, (seg_lo - s0) * KT, min((seg_hi - s0) * KT, pmax + 1), pmin,
+                   npc > 1 ? pbase + piece : -1);
+        unit = seg_hi;
+        if (unit >= hi) break;
+        __syncthreads();  // every wave is done with the ring before the next segment refills it
+    }
+}
+
+// Log-sum-exp merge of a cut row tile's pieces, in piece order.  One
+// workgroup per (cut row tile, wave slice, column block, kv head): the 32
+// columns x D values that attention wave `wave` held in block nb, laid out
+// as [i][r][lane] f32x4 per piece, so every load is a coalesced 1 KB row.
+// Thread t handles lane t % 64 and the (i, r) pairs t / 64 + 4k.  Head g
+// runs on the XCD that wrote its pieces (b % 8 == g with 8 kv heads).
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     constexpr int kMd = D / 32;
     constexpr int kPer = kMd;  // (i, r) pairs per thread: 4 * kMd / 4
-    const int64_t item = blockIdx.x >> 3;  // tile * Hkv + g
-    const int wave = (blockIdx.x >> 1) & 3, nb = blockIdx.x & 1;
-    const int32_t nu = a.n_used[item];
-    if (nu <= 1) return;
-    const int tile = (int)(item / a.Hkv), g = (int)(item % a.Hkv);
+    const int g = blockIdx.x % a.Hkv;
+    const int rest = blockIdx.x / a.Hkv;
+    const int wave = (rest >> 1) & 3, nb = rest & 1;
+    const int k = rest >> 3;  // cut row tile
+    const int32_t* hdr = a.plan;
+    if (k >= hdr[2]) return;
+    const int32_t* til = hdr + kPlanHdr + 4 * a.P;
+    const int tile = til[8 * a.n_tiles + k];
+    const int32_t pbase = til[8 * tile + 4], nu = til[8 * tile + 5];
     const int tid = threadIdx.x, lane = tid & 63, q4 = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
     const int col = 64 * wave + 32 * nb + l32;
@@ -609,7 +655,8 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     if (p < 0 || p >= a.n_tok) return;
     const int head = g * a.G + col / a.R;
     const float cl2 = a.cl2;
-    const float2* ml = a.part_ml + item * a.n_chunks * NCOL + col;
+    const int64_t sl0 = (int64_t)g * a.max_slots + pbase;
+    const float2* ml = a.part_ml + sl0 * NCOL + col;
     float M = -1.0e30f;
     for (int c = 0; c < nu; ++c) M = fmaxf(M, ml[c * NCOL].x);
     float L = 0.0f;
@@ -620,7 +667,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
         const float2 mlc = ml[c * NCOL];
         const float w = __builtin_amdgcn_exp2f((mlc.x - M) * cl2);
         L += w * mlc.y;
-        const f32x4_t* po = a.part_o + (((item * a.n_chunks + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
+        const f32x4_t* po = a.part_o + (((sl0 + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
 #pragma unroll
         for (int k = 0; k < kPer; ++k) o[k] += w * po[(q4 + 4 * k) * 64];
     }
@@ -635,11 +682,128 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     }
 }
 
+// Inclusive prefix sum over the 1024 threads of a workgroup; *total gets the
+// sum of all.  s_w holds 16 wave totals.
+__device__ int32_t block_scan(int32_t v, int32_t* s_w, int32_t* total) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int32_t n = __shfl_up(v, o);
+        if (lane >= o) v += n;
+    }
+    if (lane == 63) s_w[w] = v;
+    __syncthreads();
+    int32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const int32_t x = s_w[k];
+        pre += k < w ? x : 0;
+        tot += x;
+    }
+    __syncthreads();
+    *total = tot;
+    return v + pre;
+}
+
+// The plan of a call (one workgroup of 1024 threads; layout at AttnArgs::plan).
+// Row tile t with u = pmax/64 + 1 units (0 if no row has a valid position)
+// spans [s0 - kSegCost, s1) of the line and its units are [s0, s1); range j
+// of P' = min(P, W) is [lo_j, lo_{j+1}) with lo_j = floor(j W / P'), so
+// position x lies in range floor(((x + 1) P' - 1) / W), and the ranges
+// starting in the span of row tile t are j in
+// [ceil((s0 - kSegCost) P' / W), ceil(s1 P' / W)).  A row tile whose units
+// ranges cut has one piece per range meeting them, numbered in unit order,
+// in slots [slot base, + pieces).  Every step is a parallel pass over the
+// row tiles.
+__global__ __launch_bounds__(1024) void plan_kernel(AttnArgs a) {
+    __shared__ int32_t s_lo[1024], s_hi[1024], s_w[16];
+    const int tid = threadIdx.x;
+    int32_t* hdr = a.plan;
+    int32_t* rng = hdr + kPlanHdr;
+    int32_t* til = rng + 4 * a.P;
+    int32_t* spl = til + 8 * a.n_tiles;
+    // pass 1: each row tile's smallest and largest valid position, its units
+    // and their prefix over the row tiles
+    int32_t carry = 0;
+    for (int32_t base = 0; base < a.n_tiles; base += 1024) {
+        s_lo[tid] = INT_MAX;
+        s_hi[tid] = -1;
+        __syncthreads();
+        const int64_t r0 = (int64_t)base * a.R, r1 = min(a.n_sel, (int64_t)(base + 1024) * a.R);
+        for (int64_t r = r0 + tid; r < r1; r += 1024) {
+            const int32_t p = a.pos[r];
+            if (p >= 0 && p < a.n_tok) {
+                const int k = (int)(r / a.R - base);
+                atomicMin(&s_lo[k], p);
+                atomicMax(&s_hi[k], p);
+            }
+        }
+        __syncthreads();
+        const int32_t t = base + tid;
+        const int32_t pmax = s_hi[tid], pmin = s_lo[tid];
+        const int32_t units = (t < a.n_tiles && pmax >= 0) ? pmax / KT + 1 : 0;
+        const int32_t span = units > 0 ? units + kSegCost : 0;
+        int32_t tot;
+        const int32_t incl = block_scan(span, s_w, &tot);
+        if (t < a.n_tiles) {
+            til[8 * t] = carry + incl - units;
+            til[8 * t + 1] = carry + incl;
+            til[8 * t + 2] = pmax >= 0 ? pmin : -1;
+            til[8 * t + 3] = pmax;
+        }
+        carry += tot;
+    }
+    const int32_t W = carry;
+    const int32_t np = min(a.P, W);
+    auto owner = [&](int32_t u) { return (int32_t)(((int64_t)(u + 1) * np - 1) / W); };
+    auto first_range = [&](int32_t u) { return (int32_t)(((int64_t)u * np + W - 1) / W); };  // ceil(u P' / W)
+    // pass 2: pieces, slot bases, the list of cut row tiles, range starts
+    // (each thread reads back only the entries it wrote itself)
+    int32_t slots = 0, n_split = 0;
+    for (int32_t base = 0; base < a.n_tiles; base += 1024) {
+        const int32_t t = base + tid;
+        int32_t s0 = 0, s1 = 0, pieces = 0;
+        if (t < a.n_tiles) {
+            s0 = til[8 * t];
+            s1 = til[8 * t + 1];
+            if (s1 > s0) pieces = owner(s1 - 1) - owner(s0) + 1;
+        }
+        const int32_t cut = pieces > 1 ? 1 : 0;
+        int32_t tot_slots, tot_cut;
+        const int32_t incl_slots = block_scan(cut * pieces, s_w, &tot_slots);
+        const int32_t incl_cut = block_scan(cut, s_w, &tot_cut);
+        if (t < a.n_tiles) {
+            til[8 * t + 4] = slots + incl_slots - cut * pieces;
+            til[8 * t + 5] = pieces;
+            til[8 * t + 6] = 0;
+            til[8 * t + 7] = 0;
+            if (cut) spl[n_split + incl_cut - 1] = t;
+            if (s1 > s0) {
+                const int32_t j1 = first_range(s1);
+                for (int32_t j = first_range(s0 - kSegCost); j < j1; ++j) {
+                    rng[4 * j] = (int32_t)((int64_t)j * W / np);
+                    rng[4 * j + 1] = (int32_t)((int64_t)(j + 1) * W / np);
+                    rng[4 * j + 2] = t;
+                    rng[4 * j + 3] = max(0, j - owner(s0));
+                }
+            }
+        }
+        slots += tot_slots;
+        n_split += tot_cut;
+    }
+    if (tid == 0) {
+        hdr[0] = W;
+        hdr[1] = np;
+        hdr[2] = n_split;
+        hdr[3] = slots;
+    }
+}
+
 template <int D>
 hipError_t launch(const AttnArgs& args, hipStream_t s) {
-    const int64_t items = (int64_t)args.n_tiles * args.Hkv;
-    hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(items * args.n_chunks)), dim3(256), 0, s, args);
-    if (args.n_chunks > 1) hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)(items * 8)), dim3(256), 0, s, args);
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, args);
+    hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(args.P * args.Hkv)), dim3(256), 0, s, args);
+    hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)(args.P * args.Hkv * 8)), dim3(256), 0, s, args);
     return hipGetLastError();
 }
 
@@ -653,40 +817,19 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
     const int32_t G = n_q_heads / n_kv_heads;
     p.rows_per_tile = dtype == SEMSHARE_BF16 ? NCOL / G : 1;
     p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
-    const int64_t n_kt = (n_tok + KT - 1) / KT;
-    p.split_units = (int32_t)std::max<int64_t>(n_kt, 1);  // one piece per item
-    p.n_chunks = 1;
+    p.P = p.max_slots = 0;
+    p.off_plan = p.off_part_o = p.off_part_ml = p.total = 0;
     if (dtype == SEMSHARE_BF16 && n_sel > 0) {
-        // Work estimate in 64-key tiles with the selected rows spread over the
-        // prompt (a tile's causal range then averages half of it).  Items
-        // longer than 3/4 of one CU's share are cut into equal pieces (shorter
-        // pieces balance the CUs better but cost partial-result traffic and a
-        // prologue each; 3/4 measured best at 5k tokens), never shorter than
-        // 4 tiles.
-        const double share = (double)p.n_tiles * n_kv_heads * (n_kt + 1) / 2.0 / kCUs;
-        const int64_t su = std::max<int64_t>(kMinPieceKt, (int64_t)(share * kSplitShares));
-        if (su < n_kt) {
-            p.split_units = (int32_t)su;
-            p.n_chunks = (int32_t)((n_kt + su - 1) / su);
-            // Items with fewer pieces leave their trailing chunk slots empty.
-            // At an even stride those empty workgroups line up with the
-            // dispatcher's round-robin over the shader engines of an XCD and
-            // the real ones all land on half of its CUs (measured 1.6x slower);
-            // an odd stride spreads them.
-            if (p.n_chunks % 2 == 0) p.n_chunks += 1;
-        }
+        // one range per CU; the cut row tiles hold at most two pieces per
+        // range boundary inside them, and at most n_tiles + P pieces in all
+        p.P = std::max(1, kCUs / n_kv_heads);
+        p.max_slots = (int32_t)std::min<int64_t>(2 * (int64_t)p.P, p.n_tiles + p.P);
+        const size_t plan_ints = kPlanHdr + 4 * (size_t)p.P + 8 * (size_t)p.n_tiles + (size_t)p.P;
+        const size_t slots = (size_t)n_kv_heads * p.max_slots;
+        p.off_part_o = align256(plan_ints * sizeof(int32_t));
+        p.off_part_ml = align256(p.off_part_o + slots * NCOL * head_dim * sizeof(float));
+        p.total = align256(p.off_part_ml + slots * NCOL * sizeof(float2));
     }
-    size_t off = 0;
-    p.off_part_o = p.off_part_ml = p.off_used = 0;
-    if (p.n_chunks > 1) {
-        const size_t pieces = (size_t)p.n_tiles * n_kv_heads * p.n_chunks;
-        off = align256(pieces * NCOL * head_dim * sizeof(float));
-        p.off_part_ml = off;
-        off = align256(off + pieces * NCOL * sizeof(float2));
-        p.off_used = off;
-        off = align256(off + (size_t)p.n_tiles * n_kv_heads * sizeof(int32_t));
-    }
-    p.total = off;
     return p;
 }
 
@@ -700,7 +843,7 @@ hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream
     t.out = static_cast<uint16_t*>(a.out);
     t.part_o = reinterpret_cast<f32x4_t*>(ws + p.off_part_o);
     t.part_ml = reinterpret_cast<float2*>(ws + p.off_part_ml);
-    t.n_used = reinterpret_cast<int32_t*>(ws + p.off_used);
+    t.plan = reinterpret_cast<int32_t*>(ws + p.off_plan);
     t.n_sel = a.n_sel;
     t.n_tok = a.n_tok;
     t.Hq = a.n_q_heads;
@@ -708,8 +851,8 @@ hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream
     t.G = a.n_q_heads / a.n_kv_heads;
     t.R = p.rows_per_tile;
     t.n_tiles = (int32_t)p.n_tiles;
-    t.split_units = p.split_units;
-    t.n_chunks = p.n_chunks;
+    t.P = p.P;
+    t.max_slots = p.max_slots;
     t.cl2 = a.sm_scale * kLog2e;
     if (a.head_dim == 128) return launch<128>(t, s);
     return launch<64>(t, s);

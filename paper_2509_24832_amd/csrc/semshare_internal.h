@@ -117,9 +117,9 @@ struct AttnCall {
 struct AttnPlan {
     int32_t rows_per_tile;  // selected rows per tile (256 / G for bf16)
     int64_t n_tiles;
-    int32_t split_units;    // target split-KV piece length in 64-key tiles
-    int32_t n_chunks;       // most pieces per (tile, kv head); 1 = no split
-    size_t off_part_o, off_part_ml, off_used, total;
+    int32_t P;              // workgroups (ranges of the stream-K line) per kv head
+    int32_t max_slots;      // partial-result slots per kv head
+    size_t off_plan, off_part_o, off_part_ml, total;
 };
 
 size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);

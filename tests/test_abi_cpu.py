@@ -178,5 +178,11 @@ def test_split_call_validation(lib):
     W = L.semshare_partial_prefill_workspace(1280, 5120, 4096, 32, 8, 128, 1)
     assert W >= 1280 * 32 * 128 * 2 + L.semshare_qkv_rope_workspace(1280, 32, 8, 128, 1) + \
         L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1)
-    assert L.semshare_prefill_attention_workspace(256, 256, 32, 8, 128, 1) == 0  # short key range: never split
-    assert L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1) > 0  # few row tiles: split-KV
+    # bf16: the work plan plus partial-result slots for the cut row tiles, at
+    # most 2 per workgroup (256 CUs / 8 kv heads = 32 per head) whatever the size
+    slot = 256 * 128 * 4 + 256 * 8
+    for n_sel, n_tok in [(256, 256), (1280, 5120), (16384, 16384)]:
+        ws = L.semshare_prefill_attention_workspace(n_sel, n_tok, 32, 8, 128, 1)
+        assert 0 < ws <= 8 * 64 * slot + 4 * (4 + 5 * 32 + 8 * (n_sel // 64 + 1)) + 1024, (n_sel, n_tok, ws)
+    assert L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1) >= 8 * 52 * slot  # 20 row tiles + 32
+    assert L.semshare_prefill_attention_workspace(256, 256, 32, 8, 128, 0) == 0  # fp32 path: no workspace
