@@ -126,6 +126,9 @@ class Path:
         self.x_sel = torch.empty((n, self.d), dtype=bf, device="cuda")
         self.q_sel = torch.empty((n, self.hq, self.D), dtype=bf, device="cuda")
         self.out_sel = torch.empty_like(self.q_sel)
+        # the attention work plan of the selection, made once per step and shared by layers 1..L-1
+        self.plan = torch.empty(max(1, ss.attention_plan_bytes(n, self.T, self.hq, self.hkv, self.D, bf)),
+                                dtype=torch.uint8, device="cuda")
         need = max(ws_hint,
                    ss.qkv_rope_workspace_bytes(self.T, self.hq, self.hkv, self.D, bf),
                    ss.prefill_attention_workspace_bytes(self.T, self.T, self.hq, self.hkv, self.D, bf),
@@ -154,6 +157,7 @@ class Path:
                              workspace=self.ws)
         m("attn0")
         ss.select_recompute(self.sigma, self.n_sel, out=self.sel)
+        ss.attention_plan(self.sel, self.T, hq, hkv, self.D, out=self.plan)
         m("select")
         ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
         m("xsel")
@@ -163,7 +167,7 @@ class Path:
                         workspace=self.ws)
             m("qkv")
             ss.prefill_attention(self.q_sel, self.sel, self.asm_k[l], self.asm_v[l], hkv, out=self.out_sel,
-                                 workspace=self.ws)
+                                 workspace=self.ws, plan=self.plan)
             m("attn")
 
 
@@ -304,7 +308,7 @@ def main():
     gather_ms = avg("gather")
     match_ms = avg("match")
     pp_ms = (avg("qkv0") + attn0_ms + (L - 1) * (attn_ms + qkv_ms))
-    # the dominant call: prefill_attention (attention kernel + split-KV combine),
+    # the dominant call: prefill_attention (attention kernel + combine of cut row tiles),
     # averaged over the 32 calls of a step (layer 0 over all 5120 rows, then
     # 31 partial layers); achieved = algorithmic flops per call / event-timed
     # duration per call
@@ -342,7 +346,7 @@ def main():
         "attention_TFLOPs": {"partial_layer": attn_flops / (attn_ms * 1e-3) / 1e12,
                              "layer0_full": attn0_flops / (attn0_ms * 1e-3) / 1e12},
         "qkv_gemm_TFLOPs": qkv_flops / (qkv_ms * 1e-3) / 1e12,
-        "roofline": {"kernel": "prefill_attention (attention_kernel + split-KV combine_kernel)", "bound": "mfma",
+        "roofline": {"kernel": "prefill_attention (attention_kernel + combine_kernel; layer 0 also its plan_kernel, layers 1-31 share the plan made after selection)", "bound": "mfma",
                      "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / BF16_PEAK_TFLOPS, "traffic": traffic,
                      "flops_per_call": attn_call_flops, "us_per_call": attn_call_ms * 1e3, "calls_per_step": L},

@@ -201,6 +201,40 @@ size_t semshare_prefill_attention_workspace(int64_t n_sel, int64_t n_tok, int32_
                                             semshare_dtype_t dtype);
 
 /*
+ * The work plan of semshare_prefill_attention for one set of selected
+ * positions, made once and reused.  The selection is made once per prompt
+ * (Section 4.2: the same high-deviation tokens are recomputed in every layer
+ * after the first), so every later layer's attention can share one plan
+ * instead of making its own.  The plan depends on sel_pos (its values),
+ * n_sel, n_tok, n_q_heads, n_kv_heads, head_dim and dtype only.
+ *   plan   device buffer of at least semshare_attention_plan_bytes() bytes,
+ *          256-byte aligned; written on `stream`.  0 bytes (nothing to do)
+ *          for dtype FP32 or n_sel == 0.
+ */
+size_t semshare_attention_plan_bytes(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                                     int32_t head_dim, semshare_dtype_t dtype);
+semshare_status_t semshare_attention_plan(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok,
+                                          int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                          semshare_dtype_t dtype, void* plan, size_t plan_bytes,
+                                          void* stream);
+
+/*
+ * semshare_prefill_attention with a plan from semshare_attention_plan (same
+ * sel_pos values and sizes; the buffer stays owned by the caller and is only
+ * read).  Same results as semshare_prefill_attention, bit for bit.  A plan
+ * made for other sizes is detected on the device and nothing is written; a
+ * plan made for other positions of the same sizes gives wrong results.  The
+ * workspace is the one semshare_prefill_attention_workspace() sizes.
+ */
+semshare_status_t semshare_prefill_attention_planned(const void* plan, size_t plan_bytes, const void* q,
+                                                     const int32_t* sel_pos, int64_t n_sel,
+                                                     const void* k_cache, const void* v_cache,
+                                                     int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                                                     int32_t head_dim, float sm_scale, void* out,
+                                                     void* workspace, size_t workspace_bytes,
+                                                     semshare_dtype_t dtype, void* stream);
+
+/*
  * High-deviation token selection (Section 3 Insight 1; Section 4.2): the
  * n_sel positions with the largest deviation sigma (ties: the lower
  * position first), written in ascending position order.  One workgroup

@@ -170,6 +170,9 @@ semshare_status_t check_workspace(const char* fn, const void* ws, size_t have, s
     return SEMSHARE_OK;
 }
 
+// plan argument of prefill_attention_impl: make the plan in the workspace
+const void* const PLAN_IN_WORKSPACE = reinterpret_cast<const void*>(uintptr_t(1));
+
 float default_scale(float sm_scale, int32_t head_dim) {
     return sm_scale > 0.0f ? sm_scale : (float)(1.0 / std::sqrt((double)head_dim));
 }
@@ -226,12 +229,13 @@ semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, i
     return from_hip(e, "qkv_rope launch");
 }
 
-semshare_status_t semshare_prefill_attention(const void* q, const int32_t* sel_pos, int64_t n_sel,
-                                             const void* k_cache, const void* v_cache, int64_t n_tok,
-                                             int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
-                                             float sm_scale, void* out, void* workspace,
-                                             size_t workspace_bytes, semshare_dtype_t dtype, void* stream) {
-    const char* fn = "prefill_attention";
+namespace {
+semshare_status_t prefill_attention_impl(const char* fn, const void* plan_buf, size_t plan_bytes, const void* q,
+                                          const int32_t* sel_pos, int64_t n_sel, const void* k_cache,
+                                          const void* v_cache, int64_t n_tok, int32_t n_q_heads,
+                                          int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out,
+                                          void* workspace, size_t workspace_bytes, semshare_dtype_t dtype,
+                                          void* stream) {
     semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, 0, n_q_heads, n_kv_heads, head_dim, dtype, false);
     if (st != SEMSHARE_OK) return st;
     if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", fn);
@@ -242,11 +246,67 @@ semshare_status_t semshare_prefill_attention(const void* q, const int32_t* sel_p
     const semshare::AttnPlan plan = semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
     st = check_workspace(fn, workspace, workspace_bytes, plan.total);
     if (st != SEMSHARE_OK) return st;
+    if (plan_buf == PLAN_IN_WORKSPACE) {
+        plan_buf = nullptr;
+    } else if (plan.plan_bytes > 0) {
+        if (!plan_buf || plan_bytes < plan.plan_bytes)
+            return fail(SEMSHARE_E_INVAL, "%s: plan of %zu bytes is smaller than the %zu required", fn, plan_bytes,
+                        plan.plan_bytes);
+        if (reinterpret_cast<uintptr_t>(plan_buf) % 256) return fail(SEMSHARE_E_INVAL, "%s: plan not 256-byte aligned", fn);
+    }
     const semshare::AttnCall a{q, sel_pos, n_sel, k_cache, v_cache, n_tok, n_q_heads, n_kv_heads, head_dim,
-                               default_scale(sm_scale, head_dim), out, workspace};
+                               default_scale(sm_scale, head_dim), out, workspace, plan_buf};
     hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_attention_bf16(a, plan, (hipStream_t)stream)
                                           : semshare::launch_attention_f32(a, plan, (hipStream_t)stream);
     return from_hip(e, "prefill_attention launch");
+}
+}  // namespace
+
+semshare_status_t semshare_prefill_attention(const void* q, const int32_t* sel_pos, int64_t n_sel,
+                                             const void* k_cache, const void* v_cache, int64_t n_tok,
+                                             int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                             float sm_scale, void* out, void* workspace,
+                                             size_t workspace_bytes, semshare_dtype_t dtype, void* stream) {
+    return prefill_attention_impl("prefill_attention", PLAN_IN_WORKSPACE, 0, q, sel_pos, n_sel, k_cache, v_cache,
+                                  n_tok, n_q_heads, n_kv_heads, head_dim, sm_scale, out, workspace, workspace_bytes,
+                                  dtype, stream);
+}
+
+size_t semshare_attention_plan_bytes(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                                     int32_t head_dim, semshare_dtype_t dtype) {
+    if (!dtype_ok(dtype) || n_sel < 0 || n_tok < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0 ||
+        n_q_heads % n_kv_heads)
+        return 0;
+    return semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).plan_bytes;
+}
+
+semshare_status_t semshare_attention_plan(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok, int32_t n_q_heads,
+                                          int32_t n_kv_heads, int32_t head_dim, semshare_dtype_t dtype, void* plan,
+                                          size_t plan_bytes, void* stream) {
+    const char* fn = "attention_plan";
+    semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, 0, n_q_heads, n_kv_heads, head_dim, dtype, false);
+    if (st != SEMSHARE_OK) return st;
+    const semshare::AttnPlan p = semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
+    if (p.plan_bytes == 0) return ok();  // nothing to plan (no rows, or the fp32 path)
+    if (!sel_pos) return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (!plan || plan_bytes < p.plan_bytes)
+        return fail(SEMSHARE_E_INVAL, "%s: plan of %zu bytes is smaller than the %zu required", fn, plan_bytes,
+                    p.plan_bytes);
+    if (reinterpret_cast<uintptr_t>(plan) % 256) return fail(SEMSHARE_E_INVAL, "%s: plan not 256-byte aligned", fn);
+    const semshare::AttnCall a{nullptr, sel_pos, n_sel, nullptr, nullptr, n_tok, n_q_heads, n_kv_heads, head_dim,
+                               0.0f, nullptr, nullptr, nullptr};
+    return from_hip(semshare::launch_attention_plan_bf16(a, p, plan, (hipStream_t)stream), "attention_plan launch");
+}
+
+semshare_status_t semshare_prefill_attention_planned(const void* plan, size_t plan_bytes, const void* q,
+                                                     const int32_t* sel_pos, int64_t n_sel, const void* k_cache,
+                                                     const void* v_cache, int64_t n_tok, int32_t n_q_heads,
+                                                     int32_t n_kv_heads, int32_t head_dim, float sm_scale, void* out,
+                                                     void* workspace, size_t workspace_bytes,
+                                                     semshare_dtype_t dtype, void* stream) {
+    return prefill_attention_impl("prefill_attention_planned", plan, plan_bytes, q, sel_pos, n_sel, k_cache,
+                                  v_cache, n_tok, n_q_heads, n_kv_heads, head_dim, sm_scale, out, workspace,
+                                  workspace_bytes, dtype, stream);
 }
 
 semshare_status_t semshare_partial_prefill(
@@ -278,7 +338,7 @@ semshare_status_t semshare_partial_prefill(
     if (e != hipSuccess || !out) return from_hip(e, "partial_prefill launch");
     const semshare::AttnPlan plan = semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype);
     const semshare::AttnCall aa{q_ws, sel_pos, n_sel, k_cache, v_cache, n_tok, n_q_heads, n_kv_heads, head_dim,
-                                default_scale(sm_scale, head_dim), out, ws + lay.off_attn};
+                                default_scale(sm_scale, head_dim), out, ws + lay.off_attn, nullptr};
     e = dtype == SEMSHARE_BF16 ? semshare::launch_attention_bf16(aa, plan, (hipStream_t)stream)
                                : semshare::launch_attention_f32(aa, plan, (hipStream_t)stream);
     return from_hip(e, "partial_prefill launch");

@@ -57,7 +57,9 @@ constexpr int NCOL = 256;    // query columns per workgroup
 constexpr int kStages = 4;   // K/V ring depth
 constexpr float kSumLimit = 65536.0f;  // 2^16
 constexpr int kCUs = 256;        // compute units of the chip
-constexpr int kPlanHdr = 4;      // plan header: W, ranges, split row tiles, slots used
+// plan header: W, ranges, split row tiles, slots used, then the sizes it was
+// made for (n_sel, n_tok, Hq, Hkv, R), which a launch checks before using it
+constexpr int kPlanHdr = 12;
 // Fixed cost of a segment (Q and first K/V loads before the key loop, the
 // output or partial-result stores after it) in units of one 64-key tile of
 // the key loop (measured ~14 us against ~2 us per unit at 256 columns x D 128).
@@ -75,7 +77,7 @@ struct AttnArgs {
     uint16_t* out;            // [n_sel][Hq][D]
     f32x4_t* part_o;          // [Hkv][max_slots][NCOL * D / 4], register-native order
     float2* part_ml;          // [Hkv][max_slots][NCOL]  (m, l)
-    // plan (int32): header [kPlanHdr] = W, ranges P', split row tiles, slots;
+    // plan (int32): header [kPlanHdr] = W, ranges P', split row tiles, slots, sizes;
     // ranges [P][4] = first unit, end unit, first row tile, piece index of
     // its first segment; row tiles [n_tiles][8] = first unit, end unit, pmin,
     // pmax, slot base, pieces, -, -; split row tiles [P]
@@ -590,6 +592,12 @@ __device__ __forceinline__ int32_t sload(const int32_t* p) {
     return *(const __attribute__((address_space(4))) int32_t*)p;
 }
 
+// A plan made for other sizes is not used (it could point past the buffers).
+__device__ __forceinline__ bool plan_fits(const AttnArgs& a, const int32_t* hdr) {
+    return sload(hdr + 4) == (int32_t)a.n_sel && sload(hdr + 5) == (int32_t)a.n_tok && sload(hdr + 6) == a.Hq &&
+           sload(hdr + 7) == a.Hkv && sload(hdr + 8) == a.R;
+}
+
 // Workgroup b serves kv head b % Hkv (with 8 kv heads each XCD serves one, so
 // its K/V stay in that XCD's L2) and walks range b / Hkv of the plan.
 template <int D>
@@ -599,7 +607,7 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     const int g = b % a.Hkv;
     const int jw = b / a.Hkv;
     const int32_t* hdr = a.plan;
-    if (jw >= sload(hdr + 1)) return;
+    if (!plan_fits(a, hdr) || jw >= sload(hdr + 1)) return;
     const int32_t* rg = hdr + kPlanHdr + 4 * jw;
     int32_t unit = sload(rg);
     const int32_t hi = sload(rg + 1);
@@ -642,7 +650,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     const int wave = (rest >> 1) & 3, nb = rest & 1;
     const int k = rest >> 3;  // cut row tile
     const int32_t* hdr = a.plan;
-    if (k >= hdr[2]) return;
+    if (!plan_fits(a, hdr) || k >= sload(hdr + 2)) return;
     const int32_t* til = hdr + kPlanHdr + 4 * a.P;
     const int tile = til[8 * a.n_tiles + k];
     const int32_t pbase = til[8 * tile + 4], nu = til[8 * tile + 5];
@@ -796,12 +804,17 @@ __global__ __launch_bounds__(1024) void plan_kernel(AttnArgs a) {
         hdr[1] = np;
         hdr[2] = n_split;
         hdr[3] = slots;
+        hdr[4] = (int32_t)a.n_sel;
+        hdr[5] = (int32_t)a.n_tok;
+        hdr[6] = a.Hq;
+        hdr[7] = a.Hkv;
+        hdr[8] = a.R;
     }
 }
 
 template <int D>
-hipError_t launch(const AttnArgs& args, hipStream_t s) {
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, args);
+hipError_t launch(const AttnArgs& args, bool make_plan, hipStream_t s) {
+    if (make_plan) hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, args);
     hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(args.P * args.Hkv)), dim3(256), 0, s, args);
     hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)(args.P * args.Hkv * 8)), dim3(256), 0, s, args);
     return hipGetLastError();
@@ -818,7 +831,7 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
     p.rows_per_tile = dtype == SEMSHARE_BF16 ? NCOL / G : 1;
     p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
     p.P = p.max_slots = 0;
-    p.off_plan = p.off_part_o = p.off_part_ml = p.total = 0;
+    p.off_plan = p.off_part_o = p.off_part_ml = p.total = p.plan_bytes = 0;
     if (dtype == SEMSHARE_BF16 && n_sel > 0) {
         // one range per CU; the cut row tiles hold at most two pieces per
         // range boundary inside them, and at most n_tiles + P pieces in all
@@ -826,14 +839,16 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
         p.max_slots = (int32_t)std::min<int64_t>(2 * (int64_t)p.P, p.n_tiles + p.P);
         const size_t plan_ints = kPlanHdr + 4 * (size_t)p.P + 8 * (size_t)p.n_tiles + (size_t)p.P;
         const size_t slots = (size_t)n_kv_heads * p.max_slots;
-        p.off_part_o = align256(plan_ints * sizeof(int32_t));
+        p.plan_bytes = plan_ints * sizeof(int32_t);
+        p.off_part_o = align256(p.plan_bytes);
         p.off_part_ml = align256(p.off_part_o + slots * NCOL * head_dim * sizeof(float));
         p.total = align256(p.off_part_ml + slots * NCOL * sizeof(float2));
     }
     return p;
 }
 
-hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream_t s) {
+namespace {
+AttnArgs attn_args(const AttnCall& a, const AttnPlan& p) {
     unsigned char* ws = static_cast<unsigned char*>(a.workspace);
     AttnArgs t{};
     t.q = static_cast<const uint16_t*>(a.q);
@@ -854,8 +869,23 @@ hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream
     t.P = p.P;
     t.max_slots = p.max_slots;
     t.cl2 = a.sm_scale * kLog2e;
-    if (a.head_dim == 128) return launch<128>(t, s);
-    return launch<64>(t, s);
+    return t;
+}
+}  // namespace
+
+hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream_t s) {
+    AttnArgs t = attn_args(a, p);
+    const bool make_plan = a.plan == nullptr;
+    if (!make_plan) t.plan = static_cast<int32_t*>(const_cast<void*>(a.plan));
+    if (a.head_dim == 128) return launch<128>(t, make_plan, s);
+    return launch<64>(t, make_plan, s);
+}
+
+hipError_t launch_attention_plan_bf16(const AttnCall& a, const AttnPlan& p, void* plan, hipStream_t s) {
+    AttnArgs t = attn_args(a, p);
+    t.plan = static_cast<int32_t*>(plan);
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, t);
+    return hipGetLastError();
 }
 
 }  // namespace semshare

@@ -111,6 +111,7 @@ struct AttnCall {
     float sm_scale;
     void* out;
     void* workspace;  // plan_attention().total bytes
+    const void* plan;  // a plan made by launch_attention_plan_bf16, or null: plan into the workspace
 };
 
 // Work decomposition and workspace partition of the attention step.
@@ -120,6 +121,7 @@ struct AttnPlan {
     int32_t P;              // workgroups (ranges of the stream-K line) per kv head
     int32_t max_slots;      // partial-result slots per kv head
     size_t off_plan, off_part_o, off_part_ml, total;
+    size_t plan_bytes;      // the plan alone (at off_plan)
 };
 
 size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);
@@ -149,6 +151,8 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
 hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s);
 hipError_t launch_qkv_f32(const QkvArgs& a, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream_t s);
+// The plan alone, into `plan` (AttnPlan::plan_bytes bytes).
+hipError_t launch_attention_plan_bf16(const AttnCall& a, const AttnPlan& p, void* plan, hipStream_t s);
 hipError_t launch_attention_f32(const AttnCall& a, const AttnPlan& p, hipStream_t s);
 
 }  // namespace semshare

@@ -63,6 +63,10 @@ def load() -> ctypes.CDLL:
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_prefill_attention_workspace": (SZ, [I64, I64, I32, I32, I32, I32]),
+        "semshare_attention_plan_bytes": (SZ, [I64, I64, I32, I32, I32, I32]),
+        "semshare_attention_plan": (I32, [P, I64, I64, I32, I32, I32, I32, P, SZ, P]),
+        "semshare_prefill_attention_planned": (I32, [P, SZ, P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ,
+                                                     I32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -313,10 +317,31 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
     return q_out, deviation
 
 
+def attention_plan_bytes(n_sel: int, n_tok: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                         dtype: torch.dtype = torch.bfloat16) -> int:
+    return int(load().semshare_attention_plan_bytes(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim,
+                                                    BF16 if dtype == torch.bfloat16 else FP32))
+
+
+def attention_plan(sel_pos: torch.Tensor, n_tok: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                   dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Work plan of prefill_attention for these selected positions (reusable across layers)."""
+    _dev(sel_pos, "sel_pos", torch.int32)
+    n_sel = sel_pos.numel()
+    need = attention_plan_bytes(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype)
+    if out is None:
+        out = torch.empty(max(need, 1), dtype=torch.uint8, device=sel_pos.device)
+    _dev(out, "plan", torch.uint8)
+    _call("semshare_attention_plan", _ptr(sel_pos), n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, BF16 if dtype == torch.bfloat16 else FP32,
+          _ptr(out), out.numel(), _stream())
+    return out
+
+
 def prefill_attention(q: torch.Tensor, sel_pos: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                       n_kv_heads: int, sm_scale: float = 0.0, out: Optional[torch.Tensor] = None,
-                      workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Causal GQA attention of the selected rows (q [n_sel, Hq, D]) over the cache."""
+                      workspace: Optional[torch.Tensor] = None, plan: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Causal GQA attention of the selected rows (q [n_sel, Hq, D]) over the cache (with `plan` from
+    attention_plan for the same positions and sizes: the plan step is skipped)."""
     _dev(q, "q")
     dt = q.dtype
     _dev(sel_pos, "sel_pos", torch.int32)
@@ -329,9 +354,15 @@ def prefill_attention(q: torch.Tensor, sel_pos: torch.Tensor, k_cache: torch.Ten
     _dev(out, "out", dt)
     ws = _workspace(prefill_attention_workspace_bytes(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dt),
                     workspace, q)
-    _call("semshare_prefill_attention", _ptr(q), _ptr(sel_pos), n_sel, _ptr(k_cache), _ptr(v_cache), n_tok,
-          n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out), _ptr(ws), 0 if ws is None else ws.numel(),
-          _dt(q), _stream())
+    if plan is None:
+        _call("semshare_prefill_attention", _ptr(q), _ptr(sel_pos), n_sel, _ptr(k_cache), _ptr(v_cache), n_tok,
+              n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out), _ptr(ws), 0 if ws is None else ws.numel(),
+              _dt(q), _stream())
+    else:
+        _dev(plan, "plan", torch.uint8)
+        _call("semshare_prefill_attention_planned", _ptr(plan), plan.numel(), _ptr(q), _ptr(sel_pos), n_sel,
+              _ptr(k_cache), _ptr(v_cache), n_tok, n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out),
+              _ptr(ws), 0 if ws is None else ws.numel(), _dt(q), _stream())
     return out
 
 

@@ -200,3 +200,44 @@ def test_split_calls_equal_partial_prefill():
     qr, _, _ = orc.qkv_rows(x_all[sel], sel, w.wq, w.wk, w.wv, hq, hkv, d, dtype="bf16", want_kv=False)
     b = rotated_pair_bound(fp32_dot_error_bound(x_all[sel], w.wq), d) + 1e-6 * np.abs(qr)
     assert np.all(np.abs(host(q).reshape(len(sel), -1) - qr) <= bf16_ulp(qr) + b)
+
+
+@pytest.mark.parametrize("n_tok,hq,hkv,d,n_sel", [(700, 16, 4, 128, 200), (5120, 32, 8, 128, 1280),
+                                                  (300, 8, 8, 64, 300)])
+def test_planned_attention_equals_unplanned(n_tok, hq, hkv, d, n_sel):
+    """One plan from semshare_attention_plan serves several layers' calls
+    (different caches and queries, the same positions): each planned call is
+    bit for bit the call that makes its own plan, and agrees with the oracle
+    on sampled rows."""
+    cfg = CONFIGS[1]
+    announce(f"planned attention n_tok={n_tok} hq={hq} hkv={hkv} d={d} n_sel={n_sel}")
+    sel = workloads.make_sel_pos(cfg, n_tok, n_sel, tag=21)
+    ps = dev_i32(sel)
+    plan = ss.attention_plan(ps, n_tok, hq, hkv, d)
+    assert plan.numel() == ss.attention_plan_bytes(n_sel, n_tok, hq, hkv, d) > 0
+    for layer in range(2):
+        k, v = workloads.make_cache(cfg, 1, n_tok, n_kv_heads=hkv, head_dim=d, tag=30 + layer)
+        q = workloads.make_rows(cfg, n_sel, hq * d, tag=40 + layer).reshape(n_sel, hq, d)
+        qd, kd, vd = dev(q, "bf16"), dev(k[0], "bf16"), dev(v[0], "bf16")
+        want = ss.prefill_attention(qd, ps, kd, vd, hkv)
+        got = ss.prefill_attention(qd, ps, kd, vd, hkv, plan=plan)
+        assert torch.equal(got, want)
+        rows = np.unique(np.linspace(0, n_sel - 1, 6).astype(int))
+        ref = orc.attention_rows(host(qd)[rows], sel[rows], host(kd), host(vd), hq, hkv, d, dtype="bf16")
+        assert np.max(np.abs(host(got)[rows].reshape(len(rows), -1) - ref.reshape(len(rows), -1))) <= ATOL["bf16"]
+
+
+def test_plan_for_other_sizes_is_not_used():
+    """A plan made for other sizes is rejected on the device: the call writes nothing."""
+    cfg = CONFIGS[1]
+    n_tok, hq, hkv, d, n_sel = 700, 16, 4, 128, 200
+    announce("plan size check")
+    sel = workloads.make_sel_pos(cfg, n_tok, n_sel, tag=22)
+    ps = dev_i32(sel)
+    other = ss.attention_plan(ps, n_tok + 64, hq, hkv, d)  # same buffer size, other n_tok
+    assert other.numel() >= ss.attention_plan_bytes(n_sel, n_tok, hq, hkv, d)
+    k, v = workloads.make_cache(cfg, 1, n_tok, n_kv_heads=hkv, head_dim=d, tag=23)
+    q = workloads.make_rows(cfg, n_sel, hq * d, tag=24).reshape(n_sel, hq, d)
+    out = torch.full((n_sel, hq, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    ss.prefill_attention(dev(q, "bf16"), ps, dev(k[0], "bf16"), dev(v[0], "bf16"), hkv, out=out, plan=other)
+    assert torch.all(out == 7.0)
