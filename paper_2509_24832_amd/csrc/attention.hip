@@ -40,9 +40,11 @@
 // together whatever the mix of short and long causal ranges.  A workgroup
 // walks its range one segment (the part of a row tile inside it) at a time.  A row
 // tile inside a single range writes its output directly; the pieces of a row
-// tile that range boundaries cut write (m, l, O) in register order
-// (coalesced) to slots the plan assigns, and a combine kernel merges them by
-// log-sum-exp in piece order (deterministic).
+// tile that range boundaries cut write (m, l) in fp32 and O / l in bf16, in
+// register order (coalesced), to slots the plan assigns, and a combine kernel
+// merges them by log-sum-exp in piece order (deterministic).  bf16 pieces
+// halve that traffic; each adds one bf16 rounding (relative 2^-9) before the
+// output's own.
 #include <algorithm>
 #include <climits>
 
@@ -75,7 +77,7 @@ struct AttnArgs {
     const uint16_t* k_cache;  // [n_tok][Hkv][D]
     const uint16_t* v_cache;
     uint16_t* out;            // [n_sel][Hq][D]
-    f32x4_t* part_o;          // [Hkv][max_slots][NCOL * D / 4], register-native order
+    u32x2_t* part_o;          // [Hkv][max_slots][NCOL * D / 4] bf16 x4 (O / l), register-native order
     float2* part_ml;          // [Hkv][max_slots][NCOL]  (m, l)
     // plan (int32): header [kPlanHdr] = W, ranges P', split row tiles, slots, sizes;
     // ranges [P][4] = first unit, end unit, first row tile, piece index of
@@ -571,17 +573,18 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         return;
     }
 
-    // piece of a cut row tile: publish its (m, l, O) in register order
+    // piece of a cut row tile: publish its (m, l) and O / l in register order
     const int64_t sl = (int64_t)g * a.max_slots + slot;
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-        f32x4_t* po = a.part_o + ((sl * 4 + wave) * 2 + nb) * (C::kMd * 4 * 64) + lane;
+        u32x2_t* po = a.part_o + ((sl * 4 + wave) * 2 + nb) * (C::kMd * 4 * 64) + lane;
+        const float inv = l_tot[nb] > 0.0f ? 1.0f / l_tot[nb] : 0.0f;  // l = 0: no key of this piece
 #pragma unroll
         for (int i = 0; i < C::kMd; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                po[(i * 4 + r) * 64] = f32x4_t{oacc[nb][i][4 * r], oacc[nb][i][4 * r + 1], oacc[nb][i][4 * r + 2],
-                                               oacc[nb][i][4 * r + 3]};
+                po[(i * 4 + r) * 64] = u32x2_t{pack_bf16x2(oacc[nb][i][4 * r] * inv, oacc[nb][i][4 * r + 1] * inv),
+                                               pack_bf16x2(oacc[nb][i][4 * r + 2] * inv, oacc[nb][i][4 * r + 3] * inv)};
         if (half == 0) a.part_ml[sl * NCOL + col_of(nb)] = make_float2(m_run[nb], l_tot[nb]);
     }
 }
@@ -673,11 +676,16 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
     for (int k = 0; k < kPer; ++k) o[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < nu; ++c) {
         const float2 mlc = ml[c * NCOL];
-        const float w = __builtin_amdgcn_exp2f((mlc.x - M) * cl2);
-        L += w * mlc.y;
-        const f32x4_t* po = a.part_o + (((sl0 + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
+        const float wl = __builtin_amdgcn_exp2f((mlc.x - M) * cl2) * mlc.y;  // weight of O_c / l_c
+        L += wl;
+        const u32x2_t* po = a.part_o + (((sl0 + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) o[k] += w * po[(q4 + 4 * k) * 64];
+        for (int k = 0; k < kPer; ++k) {
+            const u32x2_t x = po[(q4 + 4 * k) * 64];
+            // bf16 -> fp32: the 16 bits on top
+            o[k] += wl * f32x4_t{__builtin_bit_cast(float, x[0] << 16), __builtin_bit_cast(float, x[0] & 0xffff0000u),
+                                 __builtin_bit_cast(float, x[1] << 16), __builtin_bit_cast(float, x[1] & 0xffff0000u)};
+        }
     }
     const float inv = 1.0f / L;
     uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D;
@@ -841,7 +849,7 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
         const size_t slots = (size_t)n_kv_heads * p.max_slots;
         p.plan_bytes = plan_ints * sizeof(int32_t);
         p.off_part_o = align256(p.plan_bytes);
-        p.off_part_ml = align256(p.off_part_o + slots * NCOL * head_dim * sizeof(float));
+        p.off_part_ml = align256(p.off_part_o + slots * NCOL * head_dim * sizeof(uint16_t));
         p.total = align256(p.off_part_ml + slots * NCOL * sizeof(float2));
     }
     return p;
@@ -856,7 +864,7 @@ AttnArgs attn_args(const AttnCall& a, const AttnPlan& p) {
     t.k_cache = static_cast<const uint16_t*>(a.k_cache);
     t.v_cache = static_cast<const uint16_t*>(a.v_cache);
     t.out = static_cast<uint16_t*>(a.out);
-    t.part_o = reinterpret_cast<f32x4_t*>(ws + p.off_part_o);
+    t.part_o = reinterpret_cast<u32x2_t*>(ws + p.off_part_o);
     t.part_ml = reinterpret_cast<float2*>(ws + p.off_part_ml);
     t.plan = reinterpret_cast<int32_t*>(ws + p.off_plan);
     t.n_sel = a.n_sel;
