@@ -276,7 +276,10 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
 
     // Sub-tile u is half u%2 of the 64-key tile u/2 in ring stage (u/2) % kStages.
     const uint32_t smem_lds = lds_addr(smem);
-    auto stage_of = [&](int u) { return smem_lds + ((u >> 1) % kStages) * C::kStage + (u & 1) * 32 * C::kRowBytes; };
+    auto stage_of = [&](int u) {
+        const uint32_t uu = (uint32_t)u;  // u >= 0: masks instead of signed remainders
+        return smem_lds + ((uu >> 1) & (kStages - 1)) * C::kStage + (uu & 1) * 32 * C::kRowBytes;
+    };
     // K fragments of sub-tile u (A operand of S^T, k-step s)
     auto read_k = [&](int u, bf16x8_t (&kf)[C::kKs]) {
         const uint32_t kb0 = stage_of(u) + k_ro0;
