@@ -267,10 +267,17 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     };
 
     f32x16_t oacc[2][C::kMd];
+    // O is zeroed after the first sub-tile's probabilities (zero_o): before
+    // it the accumulation registers hold Q and two score tiles only
+    auto zero_o = [&]() {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int i = 0; i < C::kMd; ++i) oacc[nb][i] = f32x16_t{};
+            for (int i = 0; i < C::kMd; ++i) {
+                oacc[nb][i] = f32x16_t{};
+                asm volatile("" : "+a"(oacc[nb][i]));
+            }
+    };
     float m_run[2] = {-1.0e30f, -1.0e30f}, l_run[2] = {0.0f, 0.0f};
     const float cl2 = a.cl2;
 
@@ -356,7 +363,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     };
     // accept the sub-tile's probabilities, or (rare) move the reference to
     // the sub-tile's maximum, rescale O and l, and form them again
-    auto settle = [&](const f32x16_t (&sacc)[2], bf16x8_t (&pb)[2][2], float (&ts)[2]) {
+    auto settle = [&](const f32x16_t (&sacc)[2], bf16x8_t (&pb)[2][2], float (&ts)[2], bool o_live) {
         if (__any(!(ts[0] <= kSumLimit) || !(ts[1] <= kSumLimit))) {
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb) {
@@ -367,14 +374,16 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
                 const float m_new = fmaxf(m_run[nb], mx);
                 const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * cl2);
                 m_run[nb] = m_new;
-                l_run[nb] *= alpha;
+                if (o_live) {
+                    l_run[nb] *= alpha;
 #pragma unroll
-                for (int i = 0; i < C::kMd; ++i) {
-                    // one accumulator at a time: bounded register staging
+                    for (int i = 0; i < C::kMd; ++i) {
+                        // one accumulator at a time: bounded register staging
+                        __builtin_amdgcn_sched_barrier(0);
+                        oacc[nb][i] *= alpha;
+                    }
                     __builtin_amdgcn_sched_barrier(0);
-                    oacc[nb][i] *= alpha;
                 }
-                __builtin_amdgcn_sched_barrier(0);
             }
             exp_pack(sacc, pb, ts);
         }
@@ -394,9 +403,6 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         for (int s = 0; s < C::kKs; ++s) {
             const u32x4_t w = p_l[nb] >= 0 ? qv[nb][s] : u32x4_t{0u, 0u, 0u, 0u};
             qf[nb][s] = __builtin_bit_cast(bf16x8_t, w);
-            // kept in accumulation registers (MFMA reads its B operand from
-            // there), leaving the vector registers to K/V fragments and softmax
-            asm volatile("" : "+a"(qf[nb][s]));
         }
     if (n_kt > 1) issue(1);
     if (n_kt > 2) issue(2);
@@ -411,9 +417,15 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     {
         bf16x8_t kf[C::kKs];
         read_k(0, kf);
-        s_mfma(kf, sA);
+        s_mfma(kf, sA);  // Q still in vector registers here
         mask(0, sA);
     }
+    // Q kept in accumulation registers from here on (MFMA reads its B operand
+    // from there), leaving the vector registers to K/V fragments and softmax
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int s = 0; s < C::kKs; ++s) asm volatile("" : "+a"(qf[nb][s]));
     // Sub-tile u with a successor: S(u+1) and PV(u-1) on the matrix cores
     // while the probabilities of u are formed.  An odd u first opens tile
     // (u+1)/2 (its loads done, the stage of tile (u+1)/2 - 2 free again).
@@ -515,7 +527,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
                     pc[nb][sp] = __builtin_bit_cast(bf16x8_t, u32x4_t{pw[8 * nb + 4 * sp], pw[8 * nb + 4 * sp + 1],
                                                                       pw[8 * nb + 4 * sp + 2], pw[8 * nb + 4 * sp + 3]});
         }
-        settle(cur, pc, ts);
+        settle(cur, pc, ts, has_prev);
         mask(u + 1, nxt);
     };
     // The last sub-tile u: PV(u-1) while its probabilities are formed, then PV(u).
@@ -527,14 +539,16 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             pv_mfma(vf, pp);
         }
         exp_pack(cur, pc, ts);
-        settle(cur, pc, ts);
+        settle(cur, pc, ts, has_prev);
         read_v(u, vf);
         pv_mfma(vf, pc);
     };
     if (n_sub == 1) {
+        zero_o();
         last(0, sA, pA, pB, false);
     } else {
         body(0, sA, sB, pA, pB, false, false);
+        zero_o();
         int u = 1;
         for (; u + 2 < n_sub; u += 2) {
             body(u, sB, sA, pB, pA, true, true);
