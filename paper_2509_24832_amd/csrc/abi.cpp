@@ -140,6 +140,10 @@ semshare_status_t check_prefill_shapes(const char* fn, int64_t n_sel, int64_t n_
         if (128 % G) return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 needs 128 %% (n_q_heads/n_kv_heads) == 0", fn);
         if (((int64_t)n_kv_heads * head_dim) % 128)
             return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 needs n_kv_heads*head_dim %% 128 == 0", fn);
+        // the projection addresses its operands by 32-bit byte offsets
+        if (need_hidden && (2 * n_sel * hidden >= (int64_t(1) << 31) ||
+                            2 * (int64_t)n_q_heads * head_dim * hidden >= (int64_t(1) << 31)))
+            return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 x_sel or a weight matrix of 2 GiB or more", fn);
     } else {
         if (head_dim > 128) return fail(SEMSHARE_E_UNSUPPORTED, "%s: fp32 supports head_dim <= 128", fn);
         if (n_tok > 8192) return fail(SEMSHARE_E_UNSUPPORTED, "%s: fp32 path supports n_tok <= 8192", fn);

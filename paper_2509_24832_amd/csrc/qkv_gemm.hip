@@ -44,10 +44,27 @@ struct Cfg {
     static constexpr int kLoads = kALoads + kBLoads;
 };
 
-typedef __attribute__((address_space(3))) void lds_void_t;
+// 16 bytes per lane from gbase + off (bytes) straight into LDS at lds_base +
+// 16 * lane (global_load_lds_dwordx4, M0 = the wave-uniform LDS base, scalar
+// base address + 32-bit lane offset).  Inline assembly on purpose: the
+// compiler models the builtin form as an LDS access that can complete out of
+// order, and then waits for lgkmcnt(0), i.e. for every LDS read in flight,
+// before each MFMA group, which serialises the operand reads with the
+// multiplies.  Stage readiness is established explicitly instead
+// (wait_vmcnt + ring_barrier).
+__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
+    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory", "m0");
+}
 
-__device__ __forceinline__ void g2lds(const void* g, unsigned char* lds) {
-    __builtin_amdgcn_global_load_lds(g, (lds_void_t*)lds, 16, 0, 0);
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
 // s_waitcnt vmcnt(n) (n < 16), other counters left at their maximum.
@@ -101,28 +118,30 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
     // Direct-load sources: instruction i of this wave fills LDS rows
     // [8*grp, 8*grp+8) of its operand; lane -> (row = 8*grp + lane/8, chunk pc = lane%8)
     // and loads the global chunk that the swizzle places there.  Sources are a
-    // uniform base (advanced per K tile) plus a fixed per-lane 32-bit offset.
+    // uniform base (advanced per K tile) plus a fixed per-lane 32-bit byte
+    // offset (operands below 2 GiB, checked by the caller).
     const int lrow = lane >> 3, lpc = lane & 7;
-    int32_t a_off[C::kALoads], b_off[C::kBLoads];
+    uint32_t a_off[C::kALoads], b_off[C::kBLoads];
 #pragma unroll
     for (int i = 0; i < C::kALoads; ++i) {
         const int row = 8 * (wave * C::kALoads + i) + lrow;
         int64_t grow = m0 + row;
         if (grow > g.n_sel - 1) grow = g.n_sel - 1;  // tail rows: computed, never stored
-        a_off[i] = (int32_t)(grow * g.hidden) + 8 * (lpc ^ ((row >> 1) & 7));
+        a_off[i] = 2u * (uint32_t)(grow * g.hidden + 8 * (lpc ^ ((row >> 1) & 7)));
     }
 #pragma unroll
     for (int i = 0; i < C::kBLoads; ++i) {
         const int row = 8 * (wave * C::kBLoads + i) + lrow;
-        b_off[i] = (ncol0 + row) * g.hidden + 8 * (lpc ^ ((row >> 1) & 7));
+        b_off[i] = 2u * (uint32_t)((ncol0 + row) * g.hidden + 8 * (lpc ^ ((row >> 1) & 7)));
     }
-    // load j (0 .. kLoads-1) of K tile kt into ring stage ST
-    auto issue_one = [&](int j, int kt, unsigned char* stage) {
+    const uint32_t smem_base = lds_addr(smem);
+    // load j (0 .. kLoads-1) of K tile kt into the ring stage at byte offset st_off
+    auto issue_one = [&](int j, int kt, uint32_t st_off) {
         if (j < C::kALoads)
-            g2lds(g.x + (int64_t)kt * kBK + a_off[j], stage + (wave * C::kALoads + j) * 1024);
+            g2lds(g.x + (int64_t)kt * kBK, a_off[j], smem_base + st_off + (wave * C::kALoads + j) * 1024);
         else
-            g2lds(wseg + (int64_t)kt * kBK + b_off[j - C::kALoads],
-                  stage + C::kABytes + (wave * C::kBLoads + (j - C::kALoads)) * 1024);
+            g2lds(wseg + (int64_t)kt * kBK, b_off[j - C::kALoads],
+                  smem_base + st_off + C::kABytes + (wave * C::kBLoads + (j - C::kALoads)) * 1024);
     };
 
     f32x16_t acc[2][C::kNB];
@@ -140,40 +159,67 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
     const int b_row0 = ((BN / 2) * wn + l32) * 128;
 
     const int nk = g.hidden / kBK;
-    for (int j = 0; j < C::kLoads; ++j) issue_one(j, 0, smem);
+    for (int j = 0; j < C::kLoads; ++j) issue_one(j, 0, 0);
     if (nk > 1)
-        for (int j = 0; j < C::kLoads; ++j) issue_one(j, 1, smem + C::kStage);
+        for (int j = 0; j < C::kLoads; ++j) issue_one(j, 1, C::kStage);
 
-    // one K tile on ring stage ST (compile-time, so every LDS address is a constant)
-    auto step = [&](auto st_c, int kt) {
-        constexpr int ST = decltype(st_c)::value;
-        constexpr int NEXT = (ST + 2) % kStages;
-        if (kt + 1 < nk) wait_vmcnt<C::kLoads>();
-        else wait_vmcnt<0>();
-        ring_barrier();  // tile kt visible to all waves; stage NEXT free again
-        const bool more = kt + 2 < nk;
-        const unsigned char* Ab = smem + ST * C::kStage;
+    // MFMA operands of one 16-wide k-step, double-buffered in registers: the
+    // LDS reads of step s + 1 are in flight while the MFMAs of step s run
+    bf16x8_t av[2][2], bv[2][C::kNB];
+    auto read_ops = [&](const unsigned char* Ab, int s, int buf) {
         const unsigned char* Bb = Ab + C::kABytes;
 #pragma unroll
+        for (int i = 0; i < 2; ++i)
+            av[buf][i] = *reinterpret_cast<const bf16x8_t*>(Ab + a_row0 + i * 32 * 128 + koff[s]);
+#pragma unroll
+        for (int k = 0; k < C::kNB; ++k)
+            bv[buf][k] = *reinterpret_cast<const bf16x8_t*>(Bb + b_row0 + k * 32 * 128 + koff[s]);
+    };
+    if (nk > 1) wait_vmcnt<C::kLoads>();
+    else wait_vmcnt<0>();
+    ring_barrier();  // tile 0 visible to all waves
+    read_ops(smem, 0, 0);
+
+    // one K tile on ring stage ST (compile-time, so every LDS address is a
+    // constant).  The loads of tile kt + 2 go to the stage tile kt - 1 left
+    // (all waves passed the barrier that ended their reads of it); past the
+    // last tile they repeat it into a stage nobody reads any more.  The last
+    // k-step waits for tile kt + 1, meets the other waves and starts reading
+    // its first operands (after the last tile too, harmlessly, so that no
+    // branch splits the step).  Each direct load sits between two MFMAs: a
+    // load that waits for the address unit then stalls the issue of this
+    // wave while its previous MFMA still runs, not while the pipe is empty.
+    auto step = [&](auto st_c, int kt) {
+        constexpr int ST = decltype(st_c)::value;
+        constexpr int NEXT = (ST + 2) % kStages, FOLLOW = (ST + 1) % kStages;
+        constexpr int kPerStep = C::kLoads / 4;  // direct loads per k-step
+        constexpr int kM = 2 * C::kNB;            // MFMAs per k-step
+        static_assert(2 * kPerStep <= kM, "a load after every other MFMA");
+        const int kt2 = kt + 2 < nk ? kt + 2 : nk - 1;
+        const unsigned char* Ab = smem + ST * C::kStage;
+#pragma unroll
         for (int s = 0; s < 4; ++s) {
-            bf16x8_t av[2], bv[C::kNB];
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-                av[i] = *reinterpret_cast<const bf16x8_t*>(Ab + a_row0 + i * 32 * 128 + koff[s]);
-#pragma unroll
-            for (int k = 0; k < C::kNB; ++k)
-                bv[k] = *reinterpret_cast<const bf16x8_t*>(Bb + b_row0 + k * 32 * 128 + koff[s]);
-            // spread the next-but-one tile's loads over the four k-steps
-            if (more) {
-#pragma unroll
-                for (int j = s * C::kLoads / 4; j < (s + 1) * C::kLoads / 4; ++j)
-                    issue_one(j, kt + 2, smem + NEXT * C::kStage);
+            const int cur = s & 1;
+            if (s < 3) {
+                read_ops(Ab, s + 1, cur ^ 1);
+            } else {
+                // tile kt + 1 has landed: in flight after it are only the
+                // loads of tile kt + 2 issued by the first three k-steps
+                wait_vmcnt<3 * kPerStep>();
+                // this wave's reads of tile kt are done: after the barrier the
+                // loads of tile kt + 3 refill its stage
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+                ring_barrier();
+                read_ops(smem + FOLLOW * C::kStage, 0, cur ^ 1);
             }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int k = 0; k < C::kNB; ++k)
-                    acc[i][k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[k], acc[i][k], 0, 0, 0);
+            for (int q = 0; q < kM; ++q) {
+                acc[q / C::kNB][q % C::kNB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    av[cur][q / C::kNB], bv[cur][q % C::kNB], acc[q / C::kNB][q % C::kNB], 0, 0, 0);
+                if (q % 2 == 0 && q / 2 < kPerStep) issue_one(s * kPerStep + q / 2, kt2, NEXT * C::kStage);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     };
     for (int kt = 0; kt < nk; kt += kStages) {
@@ -181,6 +227,7 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
         if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
         if (kt + 2 < nk) step(std::integral_constant<int, 2>{}, kt + 2);
     }
+    wait_vmcnt<0>();  // the repeated loads past the last tile have landed
     __syncthreads();  // all waves done with the ring before it becomes the epilogue tile
 
     // ---- epilogue: accumulators -> fp32 LDS tile
@@ -197,30 +244,54 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
             }
     __syncthreads();
 
+    // Each thread owns one 8-column group (cg) of rows r0, r0 + kRowStep, ...
+    // Rows go in batches of kBatch whose global reads (position, RoPE
+    // factors, old cache rows) are all issued before any of them is used, so
+    // their latencies overlap instead of adding up row by row.
     const int half_d = g.D / 2;
-    constexpr int kGroups = BN / 8;  // 8-column groups per row
+    constexpr int kGroups = BN / 8;             // 8-column groups per row
+    constexpr int kRowStep = 256 / kGroups;     // rows between a thread's items
+    constexpr int kItems = kBM / kRowStep;      // items per thread
+    constexpr int kBatch = 8;
+    static_assert(kItems % kBatch == 0, "batches divide the items");
+    const int cg = tid % kGroups, r0 = tid / kGroups;
+    const int32_t n = ncol0 + 8 * cg;           // column within the segment
+    const int32_t k0 = (n % g.D) >> 1;          // first RoPE pair of the group
+    const bool rope = seg < 2, kv = seg > 0, dev = kv && g.dev_parts;
 #pragma unroll 1
-    for (int ps = 0; ps < (kBM * kGroups) / 256; ++ps) {
-        const int item = ps * 256 + tid;
-        const int r = item / kGroups, cg = item % kGroups;
-        const int64_t m = m0 + r;
-        const int32_t n = ncol0 + 8 * cg;  // column within the segment
-        float v8[8];
-        {
-            const f32x4_t c0 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg);
-            const f32x4_t c1 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg + 4);
+    for (int b0 = 0; b0 < kItems; b0 += kBatch) {
+        int32_t p[kBatch];
+        float2 cs[kBatch][4];
+        u32x4_t old[kBatch];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) { v8[e] = c0[e]; v8[4 + e] = c1[e]; }
+        for (int u = 0; u < kBatch; ++u) {
+            const int64_t m = m0 + r0 + (b0 + u) * kRowStep;
+            const bool ok = m < g.n_sel;
+            p[u] = ok && kv ? g.pos[m] : -1;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) cs[u][e] = ok && rope ? g.rope[m * half_d + k0 + e] : make_float2(1.0f, 0.0f);
         }
-        float dsum = 0.0f;
-        if (m < g.n_sel) {
-            const int32_t p = g.pos[m];
-            if (seg < 2) {  // RoPE on q and k: pairs (2k, 2k+1) within the head
-                const int32_t k0 = (n % g.D) >> 1;
-                const float2* cs = g.rope + m * half_d + k0;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            old[u] = u32x4_t{0u, 0u, 0u, 0u};
+            if (dev && p[u] >= 0 && p[u] < g.n_tok)
+                old[u] = *reinterpret_cast<const u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n);
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int r = r0 + (b0 + u) * kRowStep;
+            const int64_t m = m0 + r;
+            float v8[8];
+            {
+                const f32x4_t c0 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg);
+                const f32x4_t c1 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg + 4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) { v8[e] = c0[e]; v8[4 + e] = c1[e]; }
+            }
+            if (rope) {  // RoPE on q and k: pairs (2k, 2k+1) within the head
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float2 t = cs[e];
+                    const float2 t = cs[u][e];
                     const float x0 = v8[2 * e], x1 = v8[2 * e + 1];
                     v8[2 * e] = t.x * x0 - t.y * x1;
                     v8[2 * e + 1] = t.y * x0 + t.x * x1;
@@ -228,27 +299,28 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
             }
             const u32x4_t packed = u32x4_t{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
                                            pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
-            if (seg == 0) {
-                *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
-            } else if (p >= 0 && p < g.n_tok) {
-                uint16_t* dst = kvseg + (int64_t)p * seg_cols + n;
-                if (g.dev_parts) {
-                    const u32x4_t old = *reinterpret_cast<const u32x4_t*>(dst);
+            float dsum = 0.0f;
+            if (m < g.n_sel) {
+                if (seg == 0) {
+                    *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
+                } else if (p[u] >= 0 && p[u] < g.n_tok) {
+                    if (dev) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float d0 = bf16_lo(old[e]) - bf16_lo(packed[e]);
-                        const float d1 = bf16_hi(old[e]) - bf16_hi(packed[e]);
-                        dsum += d0 * d0 + d1 * d1;
+                        for (int e = 0; e < 4; ++e) {
+                            const float d0 = bf16_lo(old[u][e]) - bf16_lo(packed[e]);
+                            const float d1 = bf16_hi(old[u][e]) - bf16_hi(packed[e]);
+                            dsum += d0 * d0 + d1 * d1;
+                        }
                     }
+                    *reinterpret_cast<u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n) = packed;
                 }
-                *reinterpret_cast<u32x4_t*>(dst) = packed;
             }
-        }
-        if (g.dev_parts && seg > 0) {
-            // the kGroups threads of one tile row are consecutive lanes (kGroups divides 64)
+            if (dev) {
+                // the kGroups threads of one tile row are consecutive lanes (kGroups divides 64)
 #pragma unroll
-            for (int o = kGroups / 2; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o, kGroups);
-            if (cg == 0 && m < g.n_sel) g.dev_parts[(2 * m + (seg - 1)) * (seg_cols / BN) + nt] = dsum;
+                for (int o = kGroups / 2; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o, kGroups);
+                if (cg == 0 && m < g.n_sel) g.dev_parts[(2 * m + (seg - 1)) * (seg_cols / BN) + nt] = dsum;
+            }
         }
     }
 }
