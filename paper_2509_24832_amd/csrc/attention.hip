@@ -82,7 +82,8 @@ struct AttnArgs {
     // plan (int32): header [kPlanHdr] = W, ranges P', split row tiles, slots, sizes;
     // ranges [P][4] = first unit, end unit, first row tile, piece index of
     // its first segment; row tiles [n_tiles][8] = first unit, end unit, pmin,
-    // pmax, slot base, pieces, -, -; split row tiles [P]
+    // pmax, slot base, pieces, -, -; cut row tiles [P][4] = row tile, slot
+    // base, pieces, -
     int32_t* plan;
     int64_t n_sel, n_tok;
     int32_t Hq, Hkv, G, R;
@@ -655,64 +656,99 @@ __global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
     }
 }
 
-// Log-sum-exp merge of a cut row tile's pieces, in piece order.  One
-// workgroup per (cut row tile, wave slice, column block, kv head): the 32
-// columns x D values that attention wave `wave` held in block nb, laid out
-// as [i][r][lane] f32x4 per piece, so every load is a coalesced 1 KB row.
-// Thread t handles lane t % 64 and the (i, r) pairs t / 64 + 4k.  Head g
-// runs on the XCD that wrote its pieces (b % 8 == g with 8 kv heads).
+// Log-sum-exp merge of a cut row tile's pieces.  One workgroup per (cut row
+// tile, wave slice, column block, kv head): the 32 columns x D values that
+// attention wave `wave` held in block nb, laid out as [i][r][lane] f32x4 per
+// piece, so every load is a coalesced 1 KB row.  Thread t handles lane
+// t % 64 and the (i, r) pairs t / 64 + 4k.  Head g runs on the XCD that
+// wrote its pieces (b % 8 == g with 8 kv heads).  Pieces are read kPc at a
+// time, all their loads in flight together, and merged into a running
+// (max, sum, O) (one group in the common case of at most kPc pieces).
 template <int D>
-__global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
+__device__ __forceinline__ void combine_item(const AttnArgs& a, const int32_t* hdr, int item) {
     constexpr int kMd = D / 32;
     constexpr int kPer = kMd;  // (i, r) pairs per thread: 4 * kMd / 4
-    const int g = blockIdx.x % a.Hkv;
-    const int rest = blockIdx.x / a.Hkv;
+    constexpr int kPc = 4;
+    const int g = item % a.Hkv;
+    const int rest = item / a.Hkv;
     const int wave = (rest >> 1) & 3, nb = rest & 1;
     const int k = rest >> 3;  // cut row tile
-    const int32_t* hdr = a.plan;
-    if (!plan_fits(a, hdr) || k >= sload(hdr + 2)) return;
-    const int32_t* til = hdr + kPlanHdr + 4 * a.P;
-    const int tile = til[8 * a.n_tiles + k];
-    const int32_t pbase = til[8 * tile + 4], nu = til[8 * tile + 5];
+    const int32_t* ent = hdr + kPlanHdr + 4 * a.P + 8 * a.n_tiles + 4 * k;
+    const int tile = sload(ent), pbase = sload(ent + 1), nu = sload(ent + 2);
     const int tid = threadIdx.x, lane = tid & 63, q4 = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
     const int col = 64 * wave + 32 * nb + l32;
     const int64_t row = (int64_t)tile * a.R + col % a.R;
     if (row >= a.n_sel) return;
     const int32_t p = a.pos[row];
-    if (p < 0 || p >= a.n_tok) return;
     const int head = g * a.G + col / a.R;
     const float cl2 = a.cl2;
     const int64_t sl0 = (int64_t)g * a.max_slots + pbase;
     const float2* ml = a.part_ml + sl0 * NCOL + col;
-    float M = -1.0e30f;
-    for (int c = 0; c < nu; ++c) M = fmaxf(M, ml[c * NCOL].x);
-    float L = 0.0f;
+    const u32x2_t* po0 = a.part_o + ((sl0 * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
+    constexpr int64_t kPieceStride = 4 * 2 * kMd * 4 * 64;  // u32x2 per slot
+    float M = -1.0e30f, L = 0.0f;
     f32x4_t o[kPer];
 #pragma unroll
     for (int k = 0; k < kPer; ++k) o[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < nu; ++c) {
-        const float2 mlc = ml[c * NCOL];
-        const float wl = __builtin_amdgcn_exp2f((mlc.x - M) * cl2) * mlc.y;  // weight of O_c / l_c
-        L += wl;
-        const u32x2_t* po = a.part_o + (((sl0 + c) * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
+    for (int c0 = 0; c0 < nu; c0 += kPc) {
+        float2 mlc[kPc];
+        u32x2_t x[kPc][kPer];
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const u32x2_t x = po[(q4 + 4 * k) * 64];
-            // bf16 -> fp32: the 16 bits on top
-            o[k] += wl * f32x4_t{__builtin_bit_cast(float, x[0] << 16), __builtin_bit_cast(float, x[0] & 0xffff0000u),
-                                 __builtin_bit_cast(float, x[1] << 16), __builtin_bit_cast(float, x[1] & 0xffff0000u)};
+        for (int c = 0; c < kPc; ++c) {
+            mlc[c] = make_float2(-1.0e30f, 0.0f);
+            if (c0 + c < nu) {
+                mlc[c] = ml[(c0 + c) * NCOL];
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) x[c][k] = po0[(c0 + c) * kPieceStride + (q4 + 4 * k) * 64];
+            }
+        }
+        float Mn = M;
+#pragma unroll
+        for (int c = 0; c < kPc; ++c) Mn = fmaxf(Mn, mlc[c].x);
+        const float sc = __builtin_amdgcn_exp2f((M - Mn) * cl2);
+        M = Mn;
+        L *= sc;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) o[k] *= sc;
+#pragma unroll
+        for (int c = 0; c < kPc; ++c) {
+            if (c0 + c < nu) {
+                const float wl = __builtin_amdgcn_exp2f((mlc[c].x - M) * cl2) * mlc[c].y;  // weight of O_c / l_c
+                L += wl;
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) {
+                    // bf16 -> fp32: the 16 bits on top
+                    const u32x2_t xx = x[c][k];
+                    o[k] += wl * f32x4_t{__builtin_bit_cast(float, xx[0] << 16),
+                                         __builtin_bit_cast(float, xx[0] & 0xffff0000u),
+                                         __builtin_bit_cast(float, xx[1] << 16),
+                                         __builtin_bit_cast(float, xx[1] & 0xffff0000u)};
+                }
+            }
         }
     }
+    if (p < 0 || p >= a.n_tok) return;
     const float inv = 1.0f / L;
     uint16_t* op = a.out + (row * a.Hq + head) * (int64_t)D;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
         const int ir = q4 + 4 * k, i = ir >> 2, r = ir & 3;
-        const f32x4_t x = o[k] * inv;
+        const f32x4_t v = o[k] * inv;
         *reinterpret_cast<u32x2_t*>(op + 32 * i + 8 * r + 4 * half) =
-            u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+            u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
     }
+}
+
+// Items (cut row tile, wave slice, column block, kv head) in strides of the
+// grid, which the launch keeps at a multiple of 8 and far below the item
+// bound, so that workgroups are not spent on items a call does not have.
+template <int D>
+__global__ __launch_bounds__(256) void combine_kernel(AttnArgs a) {
+    const int32_t* hdr = a.plan;
+    if (!plan_fits(a, hdr)) return;
+    const int n_items = sload(hdr + 2) * 8 * a.Hkv;
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) combine_item<D>(a, hdr, item);
 }
 
 // Inclusive prefix sum over the 1024 threads of a workgroup; *total gets the
@@ -810,7 +846,13 @@ __global__ __launch_bounds__(1024) void plan_kernel(AttnArgs a) {
             til[8 * t + 5] = pieces;
             til[8 * t + 6] = 0;
             til[8 * t + 7] = 0;
-            if (cut) spl[n_split + incl_cut - 1] = t;
+            if (cut) {  // the combine reads the three fields at once
+                int32_t* e = spl + 4 * (n_split + incl_cut - 1);
+                e[0] = t;
+                e[1] = slots + incl_slots - cut * pieces;
+                e[2] = pieces;
+                e[3] = 0;
+            }
             if (s1 > s0) {
                 const int32_t j1 = first_range(s1);
                 for (int32_t j = first_range(s0 - kSegCost); j < j1; ++j) {
@@ -841,7 +883,8 @@ template <int D>
 hipError_t launch(const AttnArgs& args, bool make_plan, hipStream_t s) {
     if (make_plan) hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, args);
     hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(args.P * args.Hkv)), dim3(256), 0, s, args);
-    hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)(args.P * args.Hkv * 8)), dim3(256), 0, s, args);
+    hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)std::min(args.P * args.Hkv * 8, 2 * kCUs)), dim3(256), 0, s,
+                       args);
     return hipGetLastError();
 }
 
@@ -862,7 +905,7 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
         // range boundary inside them, and at most n_tiles + P pieces in all
         p.P = std::max(1, kCUs / n_kv_heads);
         p.max_slots = (int32_t)std::min<int64_t>(2 * (int64_t)p.P, p.n_tiles + p.P);
-        const size_t plan_ints = kPlanHdr + 4 * (size_t)p.P + 8 * (size_t)p.n_tiles + (size_t)p.P;
+        const size_t plan_ints = kPlanHdr + 4 * (size_t)p.P + 8 * (size_t)p.n_tiles + 4 * (size_t)p.P;
         const size_t slots = (size_t)n_kv_heads * p.max_slots;
         p.plan_bytes = plan_ints * sizeof(int32_t);
         p.off_part_o = align256(p.plan_bytes);
