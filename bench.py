@@ -53,8 +53,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "61ac46450d664258cd96a351f48410f68bce29ae352165bfcdc6a4d315aaabb2",
-                "bytes_per_call": 171212094}
+ATTN_TRAFFIC = {"source_sha256": "db0bd73c8bf2c3f32ef785b42161145498f381830e08e0b520378ca94d48183e",
+                "bytes_per_call": 138171231}
 
 
 def source_sha256(rel):

@@ -557,10 +557,18 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         }
         if (u + 1 < n_sub) {  // u = n_sub - 2
             body(u, sB, sA, pB, pA, true, true);
-            last(u + 1, sA, pA, pB, true);
-        } else {  // u = n_sub - 1
-            last(u, sB, pB, pA, true);
+            ++u;
+        } else {  // u = n_sub - 1: its scores and the previous probabilities move to where the other path has them
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                sA[nb] = sB[nb];
+#pragma unroll
+                for (int sp = 0; sp < 2; ++sp) pB[nb][sp] = pA[nb][sp];
+            }
         }
+        // one call site for the last sub-tile: the register assignment of
+        // the two paths above then agrees where they meet
+        last(u, sA, pA, pB, true);
     }
 
     // ---- results: oacc[nb][i][4r + e] = O[col][d = 32i + 8r + 4half + e]
