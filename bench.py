@@ -127,6 +127,7 @@ class Path:
         self.q_sel = torch.empty((n, self.hq, self.D), dtype=bf, device="cuda")
         self.out_sel = torch.empty_like(self.q_sel)
         # the attention work plan of the selection, made once per step and shared by layers 1..L-1
+        self.rope_sel = torch.empty(max(16, ss.rope_table_bytes(n, self.D)), dtype=torch.uint8, device="cuda")
         self.plan = torch.empty(max(1, ss.attention_plan_bytes(n, self.T, self.hq, self.hkv, self.D, bf)),
                                 dtype=torch.uint8, device="cuda")
         need = max(ws_hint,
@@ -158,13 +159,14 @@ class Path:
         m("attn0")
         ss.select_recompute(self.sigma, self.n_sel, out=self.sel)
         ss.attention_plan(self.sel, self.T, hq, hkv, self.D, out=self.plan)
+        ss.rope_table(self.sel, self.T, self.D, out=self.rope_sel)
         m("select")
         ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
         m("xsel")
         for l in range(1, self.L):
             wq, wk, wv = self.w[l]
             ss.qkv_rope(self.x_sel, self.sel, wq, wk, wv, self.asm_k[l], self.asm_v[l], hq, hkv, q_out=self.q_sel,
-                        workspace=self.ws)
+                        workspace=self.ws, rope_table=self.rope_sel)
             m("qkv")
             ss.prefill_attention(self.q_sel, self.sel, self.asm_k[l], self.asm_v[l], hkv, out=self.out_sel,
                                  workspace=self.ws, plan=self.plan)

@@ -179,6 +179,37 @@ size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_k
                                    int32_t head_dim, semshare_dtype_t dtype);
 
 /*
+ * The RoPE factor table of semshare_qkv_rope for one set of selected
+ * positions, made once and reused.  RoPE (Section 4.3.3: the recomputed q
+ * and k are rotated by their own positions) depends on the position and the
+ * pair index only, and the same tokens are recomputed in every layer
+ * (Section 4.2), so the layers of one selection can share one table.
+ *   table  device buffer of at least semshare_rope_table_bytes() bytes,
+ *          16-byte aligned; [n_sel][head_dim/2] float32 pairs (cos, sin) of
+ *          the angle sel_pos[i] * rope_base^(-2k/head_dim), computed in
+ *          float64 and rounded (positions outside [0, n_tok) use 0).
+ *          Written on `stream`.  bf16 projection only.
+ */
+size_t semshare_rope_table_bytes(int64_t n_sel, int32_t head_dim);
+semshare_status_t semshare_rope_table(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok, int32_t head_dim,
+                                      double rope_base, void* table, size_t table_bytes, void* stream);
+
+/*
+ * semshare_qkv_rope (bf16) with the RoPE factors from semshare_rope_table
+ * (same sel_pos values, n_sel, n_tok and head_dim; rope_base is the table's).
+ * The table stays owned by the caller and is only read.  Same results as
+ * semshare_qkv_rope with that rope_base, bit for bit; a table of other
+ * positions gives wrong results.  The workspace is the one
+ * semshare_qkv_rope_workspace() sizes.  dtype FP32: SEMSHARE_E_UNSUPPORTED.
+ */
+semshare_status_t semshare_qkv_rope_tabled(const void* rope_table, size_t rope_table_bytes, const void* x_sel,
+                                           const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
+                                           const void* wv, void* k_cache, void* v_cache, int64_t n_tok,
+                                           int32_t hidden, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                           void* q_out, float* deviation_out, void* workspace,
+                                           size_t workspace_bytes, semshare_dtype_t dtype, void* stream);
+
+/*
  * Step 2 of semshare_partial_prefill on its own (same kernels): causal
  * grouped-query attention of the selected rows over the cache (step 4
  * above), for q as semshare_qkv_rope writes it.  Keys j <= sel_pos[i] of kv

@@ -208,13 +208,14 @@ size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t 
     return prefill_layout(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
 }
 
-semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, int64_t n_sel,
-                                    const void* wq, const void* wk, const void* wv, void* k_cache,
-                                    void* v_cache, int64_t n_tok, int32_t hidden, int32_t n_q_heads,
-                                    int32_t n_kv_heads, int32_t head_dim, double rope_base, void* q_out,
-                                    float* deviation_out, void* workspace, size_t workspace_bytes,
-                                    semshare_dtype_t dtype, void* stream) {
-    const char* fn = "qkv_rope";
+namespace {
+// rope_table == nullptr: semshare_qkv_rope (the table is made in the workspace)
+semshare_status_t qkv_rope_impl(const char* fn, const void* rope_table, size_t rope_table_bytes, const void* x_sel,
+                                const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
+                                const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
+                                int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base,
+                                void* q_out, float* deviation_out, void* workspace, size_t workspace_bytes,
+                                semshare_dtype_t dtype, void* stream) {
     semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim, dtype, true);
     if (st != SEMSHARE_OK) return st;
     if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
@@ -226,11 +227,66 @@ semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, i
         return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
     st = check_workspace(fn, workspace, workspace_bytes, semshare::qkv_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dtype));
     if (st != SEMSHARE_OK) return st;
-    const semshare::QkvArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden, n_q_heads,
-                              n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace};
+    semshare::QkvArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden, n_q_heads,
+                        n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace};
+    if (rope_table) {
+        if (dtype != SEMSHARE_BF16) return fail(SEMSHARE_E_UNSUPPORTED, "%s: the RoPE table is for bf16 only", fn);
+        if (!aligned16(rope_table)) return fail(SEMSHARE_E_INVAL, "%s: rope_table must be 16-byte aligned", fn);
+        if (rope_table_bytes < semshare_rope_table_bytes(n_sel, head_dim))
+            return fail(SEMSHARE_E_INVAL, "%s: rope_table of %zu bytes, %zu needed", fn, rope_table_bytes,
+                        semshare_rope_table_bytes(n_sel, head_dim));
+        a.rope_table = rope_table;
+    }
     hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_qkv_bf16(a, (hipStream_t)stream)
                                           : semshare::launch_qkv_f32(a, (hipStream_t)stream);
     return from_hip(e, "qkv_rope launch");
+}
+}  // namespace
+
+semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, int64_t n_sel,
+                                    const void* wq, const void* wk, const void* wv, void* k_cache,
+                                    void* v_cache, int64_t n_tok, int32_t hidden, int32_t n_q_heads,
+                                    int32_t n_kv_heads, int32_t head_dim, double rope_base, void* q_out,
+                                    float* deviation_out, void* workspace, size_t workspace_bytes,
+                                    semshare_dtype_t dtype, void* stream) {
+    return qkv_rope_impl("qkv_rope", nullptr, 0, x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden,
+                         n_q_heads, n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace,
+                         workspace_bytes, dtype, stream);
+}
+
+size_t semshare_rope_table_bytes(int64_t n_sel, int32_t head_dim) {
+    if (n_sel <= 0 || head_dim <= 0 || (head_dim & 1)) return 0;
+    return (size_t)n_sel * (size_t)(head_dim / 2) * 2 * sizeof(float);
+}
+
+semshare_status_t semshare_rope_table(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok, int32_t head_dim,
+                                      double rope_base, void* table, size_t table_bytes, void* stream) {
+    const char* fn = "rope_table";
+    if (n_sel < 0 || n_tok < 0) return fail(SEMSHARE_E_INVAL, "%s: negative size", fn);
+    if (head_dim <= 0 || (head_dim & 1)) return fail(SEMSHARE_E_INVAL, "%s: head_dim must be even and > 0", fn);
+    if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
+    if (n_sel == 0) return ok();
+    if (!sel_pos || !table) return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (!aligned16(table)) return fail(SEMSHARE_E_INVAL, "%s: table must be 16-byte aligned", fn);
+    if (table_bytes < semshare_rope_table_bytes(n_sel, head_dim))
+        return fail(SEMSHARE_E_INVAL, "%s: table of %zu bytes, %zu needed", fn, table_bytes,
+                    semshare_rope_table_bytes(n_sel, head_dim));
+    return from_hip(semshare::launch_rope_table(sel_pos, n_sel, n_tok, head_dim, rope_base, table, (hipStream_t)stream),
+                    "rope_table launch");
+}
+
+semshare_status_t semshare_qkv_rope_tabled(const void* rope_table, size_t rope_table_bytes, const void* x_sel,
+                                           const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
+                                           const void* wv, void* k_cache, void* v_cache, int64_t n_tok,
+                                           int32_t hidden, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                           void* q_out, float* deviation_out, void* workspace,
+                                           size_t workspace_bytes, semshare_dtype_t dtype, void* stream) {
+    const char* fn = "qkv_rope_tabled";
+    if (!rope_table && n_sel > 0) return fail(SEMSHARE_E_INVAL, "%s: null rope_table", fn);
+    // rope_base only passes the shared checks: the table holds the factors
+    return qkv_rope_impl(fn, rope_table, rope_table_bytes, x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache,
+                         n_tok, hidden, n_q_heads, n_kv_heads, head_dim, 10000.0, q_out, deviation_out, workspace,
+                         workspace_bytes, dtype, stream);
 }
 
 namespace {

@@ -2,7 +2,8 @@
 // deviation of Appendix A.4), bf16 storage with fp32 accumulation.
 //
 // Kernels, in stream order:
-//  1. prep        RoPE (cos, sin) table for the selected positions, one entry
+//  1. prep        RoPE (cos, sin) table for the selected positions (skipped
+//                 when the caller passes one made beforehand), one entry
 //                 per (row, pair) shared by all heads and by q and k.
 //  2. qkv_gemm    projection + RoPE + deviation partials + cache scatter
 //                 (qkv_gemm.hip).
@@ -63,18 +64,25 @@ size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads,
            align256((size_t)n_sel * 2 * qkv_dev_parts(n_q_heads, n_kv_heads, head_dim, dtype) * sizeof(float));
 }
 
+hipError_t launch_rope_table(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok, int32_t head_dim,
+                             double rope_base, void* table, hipStream_t s) {
+    const int32_t half_d = head_dim / 2;
+    const int64_t n = n_sel * half_d;
+    if (n > 0)
+        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, sel_pos, n_sel, n_tok,
+                           half_d, log2(rope_base), static_cast<float2*>(table));
+    return hipGetLastError();
+}
+
 hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     unsigned char* ws = static_cast<unsigned char*>(a.workspace);
-    float2* rope = reinterpret_cast<float2*>(ws);
+    // a table made beforehand (shared by the layers of one selection), else
+    // one made here in the workspace
+    const float2* rope = a.rope_table ? static_cast<const float2*>(a.rope_table) : reinterpret_cast<float2*>(ws);
     float* dev_parts = a.deviation_out
                            ? reinterpret_cast<float*>(ws + qkv_workspace_dev_offset(a.n_sel, a.head_dim, SEMSHARE_BF16))
                            : nullptr;
-    const int32_t half_d = a.head_dim / 2;
-    {
-        const int64_t n = a.n_sel * half_d;
-        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sel_pos, a.n_sel,
-                           a.n_tok, half_d, log2(a.rope_base), rope);
-    }
+    if (!a.rope_table) launch_rope_table(a.sel_pos, a.n_sel, a.n_tok, a.head_dim, a.rope_base, ws, s);
     const int32_t bn = qkv_gemm_bn(a.n_q_heads, a.n_kv_heads, a.head_dim);
     GemmArgs g{};
     g.x = static_cast<const uint16_t*>(a.x_sel);

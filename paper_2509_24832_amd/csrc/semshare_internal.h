@@ -97,6 +97,7 @@ struct QkvArgs {
     void* q_out;           // [n_sel][Hq][D] or null (K/V only)
     float* deviation_out;  // [n_sel] or null
     void* workspace;       // qkv_workspace_bytes()
+    const void* rope_table = nullptr;  // bf16 path: [n_sel][D/2] (cos, sin) made by launch_rope_table, or null
 };
 
 // Step 2: causal GQA attention of the selected rows over the cache.
@@ -149,6 +150,9 @@ AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t
                         int32_t head_dim, int dtype);
 
 hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s);
+// The RoPE (cos, sin) table of the bf16 projection, [n_sel][head_dim/2] float2.
+hipError_t launch_rope_table(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok, int32_t head_dim,
+                             double rope_base, void* table, hipStream_t s);
 hipError_t launch_qkv_f32(const QkvArgs& a, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream_t s);
 // The plan alone, into `plan` (AttnPlan::plan_bytes bytes).

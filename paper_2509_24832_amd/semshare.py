@@ -63,6 +63,10 @@ def load() -> ctypes.CDLL:
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_prefill_attention_workspace": (SZ, [I64, I64, I32, I32, I32, I32]),
+        "semshare_rope_table_bytes": (SZ, [I64, I32]),
+        "semshare_rope_table": (I32, [P, I64, I64, I32, F64, P, SZ, P]),
+        "semshare_qkv_rope_tabled": (I32, [P, SZ, P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, P, P, P, SZ,
+                                           I32, P]),
         "semshare_attention_plan_bytes": (SZ, [I64, I64, I32, I32, I32, I32]),
         "semshare_attention_plan": (I32, [P, I64, I64, I32, I32, I32, I32, P, SZ, P]),
         "semshare_prefill_attention_planned": (I32, [P, SZ, P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ,
@@ -287,8 +291,9 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
              wv: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int,
              rope_base: float = 10000.0, q_out: Optional[torch.Tensor] = None, want_q: bool = True,
              deviation: Optional[torch.Tensor] = None, want_deviation: bool = False,
-             workspace: Optional[torch.Tensor] = None):
-    """Projection + RoPE + deviation + cache scatter of the selected rows.
+             workspace: Optional[torch.Tensor] = None, rope_table: Optional[torch.Tensor] = None):
+    """Projection + RoPE + deviation + cache scatter of the selected rows (with `rope_table` from
+    rope_table(), bf16: its factors instead of rope_base).
     Returns (q [n_sel, Hq, D] or None, deviation [n_sel] or None)."""
     _dev(x_sel, "x_sel")
     dt = x_sel.dtype
@@ -311,10 +316,35 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
     if not want_deviation:
         deviation = None
     ws = _workspace(qkv_rope_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dt), workspace, x_sel)
+    if rope_table is not None:
+        _dev(rope_table, "rope_table", torch.uint8)
+        _call("semshare_qkv_rope_tabled", _ptr(rope_table), rope_table.numel(), _ptr(x_sel), _ptr(sel_pos), n_sel,
+              _ptr(wq) if want_q else None, _ptr(wk), _ptr(wv), _ptr(k_cache), _ptr(v_cache), n_tok, hidden,
+              n_q_heads, n_kv_heads, head_dim, _ptr(q_out), _ptr(deviation), _ptr(ws),
+              0 if ws is None else ws.numel(), _dt(x_sel), _stream())
+        return q_out, deviation
     _call("semshare_qkv_rope", _ptr(x_sel), _ptr(sel_pos), n_sel, _ptr(wq) if want_q else None, _ptr(wk), _ptr(wv),
           _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, float(rope_base),
           _ptr(q_out), _ptr(deviation), _ptr(ws), 0 if ws is None else ws.numel(), _dt(x_sel), _stream())
     return q_out, deviation
+
+
+def rope_table_bytes(n_sel: int, head_dim: int) -> int:
+    return int(load().semshare_rope_table_bytes(n_sel, head_dim))
+
+
+def rope_table(sel_pos: torch.Tensor, n_tok: int, head_dim: int, rope_base: float = 10000.0,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """RoPE factors of qkv_rope for these selected positions (reusable across layers), as bytes."""
+    _dev(sel_pos, "sel_pos", torch.int32)
+    n_sel = sel_pos.numel()
+    need = rope_table_bytes(n_sel, head_dim)
+    if out is None:
+        out = torch.empty(max(need, 16), dtype=torch.uint8, device=sel_pos.device)
+    _dev(out, "rope_table", torch.uint8)
+    _call("semshare_rope_table", _ptr(sel_pos), n_sel, n_tok, head_dim, float(rope_base), _ptr(out), out.numel(),
+          _stream())
+    return out
 
 
 def attention_plan_bytes(n_sel: int, n_tok: int, n_q_heads: int, n_kv_heads: int, head_dim: int,

@@ -186,3 +186,23 @@ def test_split_call_validation(lib):
         assert 0 < ws <= 8 * 64 * slot + 4 * (4 + 5 * 32 + 8 * (n_sel // 64 + 1)) + 1024, (n_sel, n_tok, ws)
     assert L.semshare_prefill_attention_workspace(1280, 5120, 32, 8, 128, 1) >= 8 * 52 * slot  # 20 row tiles + 32
     assert L.semshare_prefill_attention_workspace(256, 256, 32, 8, 128, 0) == 0  # fp32 path: no workspace
+
+
+def test_rope_table_validation(lib):
+    L = ss.load()
+    assert L.semshare_rope_table_bytes(1280, 128) == 1280 * 64 * 8
+    assert L.semshare_rope_table_bytes(0, 128) == 0 and L.semshare_rope_table_bytes(8, 7) == 0
+    assert L.semshare_rope_table(FAKE, 8, 16, 7, 1e4, FAKE, 1 << 20, None) == b.E_INVAL  # odd head_dim
+    assert L.semshare_rope_table(FAKE, 8, 16, 128, 0.0, FAKE, 1 << 20, None) == b.E_INVAL  # rope_base
+    assert L.semshare_rope_table(FAKE, 8, 16, 128, 1e4, FAKE, 8 * 64 * 8 - 1, None) == b.E_INVAL  # too small
+    assert L.semshare_rope_table(FAKE, 8, 16, 128, 1e4, FAKE_ODD, 1 << 20, None) == b.E_INVAL  # alignment
+    assert L.semshare_rope_table(None, 0, 16, 128, 1e4, None, 0, None) == b.OK
+    # the projection with a table: its size and dtype, then the checks it shares with semshare_qkv_rope
+    rest = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 16, 256, 8, 2, 128, FAKE, None, FAKE, 1 << 30)
+    assert L.semshare_qkv_rope_tabled(FAKE, 8 * 64 * 8 - 1, *rest, 1, None) == b.E_INVAL
+    assert L.semshare_qkv_rope_tabled(FAKE_ODD, 1 << 20, *rest, 1, None) == b.E_INVAL
+    assert L.semshare_qkv_rope_tabled(None, 0, *rest, 1, None) == b.E_INVAL
+    assert L.semshare_qkv_rope_tabled(FAKE, 1 << 20, *rest, 0, None) == b.E_UNSUPPORTED  # fp32 projection
+    bad_n = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 256, 8, 2, 128, FAKE, None, FAKE, 1 << 30)
+    assert L.semshare_qkv_rope_tabled(FAKE, 1 << 20, *bad_n, 1, None) == b.E_INVAL  # n_sel > n_tok
+

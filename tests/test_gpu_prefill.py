@@ -241,3 +241,28 @@ def test_plan_for_other_sizes_is_not_used():
     out = torch.full((n_sel, hq, d), 7.0, dtype=torch.bfloat16, device="cuda")
     ss.prefill_attention(dev(q, "bf16"), ps, dev(k[0], "bf16"), dev(v[0], "bf16"), hkv, out=out, plan=other)
     assert torch.all(out == 7.0)
+
+
+@pytest.mark.parametrize("n_tok,hidden,hq,hkv,d,n_sel", [(700, 512, 16, 4, 128, 200), (300, 256, 8, 8, 64, 300),
+                                                         (5120, 512, 32, 8, 128, 1280)])
+def test_shared_rope_table_equals_own(n_tok, hidden, hq, hkv, d, n_sel):
+    """One RoPE table from semshare_rope_table serves several layers'
+    projections (different weights and caches, the same positions): each call
+    with it is bit for bit the call that makes its own table (q, caches,
+    deviation)."""
+    cfg = CONFIGS[1]
+    announce(f"shared rope table n_tok={n_tok} hidden={hidden} hq={hq} hkv={hkv} d={d} n_sel={n_sel}")
+    dt = cfg.dtype
+    sel = workloads.make_sel_pos(cfg, n_tok, n_sel, tag=51)
+    ps = dev_i32(sel)
+    table = ss.rope_table(ps, n_tok, d)
+    assert table.numel() == ss.rope_table_bytes(n_sel, d) == n_sel * (d // 2) * 8
+    for layer in range(2):
+        x_all, w, k, v, _ = _case(cfg, n_tok, hidden, hq, hkv, d, n_sel, tag=60 + layer)
+        xs = dev(x_all[sel], dt)
+        wq, wk, wv = dev(w.wq, dt), dev(w.wk, dt), dev(w.wv, dt)
+        k1, v1, k2, v2 = dev(k, dt), dev(v, dt), dev(k, dt), dev(v, dt)
+        q1, dev1 = ss.qkv_rope(xs, ps, wq, wk, wv, k1, v1, hq, hkv, want_deviation=True)
+        q2, dev2 = ss.qkv_rope(xs, ps, wq, wk, wv, k2, v2, hq, hkv, want_deviation=True, rope_table=table)
+        for a, b in ((q1, q2), (dev1, dev2), (k1, k2), (v1, v2)):
+            assert torch.equal(a, b)
