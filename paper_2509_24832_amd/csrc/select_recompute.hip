@@ -4,7 +4,8 @@
 //
 // One 1024-thread workgroup.  For non-negative floats the bit pattern orders
 // like the value, so a 4-pass, 8-bit-digit radix select over the bits finds
-// the threshold value T with count(> T) < n_sel <= count(>= T).  A final pass
+// the threshold value T with count(> T) < n_sel <= count(>= T); each pass
+// finds its digit by a block-wide scan of the 256 counts.  A final pass
 // walks the positions in order and keeps every value > T plus the first
 // (n_sel - count(> T)) values == T, compacting with block-wide prefix sums,
 // which yields the ascending output directly.
@@ -56,21 +57,27 @@ __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ si
     uint32_t prefix = 0, hi_mask = 0, need = (uint32_t)n_sel;
     for (int shift = 24; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += kT) hist[i] = 0;
+        if (tid == 0) {  // overwritten below by the thread whose digit crosses `need` (1 <= need)
+            s_digit = 0;
+            s_need = need;
+        }
         __syncthreads();
         for (int32_t i = tid; i < n_tok; i += kT) {
             const uint32_t u = key_of(sigma[i]);
             if ((u & hi_mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
         }
         __syncthreads();
-        if (tid == 0) {
-            uint32_t cum = 0, digit = 0, nd = need;
-            for (int b = 255; b >= 0; --b) {
-                const uint32_t h = hist[b];
-                if (cum + h >= need) { digit = (uint32_t)b; nd = need - cum; break; }
-                cum += h;
+        // the digit: counts of the higher digits summed from the top, the one
+        // thread whose digit crosses `need` publishes it (a block-wide scan,
+        // not a serial walk over the 256 bins)
+        {
+            const uint32_t h = tid < 256 ? hist[255 - tid] : 0u;
+            uint32_t above, d1, tot, d2;
+            block_scan2(h, 0u, above, d1, tot, d2, sw);
+            if (tid < 256 && above < need && above + h >= need) {
+                s_digit = 255u - (uint32_t)tid;
+                s_need = need - above;
             }
-            s_digit = digit;
-            s_need = nd;
         }
         __syncthreads();
         prefix |= s_digit << shift;
