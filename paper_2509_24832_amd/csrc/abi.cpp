@@ -67,6 +67,9 @@ semshare_status_t semshare_lsh_encode(const void* x, const void* planes, uint64_
     if (dim <= 0) return fail(SEMSHARE_E_INVAL, "lsh_encode: dim must be > 0");
     if (dtype == SEMSHARE_BF16 && dim % 64)
         return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: bf16 needs dim %% 64 == 0 (got %d)", dim);
+    // the bf16 kernel addresses 32 rows of x and the n_bits planes by 32-bit byte offsets
+    if (dtype == SEMSHARE_BF16 && dim > (1 << 20))
+        return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: bf16 needs dim <= 2^20 (got %d)", dim);
     if (dtype == SEMSHARE_FP32 && dim % 4)
         return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: fp32 needs dim %% 4 == 0 (got %d)", dim);
     if (n_tok > (int64_t(1) << 31) - 64) return fail(SEMSHARE_E_UNSUPPORTED, "lsh_encode: n_tok too large");

@@ -3,12 +3,18 @@
 //
 // bf16: a [T, d] x [n_bits, d]^T GEMM on v_mfma_f32_32x32x16_bf16.  A
 // workgroup owns 32 rows and all n_bits columns; wave w owns columns
-// [32w, 32w + 32).  Each lane streams 64 contiguous bytes of its row (and of
-// its hyperplane) per 64-wide K chunk; the K order inside the chunk is
-// permuted identically for both operands, which leaves the dot products
-// unchanged.  The epilogue never materialises the projections: a wave ballot
-// of (acc > 0) over one accumulator register yields 32 code bits of two rows
-// at once, written as 32-bit halves of the code words.
+// [32w, 32w + 32).  The hyperplanes (n_bits x d, L2-resident) are re-read by
+// every workgroup, so the kernel is bound by how many bytes each CU keeps in
+// flight: 64-wide K chunks of both operands stream through a ring of up to 7
+// LDS stages filled by direct-to-LDS loads (6 chunks, 120 KB, in flight at
+// 128 bits), with 128-byte rows whose 16-byte chunks are XOR-swizzled by
+// (row / 2) mod 8.  Inside a chunk each lane half consumes its own 16-byte
+// chunks (the K order is permuted identically for both operands, which leaves
+// the dot products unchanged).  The epilogue never materialises the
+// projections: a wave ballot of (acc > 0) over one accumulator register
+// yields 32 code bits of two rows at once, written as 32-bit halves of the
+// code words.  256-bit codes use a simpler variant that streams both operands
+// through registers one chunk ahead.
 //
 // fp32: projections on the VALU (one lane per hyperplane, four partial sums),
 // packed by a ballot over the 64 lanes of a wave.
@@ -24,6 +30,134 @@ __device__ __forceinline__ void load_chunk(const uint16_t* p, bf16x8_t (&v)[4]) 
     for (int i = 0; i < 4; ++i) {
         uint4 w = q[i];
         v[i] = __builtin_bit_cast(bf16x8_t, w);
+    }
+}
+
+typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
+
+// 16 bytes per lane from gbase + off (bytes) straight into LDS at lds_base +
+// 16 * lane (global_load_lds_dwordx4, M0 = the wave-uniform LDS base).  Inline
+// assembly, so the compiler does not wait for these loads (it models the
+// builtin as an LDS access and drains every LDS read before each MFMA);
+// readiness comes from the explicit vmcnt waits and barriers of the loop.
+__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
+    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n), other counters at their maximum (vmcnt split over bits [3:0] and [15:14])
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <int NB>
+struct LshCfg {
+    static constexpr int kRows = 32 + 32 * NB;                // rows of a stage: 32 of x, then 32*NB planes
+    static constexpr int kStage = kRows * 128;                 // bytes: 64 bf16 per row
+    static constexpr int kStages = (144 * 1024) / kStage < 7 ? (144 * 1024) / kStage : 7;
+    static constexpr int kLoads = kRows / 8;                   // 1-KB direct loads per stage (8 rows each)
+    static constexpr int kLoadsPerWave = kLoads / NB;
+    static_assert(kLoads % NB == 0, "loads divide over the waves");
+    static_assert((kStages - 1) * kLoadsPerWave < 64, "vmcnt range");
+};
+
+template <int NB>  // n_bits / 32 = waves per workgroup (2 or 4)
+__global__ __launch_bounds__(64 * NB) void lsh_encode_ring_kernel(const uint16_t* __restrict__ x,
+                                                                  const uint16_t* __restrict__ planes,
+                                                                  uint32_t* __restrict__ codes32,
+                                                                  int64_t n_tok, int32_t dim) {
+    using C = LshCfg<NB>;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[C::kStages * C::kStage];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int half = lane >> 5, l32 = lane & 31;
+    const int64_t row0 = (int64_t)blockIdx.x * 32;
+    const uint32_t smem_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)smem;
+
+    // direct-load sources: load i of a stage fills stage rows [8i, 8i + 8);
+    // lane -> (row 8i + lane/8, physical chunk lane%8), fetching the logical
+    // chunk the swizzle stores there.  Rows < 32 are rows of x (clamped to
+    // the last token: computed, never stored), the rest hyperplanes.
+    uint32_t off[C::kLoadsPerWave];
+    bool is_x[C::kLoadsPerWave];
+#pragma unroll
+    for (int j = 0; j < C::kLoadsPerWave; ++j) {
+        const int i = wave * C::kLoadsPerWave + j;
+        const int r = 8 * i + (lane >> 3);
+        const uint32_t chunk = (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+        is_x[j] = r < 32;  // uniform per load: 8 rows never straddle row 32
+        if (r < 32) {
+            const int64_t t = row0 + r < n_tok ? r : n_tok - 1 - row0;
+            off[j] = (uint32_t)(t * dim + 8 * chunk) * 2u;
+        } else {
+            off[j] = (uint32_t)((r - 32) * dim + 8 * chunk) * 2u;
+        }
+    }
+    const uint16_t* xb = x + row0 * (int64_t)dim;
+    auto issue = [&](int kt, int st) {
+#pragma unroll
+        for (int j = 0; j < C::kLoadsPerWave; ++j) {
+            const int i = wave * C::kLoadsPerWave + j;
+            g2lds(is_x[j] ? (const void*)(xb + (int64_t)kt * 64) : (const void*)(planes + (int64_t)kt * 64), off[j],
+                  smem_base + st * C::kStage + i * 1024);
+        }
+    };
+    const int nk = dim / 64;
+    // the ring always holds kStages - 1 chunks in flight; past the last chunk
+    // the last one is fetched again into a stage nobody reads any more
+#pragma unroll
+    for (int c = 0; c < C::kStages - 1; ++c) issue(c < nk ? c : nk - 1, c);
+
+    // read offsets: A rows l32, B rows 32 + 32 wave + l32; step s of a chunk
+    // reads 16-byte chunk 4 half + s, at its swizzled place
+    const uint32_t a_ro = l32 * 128, b_ro = (32 + 32 * wave + l32) * 128;
+    uint32_t koff[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) koff[s] = (uint32_t)(((4 * half + s) ^ ((l32 >> 1) & 7)) << 4);
+
+    f32x16_t acc = {};
+    int st = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_vmcnt<(C::kStages - 2) * C::kLoadsPerWave>();  // chunk kt has landed
+        ring_barrier();  // ... for every wave, and every wave is done with chunk kt - 1
+        const int nx = kt + C::kStages - 1;
+        issue(nx < nk ? nx : nk - 1, st == 0 ? C::kStages - 1 : st - 1);  // into chunk kt - 1's stage
+        const uint32_t sb = smem_base + st * C::kStage;
+        bf16x8_t a[4], b[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            a[s] = *(lds_bf16x8_t*)(uintptr_t)(sb + a_ro + koff[s]);
+            b[s] = *(lds_bf16x8_t*)(uintptr_t)(sb + b_ro + koff[s]);
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], b[s], acc, 0, 0, 0);
+        st = st + 1 == C::kStages ? 0 : st + 1;
+    }
+    wait_vmcnt<0>();  // the repeated loads past the last chunk have landed before the workgroup ends
+
+    // acc[v] holds C[row = 8*(v/4) + 4*half + (v%4)][col = 32*wave + (lane%32)]
+    constexpr int words32 = NB;  // 32-bit halves per code row
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const uint64_t bits = __ballot(acc[v] > 0.0f);
+        const int r_lo = 8 * (v / 4) + (v % 4);
+        const int64_t t_lo = row0 + r_lo, t_hi = t_lo + 4;
+        if (lane == 0 && t_lo < n_tok) codes32[t_lo * words32 + wave] = (uint32_t)bits;
+        if (lane == 1 && t_hi < n_tok) codes32[t_hi * words32 + wave] = (uint32_t)(bits >> 32);
     }
 }
 
@@ -106,8 +240,8 @@ hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes,
         const auto* pp = static_cast<const uint16_t*>(planes);
         auto* cp = reinterpret_cast<uint32_t*>(codes);
         switch (n_bits) {
-        case 64: hipLaunchKernelGGL(lsh_encode_bf16_kernel<2>, grid, dim3(128), 0, s, xp, pp, cp, n_tok, dim); break;
-        case 128: hipLaunchKernelGGL(lsh_encode_bf16_kernel<4>, grid, dim3(256), 0, s, xp, pp, cp, n_tok, dim); break;
+        case 64: hipLaunchKernelGGL(lsh_encode_ring_kernel<2>, grid, dim3(128), 0, s, xp, pp, cp, n_tok, dim); break;
+        case 128: hipLaunchKernelGGL(lsh_encode_ring_kernel<4>, grid, dim3(256), 0, s, xp, pp, cp, n_tok, dim); break;
         default: hipLaunchKernelGGL(lsh_encode_bf16_kernel<8>, grid, dim3(512), 0, s, xp, pp, cp, n_tok, dim); break;
         }
         return hipGetLastError();
