@@ -53,8 +53,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "db0bd73c8bf2c3f32ef785b42161145498f381830e08e0b520378ca94d48183e",
-                "bytes_per_call": 138171231}
+ATTN_TRAFFIC = {"source_sha256": "bbb32e83fc739eac60f53b2ca6f7a9e8a5fadc9dc415c8a09c3a2dfa34580d5d",
+                "bytes_per_call": 94021565}
 
 
 def source_sha256(rel):
