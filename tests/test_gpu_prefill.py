@@ -266,3 +266,27 @@ def test_shared_rope_table_equals_own(n_tok, hidden, hq, hkv, d, n_sel):
         q2, dev2 = ss.qkv_rope(xs, ps, wq, wk, wv, k2, v2, hq, hkv, want_deviation=True, rope_table=table)
         for a, b in ((q1, q2), (dev1, dev2), (k1, k2), (v1, v2)):
             assert torch.equal(a, b)
+
+
+def test_attention_plan_over_1024_row_tiles():
+    """More row tiles than the 1024 threads of the plan kernel (its passes
+    loop over the row tiles in blocks of 1024): 36864 rows, 8 query heads per
+    kv head (32 rows per row tile, 1152 row tiles per kv head).  The planned
+    and unplanned calls agree bit for bit and sampled rows, first, middle and
+    last, match the oracle."""
+    cfg = CONFIGS[1]
+    n_tok, hq, hkv, d = 36864, 32, 4, 64
+    n_sel = n_tok
+    announce(f"attention over 1152 row tiles n_tok={n_tok} hq={hq} hkv={hkv} d={d}")
+    sel = np.arange(n_sel, dtype=np.int32)
+    ps = dev_i32(sel)
+    k, v = workloads.make_cache(cfg, 1, n_tok, n_kv_heads=hkv, head_dim=d, tag=71)
+    q = workloads.make_rows(cfg, n_sel, hq * d, tag=72).reshape(n_sel, hq, d)
+    qd, kd, vd = dev(q, "bf16"), dev(k[0], "bf16"), dev(v[0], "bf16")
+    want = ss.prefill_attention(qd, ps, kd, vd, hkv)
+    plan = ss.attention_plan(ps, n_tok, hq, hkv, d)
+    got = ss.prefill_attention(qd, ps, kd, vd, hkv, plan=plan)
+    assert torch.equal(got, want)
+    rows = np.array([0, 1, 31, 32, 1023 * 32, 1024 * 32 + 5, n_sel // 2, n_sel - 33, n_sel - 1])
+    ref = orc.attention_rows(host(qd)[rows], sel[rows], host(kd), host(vd), hq, hkv, d, dtype="bf16")
+    assert np.max(np.abs(host(got)[rows].reshape(len(rows), -1) - ref.reshape(len(rows), -1))) <= ATOL["bf16"]
