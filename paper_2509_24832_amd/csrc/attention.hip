@@ -87,6 +87,7 @@ struct AttnArgs {
     int32_t* plan;
     int64_t n_sel, n_tok;
     int32_t Hq, Hkv, G, R;
+    int32_t lgR;              // log2(R): R = 256 / G is a power of two
     int32_t n_tiles;
     int32_t P;                // ranges (workgroups) per kv head
     int32_t max_slots;        // partial-result slots per kv head
@@ -166,6 +167,13 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = lane >> 5, l32 = lane & 31;
 
+    // the arguments the prologue needs, requested together: one wait for
+    // all of them rather than one per first use
+    const int32_t lgR = a.lgR, Hq = a.Hq, G = a.G;
+    const int64_t n_sel = a.n_sel;
+    const int32_t* const posp = a.pos;
+    const uint16_t* const qbase = a.q;
+    asm volatile("" ::"s"(lgR), "s"(Hq), "s"(G), "s"(n_sel), "s"(posp), "s"(qbase));
     // this lane's two query columns: column c of the tile is row c % R of
     // it, query head g*G + c / R
     int64_t row[2];
@@ -173,8 +181,8 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
         const int c = 64 * wave + 32 * nb + l32;
-        row[nb] = (int64_t)tile * a.R + c % a.R;
-        p_l[nb] = row[nb] < a.n_sel ? a.pos[row[nb]] : -1;  // checked below, after the Q loads are out
+        row[nb] = ((int64_t)tile << lgR) + (c & ((1 << lgR) - 1));
+        p_l[nb] = row[nb] < n_sel ? posp[row[nb]] : -1;  // checked below, after the Q loads are out
     }
     // Q^T operands: lane half h holds d in [h*D/2, h*D/2 + D/2).  All loads
     // are issued here, together with the positions; they move to the
@@ -185,7 +193,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     for (int nb = 0; nb < 2; ++nb) {
         const int c = 64 * wave + 32 * nb + l32;
         const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(
-            a.q + ((row[nb] < a.n_sel ? row[nb] : 0) * a.Hq + g * a.G + c / a.R) * (int64_t)D + half * (D / 2));
+            qbase + ((row[nb] < n_sel ? row[nb] : 0) * Hq + g * G + (c >> lgR)) * (int64_t)D + half * (D / 2));
 #pragma unroll
         for (int s = 0; s < C::kKs; ++s) qv[nb][s] = qp[s];
     }
@@ -581,7 +589,8 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     auto col_of = [&](int nb) { return 64 * wave + 32 * nb + (ln & 31); };
     auto store_out = [&](int nb, const f32x16_t (&o)[C::kMd], float inv) {
         const int c = col_of(nb);
-        uint16_t* op = a.out + (((int64_t)tile * a.R + c % a.R) * a.Hq + g * a.G + c / a.R) * (int64_t)D;
+        uint16_t* op =
+            a.out + ((((int64_t)tile << a.lgR) + (c & (a.R - 1))) * a.Hq + g * a.G + (c >> a.lgR)) * (int64_t)D;
 #pragma unroll
         for (int i = 0; i < C::kMd; ++i)
 #pragma unroll
@@ -686,10 +695,10 @@ __device__ __forceinline__ void combine_item(const AttnArgs& a, const int32_t* h
     const int tid = threadIdx.x, lane = tid & 63, q4 = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
     const int col = 64 * wave + 32 * nb + l32;
-    const int64_t row = (int64_t)tile * a.R + col % a.R;
+    const int64_t row = ((int64_t)tile << a.lgR) + (col & (a.R - 1));
     if (row >= a.n_sel) return;
     const int32_t p = a.pos[row];
-    const int head = g * a.G + col / a.R;
+    const int head = g * a.G + (col >> a.lgR);
     const float cl2 = a.cl2;
     const int64_t sl0 = (int64_t)g * a.max_slots + pbase;
     const float2* ml = a.part_ml + sl0 * NCOL + col;
@@ -941,6 +950,8 @@ AttnArgs attn_args(const AttnCall& a, const AttnPlan& p) {
     t.Hkv = a.n_kv_heads;
     t.G = a.n_q_heads / a.n_kv_heads;
     t.R = p.rows_per_tile;
+    t.lgR = 0;
+    while ((1 << (t.lgR + 1)) <= t.R) ++t.lgR;
     t.n_tiles = (int32_t)p.n_tiles;
     t.P = p.P;
     t.max_slots = p.max_slots;
