@@ -2,8 +2,11 @@
 // out[l][t] = ref[l][idx[t]] for every layer, one row = all kv heads of a
 // token.  A pure HBM copy: each wave owns 4 rows, decodes them once
 // (wave-uniform scalar math: tensor, layer, target token, source row) and
-// moves them with 16-byte non-temporal loads and stores, keeping up to 8
-// vector loads in flight per lane before the first store.  Rows whose index
+// moves them with 16-byte loads and non-temporal stores, keeping up to 8
+// vector loads in flight per lane before the first store.  The loads go
+// through the caches: a source row the index repeats is then read from them
+// (32 layers x 5120 rows with a uniformly random index, 63% distinct: 185 us
+// against 230 us with non-temporal loads; the same time with no repeats).  Rows whose index
 // lies outside [0, n_ref) are written as zeros and never read.
 #include "semshare_internal.h"
 
@@ -53,7 +56,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4* __restric
             for (int k = 0; k < 2; ++k) {
                 const uint32_t c = cb + lane + 64 * k;
                 v[u][k] = u32x4{0u, 0u, 0u, 0u};
-                if (live[u] && readable[u] && c < cpr) v[u][k] = __builtin_nontemporal_load(src[u] + c);
+                if (live[u] && readable[u] && c < cpr) v[u][k] = src[u][c];
             }
         }
 #pragma unroll
