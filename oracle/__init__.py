@@ -62,6 +62,7 @@ def _load() -> ctypes.CDLL:
                                        P, P, INT]),
         "orc_select_recompute": (None, [P, I64, I64, P]),
         "orc_similarity": (F64, [P, I64, F64, F64]),
+        "orc_bank_similarity": (None, [P, I64, P, P, INT, INT, F64, F64, P, P]),
         "orc_num_threads": (INT, []),
         "orc_set_num_threads": (None, [INT]),
     }
@@ -224,6 +225,24 @@ def select_recompute(sigma, n_sel: int) -> np.ndarray:
     pos = np.empty(n_sel, dtype=np.int32)
     _load().orc_select_recompute(_ptr(s), s.size, n_sel, _ptr(pos))
     return pos
+
+
+def bank_similarity(tgt_codes, ref_codes, offsets, dmin: float = 0.0, dmax: float = 30.0):
+    """Per reference prompt of a bank (codes [offsets[b], offsets[b+1]) of ref_codes): the sum of the
+    target tokens' top-1 Hamming distances within that prompt (int64) and its similarity score (fp64)."""
+    t = np.ascontiguousarray(tgt_codes, dtype=np.uint64)
+    r = np.ascontiguousarray(ref_codes, dtype=np.uint64)
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    if t.ndim != 2 or r.ndim != 2 or t.shape[1] != r.shape[1]:
+        raise ValueError("codes must be [n, n_words] with equal n_words")
+    n_prompts = off.size - 1
+    if n_prompts < 0 or (n_prompts > 0 and (off[0] < 0 or off[-1] > r.shape[0] or np.any(np.diff(off) < 0))):
+        raise ValueError("offsets must ascend within the bank")
+    dsum = np.empty(max(n_prompts, 0), dtype=np.int64)
+    sim = np.empty(max(n_prompts, 0), dtype=np.float64)
+    _load().orc_bank_similarity(_ptr(t), t.shape[0], _ptr(r), _ptr(off), n_prompts, t.shape[1], float(dmin),
+                                float(dmax), _ptr(dsum), _ptr(sim))
+    return dsum, sim
 
 
 def similarity(dist, dmin: float = 0.0, dmax: float = 30.0) -> float:

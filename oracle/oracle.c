@@ -380,3 +380,32 @@ double orc_similarity(const int32_t* dist, int64_t n_tgt, double dmin, double dm
     if (s > 1.0) s = 1.0;
     return s;
 }
+
+/* Reference retrieval over a bank (Appendix A.3 score, Section 5 gate): the
+ * bank holds n_prompts reference prompts, prompt b being the codes
+ * [offsets[b], offsets[b+1]) of ref.  For each prompt the target's tokens are
+ * matched against that prompt alone (orc_match); dist_sum[b] is the sum of
+ * their top-1 distances and sim[b] the similarity of those distances
+ * (orc_similarity).  A prompt with no tokens counts every target token at the
+ * largest possible distance, 64 * n_words. */
+void orc_bank_similarity(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, const int64_t* offsets,
+                         int32_t n_prompts, int32_t n_words, double dmin, double dmax, int64_t* dist_sum,
+                         double* sim) {
+    int32_t* idx = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n_tgt > 0 ? n_tgt : 1));
+    int32_t* dist = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n_tgt > 0 ? n_tgt : 1));
+    for (int32_t b = 0; b < n_prompts; ++b) {
+        const int64_t lo = offsets[b], hi = offsets[b + 1];
+        if (hi > lo) {
+            orc_match(tgt, n_tgt, ref + lo * n_words, hi - lo, n_words, idx, dist);
+        } else {
+            for (int64_t t = 0; t < n_tgt; ++t) dist[t] = 64 * n_words;
+        }
+        int64_t sum = 0;
+        for (int64_t t = 0; t < n_tgt; ++t) sum += dist[t];
+        dist_sum[b] = sum;
+        sim[b] = orc_similarity(dist, n_tgt, dmin, dmax);
+    }
+    free(idx);
+    free(dist);
+}
+

@@ -121,3 +121,61 @@ def test_similarity_closed_forms(orc):
     assert orc.similarity(np.full(10, 45, np.int32)) == 0.0
     assert orc.similarity(np.full(4, 15, np.int32)) == pytest.approx(0.5)
     assert orc.similarity(np.array([0, 6], np.int32)) == pytest.approx(0.9)
+
+
+# ------------------------------------------------- reference retrieval (A.3)
+
+def _py_bank(tgt, ref, offsets, dmin=0.0, dmax=30.0):
+    """Brute force: per prompt, the sum of the target tokens' top-1 distances
+    within it, and clip(1 - (mean - dmin) / (dmax - dmin), 0, 1)."""
+    n_words = tgt.shape[1]
+    sums, sims = [], []
+    for b in range(len(offsets) - 1):
+        prompt = ref[offsets[b]:offsets[b + 1]]
+        total = 0
+        for t in tgt:
+            if len(prompt) == 0:
+                total += 64 * n_words
+                continue
+            total += min(sum(bin(int(a) ^ int(c)).count("1") for a, c in zip(t, r)) for r in prompt)
+        mean = total / len(tgt)
+        sims.append(min(1.0, max(0.0, 1.0 - (mean - dmin) / (dmax - dmin))))
+        sums.append(total)
+    return np.array(sums), np.array(sims)
+
+
+@pytest.mark.parametrize("n_words", [1, 2, 4])
+def test_bank_similarity_equals_brute_force(orc, n_words):
+    rng = np.random.default_rng(40 + n_words)
+    tgt = rng.integers(0, 2**64, size=(23, n_words), dtype=np.uint64)
+    lens = [7, 0, 19, 1, 11]
+    ref = rng.integers(0, 2**64, size=(sum(lens), n_words), dtype=np.uint64)
+    ref[30:33] = tgt[4:7] ^ np.uint64(3)  # prompt 2 holds near copies of three target tokens
+    offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    dsum, sim = orc.bank_similarity(tgt, ref, offsets)
+    ps, pm = _py_bank(tgt, ref, offsets)
+    assert np.array_equal(dsum, ps)
+    assert np.allclose(sim, pm, rtol=0, atol=1e-15)
+    assert dsum[1] == len(tgt) * 64 * n_words  # the empty prompt: every distance the largest
+
+
+def test_bank_similarity_closed_forms(orc):
+    rng = np.random.default_rng(7)
+    tgt = rng.integers(0, 2**64, size=(40, 2), dtype=np.uint64)
+    other = rng.integers(0, 2**64, size=(40, 2), dtype=np.uint64)
+    flip2 = tgt.copy()
+    flip2[:, 0] ^= np.uint64(0b101)  # every token two bits away from its copy
+    bank = np.concatenate([other, tgt[::-1], ~tgt, flip2])
+    offsets = np.array([0, 40, 80, 120, 160], dtype=np.int64)
+    dsum, sim = orc.bank_similarity(tgt, bank, offsets)
+    assert dsum[1] == 0 and sim[1] == 1.0  # the same prompt in another order
+    # the complemented prompt: each token's top-1 is 128 minus its largest distance to another token
+    far = [max(sum(bin(int(a) ^ int(c)).count("1") for a, c in zip(t, r)) for r in tgt) for t in tgt]
+    assert dsum[2] == sum(128 - f for f in far) and sim[2] == 0.0
+    one, cmp1 = orc.bank_similarity(tgt[:1], ~tgt[:1], np.array([0, 1], dtype=np.int64))
+    assert one[0] == 128 and cmp1[0] == 0.0  # a single token against its complement
+    assert dsum[3] == 40 * 2 and sim[3] == pytest.approx(1.0 - 2.0 / 30.0)
+    assert np.argmax(sim) == 1 and sim[0] < 0.8  # random codes sit far below the 0.8 gate
+    # scale of the score: dmin/dmax are the paper's 0 and 30 by default
+    d2, s2 = orc.bank_similarity(tgt, bank, offsets, dmin=0.0, dmax=60.0)
+    assert np.array_equal(d2, dsum) and s2[3] == pytest.approx(1.0 - 2.0 / 60.0)
