@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--sweep", default="0.10,0.25,0.50", help="recompute fractions also timed ('' to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
+    ap.add_argument("--bank-similarity", action="store_true",
+                    help="instead of the hot path: time the reference retrieval over a bank (a 4096-token target "
+                         "against 16 prompts of 4096 tokens, 128- and 256-bit codes) and print its JSON line")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a known-size reference "
                          "for FETCH_SIZE / WRITE_SIZE counter runs)")
@@ -262,6 +265,48 @@ def cpu_baseline(cfg, frac, budget_s):
             "est_step_s": total, "est_stage_s": {k2: round(v2, 3) for k2, v2 in est.items()}}
 
 
+def bank_similarity_line(torch, np, ss, cfg, args):
+    """Reference retrieval (Appendix A.3 score over a bank): one 4096-token
+    target against 16 reference prompts of 4096 tokens (the bank shape),
+    seeded synthetic codes, 128 and 256 bits.  Integer VALU bound: 4W + 1
+    operations per (target, reference) pair (2W XOR, 2W popcount-accumulate,
+    one min), peak 256 CU x 4 SIMD x 16 lanes x 2.4 GHz = 39.3 T ops/s."""
+    out = {"metric": "bank_similarity_pairs_per_s", "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "higher_is_better": True, "data": "synthetic", "dtype": "u64",
+           "config": {"workload": "retrieval over a bank: 4096-token target x 16 prompts x 4096 tokens"}, "by_bits": {}}
+    n_tgt, n_prompts, per = 4096, 16, 4096
+    for w in (2, 4):
+        tgt = torch.from_numpy(cfg_codes(np, cfg, n_tgt, w, 1)).cuda()
+        ref = torch.from_numpy(cfg_codes(np, cfg, n_prompts * per, w, 2)).cuda()
+        off = torch.arange(n_prompts + 1, dtype=torch.int64, device="cuda") * per
+        ws = torch.empty(max(1, ss.semshare.load().semshare_bank_similarity_workspace(n_tgt, n_prompts)),
+                         dtype=torch.uint8, device="cuda")
+        for _ in range(args.warmup):
+            ss.bank_similarity(tgt, ref, off, workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            ss.bank_similarity(tgt, ref, off, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / args.steps * 1e3
+        pairs = n_tgt * n_prompts * per
+        ops = pairs * (4 * w + 1)
+        out["by_bits"][str(64 * w)] = {"us_per_call": round(us, 2), "pairs_per_s": pairs / (us * 1e-6),
+                                        "roofline": {"bound": "alu", "achieved": round(ops / us / 1e6, 2),
+                                                     "peak": 39.3, "unit": "T int ops/s",
+                                                     "frac": round(ops / us / 1e6 / 39.3, 3)}}
+    out["value"] = out["by_bits"]["128"]["pairs_per_s"]
+    print(json.dumps(out), flush=True)
+
+
+def cfg_codes(np, cfg, n, w, tag):
+    """Seeded synthetic code words (uniform bits), the generator of the configs."""
+    import workloads
+    return workloads.make_codes(cfg, n, w, tag=tag).view(np.int64)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -275,6 +320,9 @@ def main():
     from workloads import CONFIGS
 
     torch.cuda.set_device(0)
+    if args.bank_similarity:
+        bank_similarity_line(torch, np, ss, CONFIGS[3], args)
+        return
     cfg = CONFIGS[2]
     path = Path(torch, ss, cfg)
 

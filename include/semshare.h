@@ -277,6 +277,32 @@ semshare_status_t semshare_prefill_attention_planned(const void* plan, size_t pl
 semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
                                             int32_t* sel_pos, void* stream);
 
+/*
+ * Reference retrieval over a bank of prompts (Appendix A.3 similarity
+ * score; Section 5 applies reuse when it exceeds 0.8).  The bank holds
+ * n_prompts reference prompts, prompt b being the codes
+ * [ref_offsets[b], ref_offsets[b+1]) of ref.  For each prompt the target's
+ * tokens are matched against that prompt alone (top-1 Hamming distance, as
+ * semshare_match); dist_sum[b] is the sum of those distances and
+ * similarity[b] = clip(1 - (dist_sum[b]/n_tgt - dmin) / (dmax - dmin), 0, 1)
+ * in fp64 (the paper's min and max are 0 and 30).  A prompt with no tokens
+ * counts every target token at the largest distance, 64 * n_words; with
+ * n_tgt == 0 every score is 0.
+ *   tgt          [n_tgt][n_words] u64 codes.   ref [n_ref][n_words] u64.
+ *   ref_offsets  [n_prompts + 1] int64, device, ascending in [0, n_ref]
+ *                (the caller's contract; entries outside are clamped).
+ *   dist_sum     [n_prompts] int64, similarity [n_prompts] float64 (outputs).
+ *   n_words in 1..4; n_prompts <= 65535; dmax > dmin.
+ *   workspace    at least semshare_bank_similarity_workspace() bytes, 8-byte
+ *                aligned (per target tile partial sums; may be NULL when 0).
+ * The sums are exact integers and the scores do not depend on the schedule.
+ */
+size_t semshare_bank_similarity_workspace(int64_t n_tgt, int32_t n_prompts);
+semshare_status_t semshare_bank_similarity(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
+                                           const int64_t* ref_offsets, int32_t n_prompts, int32_t n_words,
+                                           double dmin, double dmax, int64_t* dist_sum, double* similarity,
+                                           void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -418,4 +418,32 @@ semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, i
                     "select_recompute launch");
 }
 
+size_t semshare_bank_similarity_workspace(int64_t n_tgt, int32_t n_prompts) {
+    if (n_tgt <= 0 || n_prompts <= 0) return 0;
+    return semshare::bank_similarity_workspace(n_tgt, n_prompts);
+}
+
+semshare_status_t semshare_bank_similarity(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
+                                           const int64_t* ref_offsets, int32_t n_prompts, int32_t n_words,
+                                           double dmin, double dmax, int64_t* dist_sum, double* similarity,
+                                           void* workspace, size_t workspace_bytes, void* stream) {
+    const char* fn = "bank_similarity";
+    if (n_tgt < 0 || n_ref < 0 || n_prompts < 0) return fail(SEMSHARE_E_INVAL, "%s: negative size", fn);
+    if (n_words < 1 || n_words > 4) return fail(SEMSHARE_E_INVAL, "%s: n_words must be 1..4 (got %d)", fn, n_words);
+    if (n_prompts > 65535) return fail(SEMSHARE_E_UNSUPPORTED, "%s: n_prompts must be <= 65535", fn);
+    if (n_tgt > (int64_t(1) << 31) - 256) return fail(SEMSHARE_E_UNSUPPORTED, "%s: n_tgt too large", fn);
+    if (!std::isfinite(dmin) || !std::isfinite(dmax) || !(dmax > dmin))
+        return fail(SEMSHARE_E_INVAL, "%s: need finite dmin < dmax", fn);
+    if (n_prompts == 0) return ok();
+    if (!ref_offsets || !dist_sum || !similarity || (n_tgt > 0 && !tgt) || (n_ref > 0 && !ref))
+        return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    const size_t need = semshare_bank_similarity_workspace(n_tgt, n_prompts);
+    if (workspace_bytes < need || (need > 0 && (!workspace || reinterpret_cast<uintptr_t>(workspace) % 8)))
+        return fail(SEMSHARE_E_INVAL, "%s: workspace of %zu bytes (8-byte aligned) needed, %zu given", fn, need,
+                    workspace_bytes);
+    return from_hip(semshare::launch_bank_similarity(tgt, n_tgt, ref, n_ref, ref_offsets, n_prompts, n_words, dmin,
+                                                     dmax, dist_sum, similarity, workspace, (hipStream_t)stream),
+                    "bank_similarity launch");
+}
+
 }  // extern "C"

@@ -80,6 +80,12 @@ hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_
 hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
                                    int32_t* sel_pos, hipStream_t s);
 
+size_t bank_similarity_workspace(int64_t n_tgt, int32_t n_prompts);
+hipError_t launch_bank_similarity(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
+                                  const int64_t* offsets, int32_t n_prompts, int32_t n_words, double dmin,
+                                  double dmax, int64_t* dist_sum, double* similarity, void* workspace,
+                                  hipStream_t s);
+
 // Step 1 of a partial-prefill layer: q/k/v projection, RoPE, deviation and
 // the scatter of k/v into the cache.
 struct QkvArgs {

@@ -63,6 +63,8 @@ def load() -> ctypes.CDLL:
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_prefill_attention_workspace": (SZ, [I64, I64, I32, I32, I32, I32]),
+        "semshare_bank_similarity_workspace": (SZ, [I64, I32]),
+        "semshare_bank_similarity": (I32, [P, I64, P, I64, P, I32, I32, F64, F64, P, P, P, SZ, P]),
         "semshare_rope_table_bytes": (SZ, [I64, I32]),
         "semshare_rope_table": (I32, [P, I64, I64, I32, F64, P, SZ, P]),
         "semshare_qkv_rope_tabled": (I32, [P, SZ, P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, P, P, P, SZ,
@@ -327,6 +329,34 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
           _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, float(rope_base),
           _ptr(q_out), _ptr(deviation), _ptr(ws), 0 if ws is None else ws.numel(), _dt(x_sel), _stream())
     return q_out, deviation
+
+
+def bank_similarity(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, ref_offsets: torch.Tensor,
+                    dmin: float = 0.0, dmax: float = 30.0, workspace: Optional[torch.Tensor] = None):
+    """Per reference prompt of a bank (codes [ref_offsets[b], ref_offsets[b+1]) of ref_codes): the sum of
+    the target tokens' top-1 Hamming distances within it and the similarity score.
+    Returns (dist_sum int64 [n_prompts], similarity float64 [n_prompts])."""
+    for name, t in (("tgt_codes", tgt_codes), ("ref_codes", ref_codes)):
+        if t.dim() != 2:
+            raise ValueError(f"{name} must be [n, n_words]")
+        _dev(t, name, torch.int64)
+    _dev(ref_offsets, "ref_offsets", torch.int64)
+    n_tgt, n_words = tgt_codes.shape
+    n_ref = ref_codes.shape[0]
+    if ref_codes.shape[1] != n_words:
+        raise ValueError("codes must have equal n_words")
+    n_prompts = ref_offsets.numel() - 1
+    if n_prompts < 0:
+        raise ValueError("ref_offsets needs n_prompts + 1 entries")
+    dist_sum = torch.empty(n_prompts, dtype=torch.int64, device=tgt_codes.device)  # every entry is written
+    sim = torch.empty(n_prompts, dtype=torch.float64, device=tgt_codes.device)
+    need = int(load().semshare_bank_similarity_workspace(n_tgt, n_prompts))
+    ws = workspace if workspace is not None else (torch.empty(need, dtype=torch.uint8, device=tgt_codes.device)
+                                                  if need else None)
+    _call("semshare_bank_similarity", _ptr(tgt_codes), n_tgt, _ptr(ref_codes), n_ref, _ptr(ref_offsets), n_prompts,
+          n_words, float(dmin), float(dmax), _ptr(dist_sum), _ptr(sim), _ptr(ws), 0 if ws is None else ws.numel(),
+          _stream())
+    return dist_sum, sim
 
 
 def rope_table_bytes(n_sel: int, head_dim: int) -> int:

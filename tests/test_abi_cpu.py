@@ -206,3 +206,25 @@ def test_rope_table_validation(lib):
     bad_n = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 256, 8, 2, 128, FAKE, None, FAKE, 1 << 30)
     assert L.semshare_qkv_rope_tabled(FAKE, 1 << 20, *bad_n, 1, None) == b.E_INVAL  # n_sel > n_tok
 
+
+def test_bank_similarity_validation(lib):
+    L = ss.load()
+    assert L.semshare_bank_similarity_workspace(4096, 16) == 32 * 16 * 8
+    assert L.semshare_bank_similarity_workspace(0, 16) == 0 and L.semshare_bank_similarity_workspace(10, 0) == 0
+    call = L.semshare_bank_similarity
+    ok_args = dict(tgt=FAKE, n_tgt=100, ref=FAKE, n_ref=50, off=FAKE, n_prompts=3, n_words=2, dmin=0.0, dmax=30.0,
+                   dsum=FAKE, sim=FAKE, ws=FAKE, ws_bytes=1 << 20)
+
+    def st(**kw):
+        a = dict(ok_args, **kw)
+        return call(a["tgt"], a["n_tgt"], a["ref"], a["n_ref"], a["off"], a["n_prompts"], a["n_words"], a["dmin"],
+                    a["dmax"], a["dsum"], a["sim"], a["ws"], a["ws_bytes"], None)
+    assert st(n_words=0) == b.E_INVAL and st(n_words=5) == b.E_INVAL
+    assert st(dmax=0.0) == b.E_INVAL and st(dmin=float("nan")) == b.E_INVAL
+    assert st(n_prompts=70000) == b.E_UNSUPPORTED
+    assert st(n_tgt=-1) == b.E_INVAL
+    assert st(ws_bytes=8) == b.E_INVAL and "workspace" in ss.last_error()
+    assert st(ws=FAKE + 4) == b.E_INVAL  # 8-byte alignment
+    assert st(off=None) == b.E_INVAL and st(sim=None) == b.E_INVAL
+    assert st(n_prompts=0, off=None, dsum=None, sim=None) == b.OK
+

@@ -198,3 +198,70 @@ def test_select_recompute_matches_oracle(n_tok, n_sel, levels):
     announce(f"select n_tok={n_tok} n_sel={n_sel} levels={levels}")
     got = ss.select_recompute(torch.from_numpy(sigma).cuda(), n_sel).cpu().numpy()
     assert np.array_equal(got, orc.select_recompute(sigma, n_sel))
+
+
+# ------------------------------------------------- reference retrieval (A.3)
+
+def _flip(codes: np.ndarray, rate: float, seed: int) -> np.ndarray:
+    """codes with each bit flipped with probability `rate` (seeded)."""
+    rng = np.random.default_rng(seed)
+    bits = rng.random((codes.shape[0], codes.shape[1], 64)) < rate
+    mask = (bits.astype(np.uint64) << np.arange(64, dtype=np.uint64)).sum(axis=2, dtype=np.uint64)
+    return codes ^ mask
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("n_words", [1, 2, 4])
+def test_bank_similarity_matches_oracle(n_words):
+    """Sums of top-1 distances per prompt bit-exact and scores equal to the
+    oracle's: prompts of 0, 1, 300, 700 (two LDS stages) and 1300 codes, a
+    ragged target of 333 tokens, near copies planted at several flip rates."""
+    cfg = CONFIGS[1]
+    announce(f"bank similarity W={n_words}")
+    tgt = workloads.make_codes(cfg, 333, n_words, tag=80 + n_words)
+    lens = [300, 0, 700, 1, 1300]
+    parts = [workloads.make_codes(cfg, n, n_words, tag=90 + i) if n else np.zeros((0, n_words), np.uint64)
+             for i, n in enumerate(lens)]
+    parts[2][:333] = _flip(tgt, 0.05, 1)   # a close prompt
+    parts[4][500:833] = _flip(tgt, 0.15, 2)  # a farther one
+    ref = np.concatenate(parts)
+    offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    dsum, sim = ss.bank_similarity(dev_codes(tgt), dev_codes(ref), torch.from_numpy(offsets).cuda())
+    rs, rm = orc.bank_similarity(tgt, ref, offsets)
+    assert np.array_equal(dsum.cpu().numpy(), rs)
+    assert np.allclose(sim.cpu().numpy(), rm, rtol=0, atol=1e-15)
+    assert int(np.argmax(rm)) == 2
+
+
+@pytest.mark.gpu
+def test_bank_similarity_bank_shape_picks_the_closest_member():
+    """One 4096-token target against a bank of 16 prompts of 4096 tokens at
+    128 bits, member b holding the target with bits flipped at rate
+    (0.02, 0.05, 0.1)[b % 3] (others random): the scores equal the oracle's
+    and the closest member scores highest."""
+    cfg = CONFIGS[3]
+    announce("bank similarity 4096 x 16 x 4096 W=2")
+    tgt = workloads.make_codes(cfg, 4096, 2, tag=13)
+    members = []
+    for b in range(16):
+        m = workloads.make_codes(cfg, 4096, 2, tag=200 + b)
+        if b in (3, 7, 11):
+            m = _flip(tgt, (0.02, 0.05, 0.1)[(b // 4) % 3], 300 + b)[np.random.default_rng(b).permutation(4096)]
+        members.append(m)
+    ref = np.concatenate(members)
+    offsets = (np.arange(17) * 4096).astype(np.int64)
+    dsum, sim = ss.bank_similarity(dev_codes(tgt), dev_codes(ref), torch.from_numpy(offsets).cuda())
+    rs, rm = orc.bank_similarity(tgt, ref, offsets)
+    assert np.array_equal(dsum.cpu().numpy(), rs)
+    assert np.allclose(sim.cpu().numpy(), rm, rtol=0, atol=1e-15)
+    assert int(np.argmax(sim.cpu().numpy())) == 3
+
+
+@pytest.mark.gpu
+def test_bank_similarity_empty_target():
+    cfg = CONFIGS[1]
+    announce("bank similarity empty target")
+    ref = workloads.make_codes(cfg, 10, 2, tag=5)
+    dsum, sim = ss.bank_similarity(dev_codes(np.zeros((0, 2), np.uint64)), dev_codes(ref),
+                                   torch.tensor([0, 4, 10], dtype=torch.int64, device="cuda"))
+    assert dsum.cpu().tolist() == [0, 0] and sim.cpu().tolist() == [0.0, 0.0]
