@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--sweep", default="0.10,0.25,0.50", help="recompute fractions also timed ('' to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
+    ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
+                    help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
+    ap.add_argument("--match-compare", action="store_true",
+                    help="time the XOR/popcount and int8-MFMA matchers side by side instead of the hot path")
     ap.add_argument("--bank-similarity", action="store_true",
                     help="instead of the hot path: time the reference retrieval over a bank (a 4096-token target "
                          "against 16 prompts of 4096 tokens, 128- and 256-bit codes) and print its JSON line")
@@ -56,8 +60,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "bbb32e83fc739eac60f53b2ca6f7a9e8a5fadc9dc415c8a09c3a2dfa34580d5d",
-                "bytes_per_call": 94021565}
+ATTN_TRAFFIC = {"source_sha256": "59404c5679c56e4f02c3ee28f4124f25ea63005f56862afd0c84ed45830ddba9",
+                "bytes_per_call": 93925158}
 
 
 def source_sha256(rel):
@@ -74,6 +78,7 @@ class Path:
 
         import workloads
         self.torch, self.ss, self.cfg = torch, ss, cfg
+        self.matcher = ss.match_mfma
         dev = "cuda"
         bf = torch.bfloat16
         T, d, L = cfg.n_tok, cfg.dim, cfg.n_layers
@@ -149,7 +154,7 @@ class Path:
         m("rope")
         ss.lsh_encode(self.e_rot, self.planes, out=self.codes_t)
         m("lsh")
-        ss.match(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
+        self.matcher(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
         m("match")
         ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
         m("gather")
@@ -301,6 +306,56 @@ def bank_similarity_line(torch, np, ss, cfg, args):
     print(json.dumps(out), flush=True)
 
 
+def match_compare_line(torch, np, ss, configs, args):
+    """The two top-1 Hamming matchers side by side (Sections 4.2, 4.3), on the
+    headline shape (5120 x 5120 tokens, 128 bits), the bank shape (4096 x
+    16 x 4096, 256 bits) and the long shape (32768 x 32768, 128 bits), seeded
+    synthetic codes.  XOR/popcount: integer VALU bound, 4W + 1 operations per
+    pair, peak 39.3 T ops/s.  int8 matrix cores: 2 n_b operations per pair
+    (one multiply-add per bit), dense int8 peak 5.0 P ops/s.  Both return
+    bit-identical outputs (checked here on every shape)."""
+    out = {"metric": "match_token_pairs_per_s", "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "higher_is_better": True, "data": "synthetic", "dtype": "u64",
+           "config": {"workload": "top-1 Hamming match, XOR/popcount vs int8 MFMA"}, "shapes": {}}
+    shapes = [("5120x5120_128b", configs[2], 5120, 5120, 2), ("4096x65536_256b", configs[3], 4096, 65536, 4),
+              ("32768x32768_128b", configs[4], 32768, 32768, 2)]
+    for name, cfg, n_tgt, n_ref, w in shapes:
+        tgt = torch.from_numpy(cfg_codes(np, cfg, n_tgt, w, 1)).cuda()
+        ref = torch.from_numpy(cfg_codes(np, cfg, n_ref, w, 2)).cuda()
+        pairs = n_tgt * n_ref
+        row = {}
+        res = {}
+        for kind, fn in (("xor", ss.match), ("mfma", ss.match_mfma)):
+            idx = torch.empty(n_tgt, dtype=torch.int32, device="cuda")
+            dist = torch.empty(n_tgt, dtype=torch.int32, device="cuda")
+            for _ in range(args.warmup):
+                fn(tgt, ref, idx=idx, dist=dist)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                fn(tgt, ref, idx=idx, dist=dist)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / args.steps * 1e3
+            res[kind] = (idx.cpu(), dist.cpu())
+            if kind == "xor":
+                ops, peak, unit, bound = pairs * (4 * w + 1), 39.3, "T int ops/s", "alu"
+                achieved = ops / us / 1e6
+            else:
+                ops, peak, unit, bound = pairs * 2 * 64 * w, 5000.0, "T int8 ops/s", "mfma"
+                achieved = ops / us / 1e6
+            row[kind] = {"us_per_call": round(us, 2), "pairs_per_s": pairs / (us * 1e-6),
+                         "roofline": {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+                                      "frac": round(achieved / peak, 3)}}
+        row["identical"] = bool(torch.equal(res["xor"][0], res["mfma"][0]) and torch.equal(res["xor"][1], res["mfma"][1]))
+        row["speedup_mfma"] = round(row["xor"]["us_per_call"] / row["mfma"]["us_per_call"], 2)
+        out["shapes"][name] = row
+        del tgt, ref
+    out["value"] = out["shapes"]["5120x5120_128b"]["mfma"]["pairs_per_s"]
+    print(json.dumps(out), flush=True)
+
+
 def cfg_codes(np, cfg, n, w, tag):
     """Seeded synthetic code words (uniform bits), the generator of the configs."""
     import workloads
@@ -323,8 +378,12 @@ def main():
     if args.bank_similarity:
         bank_similarity_line(torch, np, ss, CONFIGS[3], args)
         return
+    if args.match_compare:
+        match_compare_line(torch, np, ss, CONFIGS, args)
+        return
     cfg = CONFIGS[2]
     path = Path(torch, ss, cfg)
+    path.matcher = ss.match_mfma if args.matcher == "mfma" else ss.match
 
     if args.copy_calibration_mib:
         # fill the source, then a 1 GiB buffer that pushes it out of L2 and the
@@ -386,7 +445,7 @@ def main():
         "config": {"workload": f"5120-token target vs 5120-token cached reference, 32 Llama-3-8B-shaped attention "
                                f"layers (hidden 4096, 32q/8kv heads, head_dim 128), 128-bit LSH, recompute "
                                f"fraction {args.frac}", "n_tok": T, "layers": L, "recompute_frac": args.frac,
-                   "n_recompute": n_sel},
+                   "n_recompute": n_sel, "matcher": args.matcher},
         "partial_prefill_tokens_per_s": T / (pp_ms * 1e-3),
         "match_token_pairs_per_s": T * T / (match_ms * 1e-3),
         "stage_ms": {k: round(sum(v) / len(v), 4) for k, v in stages.items()},

@@ -95,6 +95,19 @@ semshare_status_t semshare_match(const uint64_t* tgt_codes, int64_t n_tgt,
                                  int32_t* idx, int32_t* dist, void* stream);
 
 /*
+ * The same match on the matrix cores (Sections 4.2 and 4.3; same contract,
+ * outputs bit-identical to semshare_match).  With the bits of a code read as
+ * +-1, the dot product of two codes of n_b bits is n_b - 2 * (Hamming
+ * distance), so the nearest code is the one with the largest dot product; the
+ * kernel computes those with int8 MFMAs over bits expanded to bytes and keeps
+ * the largest (lowest index on ties).  Arguments, limits and errors as
+ * semshare_match; the library allocates nothing.
+ */
+semshare_status_t semshare_match_mfma(const uint64_t* tgt_codes, int64_t n_tgt,
+                                      const uint64_t* ref_codes, int64_t n_ref, int32_t n_words,
+                                      int32_t* idx, int32_t* dist, void* stream);
+
+/*
  * KV rearrangement (Section 4.3; Section 4.3.2 for keeping K post-RoPE):
  * out[l][t] = ref[l][idx[t]] for every layer l, where a row is all kv heads
  * of one token (n_kv_heads * head_dim elements), copied bit for bit.  Keys

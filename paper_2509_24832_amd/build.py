@@ -37,7 +37,7 @@ COMMON_FLAGS = [
 # Per-source extra flags.  attention.hip: scores and probabilities are finite
 # or -inf by construction (masked keys), so NaN-preserving max is not needed;
 # without this every fmaxf operand is first quieted with an extra v_max.
-EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans"]}
+EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans"], "hamming_match_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def sources() -> List[str]:

@@ -81,18 +81,47 @@ semshare_status_t semshare_lsh_encode(const void* x, const void* planes, uint64_
                     "lsh_encode launch");
 }
 
+}  // extern "C"
+
+namespace {
+// The arguments both matchers take, checked alike; `ok_to_launch` is false
+// when there is nothing to do (or an error was recorded).
+semshare_status_t check_match(const char* who, const uint64_t* tgt_codes, int64_t n_tgt, const uint64_t* ref_codes,
+                              int64_t n_ref, int32_t n_words, const int32_t* idx, bool* ok_to_launch) {
+    *ok_to_launch = false;
+    if (n_tgt < 0) return fail(SEMSHARE_E_INVAL, "%s: n_tgt < 0", who);
+    if (n_words < 1 || n_words > 4) return fail(SEMSHARE_E_INVAL, "%s: n_words must be 1..4 (got %d)", who, n_words);
+    if (n_ref < 1) return fail(SEMSHARE_E_INVAL, "%s: n_ref must be >= 1", who);
+    if (n_ref >= (int64_t(1) << 23)) return fail(SEMSHARE_E_UNSUPPORTED, "%s: n_ref must be < 2^23", who);
+    if (n_tgt > (int64_t(1) << 31) - 1024) return fail(SEMSHARE_E_UNSUPPORTED, "%s: n_tgt too large", who);
+    if (n_tgt == 0) return ok();
+    if (!tgt_codes || !ref_codes || !idx) return fail(SEMSHARE_E_INVAL, "%s: null buffer", who);
+    *ok_to_launch = true;
+    return ok();
+}
+}  // namespace
+
+extern "C" {
+
 semshare_status_t semshare_match(const uint64_t* tgt_codes, int64_t n_tgt,
                                  const uint64_t* ref_codes, int64_t n_ref, int32_t n_words,
                                  int32_t* idx, int32_t* dist, void* stream) {
-    if (n_tgt < 0) return fail(SEMSHARE_E_INVAL, "match: n_tgt < 0");
-    if (n_words < 1 || n_words > 4) return fail(SEMSHARE_E_INVAL, "match: n_words must be 1..4 (got %d)", n_words);
-    if (n_ref < 1) return fail(SEMSHARE_E_INVAL, "match: n_ref must be >= 1");
-    if (n_ref >= (int64_t(1) << 23)) return fail(SEMSHARE_E_UNSUPPORTED, "match: n_ref must be < 2^23");
-    if (n_tgt > (int64_t(1) << 31) - 1024) return fail(SEMSHARE_E_UNSUPPORTED, "match: n_tgt too large");
-    if (n_tgt == 0) return ok();
-    if (!tgt_codes || !ref_codes || !idx) return fail(SEMSHARE_E_INVAL, "match: null buffer");
+    bool go;
+    const semshare_status_t st = check_match("match", tgt_codes, n_tgt, ref_codes, n_ref, n_words, idx, &go);
+    if (!go) return st;
     return from_hip(semshare::launch_match(tgt_codes, n_tgt, ref_codes, n_ref, n_words, idx, dist, (hipStream_t)stream),
                     "match launch");
+}
+
+semshare_status_t semshare_match_mfma(const uint64_t* tgt_codes, int64_t n_tgt,
+                                      const uint64_t* ref_codes, int64_t n_ref, int32_t n_words,
+                                      int32_t* idx, int32_t* dist, void* stream) {
+    bool go;
+    const semshare_status_t st = check_match("match_mfma", tgt_codes, n_tgt, ref_codes, n_ref, n_words, idx, &go);
+    if (!go) return st;
+    return from_hip(
+        semshare::launch_match_mfma(tgt_codes, n_tgt, ref_codes, n_ref, n_words, idx, dist, (hipStream_t)stream),
+        "match_mfma launch");
 }
 
 semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const int32_t* idx,

@@ -73,6 +73,9 @@ hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes,
 hipError_t launch_match(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
                         int32_t n_words, int32_t* idx, int32_t* dist, hipStream_t s);
 
+hipError_t launch_match_mfma(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
+                             int32_t n_words, int32_t* idx, int32_t* dist, hipStream_t s);
+
 hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_t* idx,
                               int64_t n_tgt, int64_t n_ref, void* dst_a, void* dst_b,
                               int32_t n_layers, int64_t row_bytes, hipStream_t s);

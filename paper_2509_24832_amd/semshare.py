@@ -54,6 +54,7 @@ def load() -> ctypes.CDLL:
         "semshare_rope_embed": (I32, [P, P, I64, I32, I64, F64, I32, P]),
         "semshare_lsh_encode": (I32, [P, P, P, I64, I32, I32, I32, P]),
         "semshare_match": (I32, [P, I64, P, I64, I32, P, P, P]),
+        "semshare_match_mfma": (I32, [P, I64, P, I64, I32, P, P, P]),
         "semshare_gather_kv": (I32, [P, P, P, I64, I64, P, P, I32, I32, I32, I32, P]),
         "semshare_partial_prefill": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, F32,
                                            P, P, P, SZ, I32, P]),
@@ -74,6 +75,9 @@ def load() -> ctypes.CDLL:
         "semshare_prefill_attention_planned": (I32, [P, SZ, P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ,
                                                      I32, P]),
     }
+    missing = set(declared_symbols()) - set(sig)
+    if missing:  # an entry without argtypes would pass pointers and int64 sizes as 32-bit ints
+        raise RuntimeError(f"no ctypes signature for {sorted(missing)}")
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
         fn.restype = res
@@ -155,9 +159,7 @@ def lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.Tensor
     return codes
 
 
-def match(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, idx: Optional[torch.Tensor] = None,
-          dist: Optional[torch.Tensor] = None, want_dist: bool = True) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
-    """Top-1 Hamming match of target codes against reference codes."""
+def _match(entry: str, tgt_codes, ref_codes, idx, dist, want_dist):
     _dev(tgt_codes, "tgt_codes", torch.int64)
     _dev(ref_codes, "ref_codes", torch.int64)
     if tgt_codes.dim() != 2 or ref_codes.dim() != 2 or tgt_codes.shape[1] != ref_codes.shape[1]:
@@ -170,9 +172,22 @@ def match(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, idx: Optional[torch.
         dist = torch.empty(n_tgt, dtype=torch.int32, device=tgt_codes.device)
     if dist is not None:
         _dev(dist, "dist", torch.int32)
-    _call("semshare_match", _ptr(tgt_codes), n_tgt, _ptr(ref_codes), ref_codes.shape[0], tgt_codes.shape[1],
+    _call(entry, _ptr(tgt_codes), n_tgt, _ptr(ref_codes), ref_codes.shape[0], tgt_codes.shape[1],
           _ptr(idx), _ptr(dist), _stream())
     return idx, dist
+
+
+def match(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, idx: Optional[torch.Tensor] = None,
+          dist: Optional[torch.Tensor] = None, want_dist: bool = True) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Top-1 Hamming match of target codes against reference codes."""
+    return _match("semshare_match", tgt_codes, ref_codes, idx, dist, want_dist)
+
+
+def match_mfma(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, idx: Optional[torch.Tensor] = None,
+               dist: Optional[torch.Tensor] = None,
+               want_dist: bool = True) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """The same match computed as +-1 dot products on the int8 matrix cores."""
+    return _match("semshare_match_mfma", tgt_codes, ref_codes, idx, dist, want_dist)
 
 
 def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Tensor,

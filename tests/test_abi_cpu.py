@@ -73,13 +73,14 @@ def test_lsh_validation(lib):
     assert _st("semshare_lsh_encode", None, None, None, 0, 64, 64, 1, None) == b.OK
 
 
-def test_match_validation(lib):
-    assert _st("semshare_match", FAKE, 4, FAKE, 4, 0, FAKE, None, None) == b.E_INVAL  # n_words
-    assert _st("semshare_match", FAKE, 4, FAKE, 4, 5, FAKE, None, None) == b.E_INVAL
-    assert _st("semshare_match", FAKE, 4, FAKE, 0, 2, FAKE, None, None) == b.E_INVAL  # empty reference
-    assert _st("semshare_match", FAKE, 4, FAKE, 1 << 23, 2, FAKE, None, None) == b.E_UNSUPPORTED
-    assert _st("semshare_match", FAKE, 4, FAKE, 4, 2, None, None, None) == b.E_INVAL  # null idx
-    assert _st("semshare_match", None, 0, None, 4, 2, None, None, None) == b.OK
+@pytest.mark.parametrize("entry", ["semshare_match", "semshare_match_mfma"])
+def test_match_validation(lib, entry):
+    assert _st(entry, FAKE, 4, FAKE, 4, 0, FAKE, None, None) == b.E_INVAL  # n_words
+    assert _st(entry, FAKE, 4, FAKE, 4, 5, FAKE, None, None) == b.E_INVAL
+    assert _st(entry, FAKE, 4, FAKE, 0, 2, FAKE, None, None) == b.E_INVAL  # empty reference
+    assert _st(entry, FAKE, 4, FAKE, 1 << 23, 2, FAKE, None, None) == b.E_UNSUPPORTED
+    assert _st(entry, FAKE, 4, FAKE, 4, 2, None, None, None) == b.E_INVAL  # null idx
+    assert _st(entry, None, 0, None, 4, 2, None, None, None) == b.OK
 
 
 def test_gather_validation(lib):

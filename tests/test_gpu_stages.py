@@ -90,6 +90,10 @@ def test_lsh_zero_rows_give_zero_codes():
 
 
 # --------------------------------------------------------------------- match
+# Both matchers (XOR/popcount and the int8 matrix-core variant) share one
+# contract and are held to the same bit-exact cases.
+MATCHERS = {"xor": lambda *a, **k: ss.match(*a, **k), "mfma": lambda *a, **k: ss.match_mfma(*a, **k)}
+
 
 @pytest.mark.parametrize("n_tgt,n_ref,n_words", [
     (512, 512, 1),
@@ -99,10 +103,12 @@ def test_lsh_zero_rows_give_zero_codes():
     (5, 70000, 4),        # many splits, tiny target
     (4096, 4096, 4),
     (300, 2048, 3),
+    (2000, 5000, 2),      # several splits with a ragged last block
 ])
-def test_match_matches_oracle(n_tgt, n_ref, n_words):
+@pytest.mark.parametrize("matcher", sorted(MATCHERS))
+def test_match_matches_oracle(n_tgt, n_ref, n_words, matcher):
     cfg = CONFIGS[1]
-    announce(f"match n_tgt={n_tgt} n_ref={n_ref} W={n_words}")
+    announce(f"match {matcher} n_tgt={n_tgt} n_ref={n_ref} W={n_words}")
     tgt = workloads.make_codes(cfg, n_tgt, n_words, tag=n_tgt)
     ref = workloads.make_codes(cfg, n_ref, n_words, tag=n_ref + 1)
     # plant exact and near matches plus duplicates so ties are exercised
@@ -110,41 +116,75 @@ def test_match_matches_oracle(n_tgt, n_ref, n_words):
     ref[:k] = tgt[:k]
     if n_ref > 2 * k + 1 and k:
         ref[k:2 * k] = tgt[:k]  # duplicates at higher indices: lowest index must win
-    idx, dist = ss.match(dev_codes(tgt), dev_codes(ref))
+    idx, dist = MATCHERS[matcher](dev_codes(tgt), dev_codes(ref))
     ri, rd = orc.match(tgt, ref)
     torch.cuda.synchronize()
     assert np.array_equal(idx.cpu().numpy(), ri)
     assert np.array_equal(dist.cpu().numpy(), rd)
 
 
-def test_match_bank_shape():
+@pytest.mark.parametrize("matcher", sorted(MATCHERS))
+def test_match_bank_shape(matcher):
     # one 4096-token target against 16 references of 4096 tokens (256-bit codes)
     cfg = CONFIGS[3]
-    announce("match bank 4096 x 65536 W=4")
+    announce(f"match {matcher} bank 4096 x 65536 W=4")
     tgt = workloads.make_codes(cfg, 4096, 4, tag=11)
     ref = workloads.make_codes(cfg, 16 * 4096, 4, tag=12)
     ref[5 * 4096 + np.arange(0, 4096, 7)] = tgt[np.arange(0, 4096, 7)]
-    idx, dist = ss.match(dev_codes(tgt), dev_codes(ref))
+    idx, dist = MATCHERS[matcher](dev_codes(tgt), dev_codes(ref))
     ri, rd = orc.match(tgt, ref)
     torch.cuda.synchronize()
     assert np.array_equal(idx.cpu().numpy(), ri) and np.array_equal(dist.cpu().numpy(), rd)
 
 
-def test_match_identical_prompts_self_match_and_no_dist():
+@pytest.mark.parametrize("matcher", sorted(MATCHERS))
+def test_match_identical_prompts_self_match_and_no_dist(matcher):
     cfg = CONFIGS[2]
     c = workloads.make_codes(cfg, 5120, 2, tag=3)
-    announce("match identical 5120")
-    idx, dist = ss.match(dev_codes(c), dev_codes(c), want_dist=False)
+    announce(f"match {matcher} identical 5120")
+    idx, dist = MATCHERS[matcher](dev_codes(c), dev_codes(c), want_dist=False)
     assert dist is None
     assert np.array_equal(idx.cpu().numpy(), np.arange(5120))
 
 
-def test_match_complement_distance():
+@pytest.mark.parametrize("matcher", sorted(MATCHERS))
+def test_match_complement_distance(matcher):
     cfg = CONFIGS[1]
     c = workloads.make_codes(cfg, 64, 2, tag=4)
-    announce("match complement")
-    idx, dist = ss.match(dev_codes(c[:1]), dev_codes(~c[:1]))
+    announce(f"match {matcher} complement")
+    idx, dist = MATCHERS[matcher](dev_codes(c[:1]), dev_codes(~c[:1]))
     assert dist.cpu().numpy()[0] == 128 and idx.cpu().numpy()[0] == 0
+
+
+@pytest.mark.parametrize("matcher", sorted(MATCHERS))
+@pytest.mark.parametrize("n_words", [1, 2, 4])
+def test_match_many_ties(matcher, n_words):
+    # references drawn from 6 distinct codes: every target's nearest distance
+    # is reached by hundreds of references, and the lowest index must win
+    cfg = CONFIGS[1]
+    announce(f"match {matcher} ties W={n_words}")
+    pool = workloads.make_codes(cfg, 6, n_words, tag=20 + n_words)
+    pick = np.random.default_rng(n_words).integers(0, 6, 3000)
+    ref = pool[pick]
+    tgt = workloads.make_codes(cfg, 700, n_words, tag=30 + n_words)
+    tgt[:6] = pool  # exact hits too
+    idx, dist = MATCHERS[matcher](dev_codes(tgt), dev_codes(ref))
+    ri, rd = orc.match(tgt, ref)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), ri) and np.array_equal(dist.cpu().numpy(), rd)
+
+
+@pytest.mark.parametrize("matcher", sorted(MATCHERS))
+def test_match_all_references_equal(matcher):
+    cfg = CONFIGS[1]
+    announce(f"match {matcher} all references equal")
+    one = workloads.make_codes(cfg, 1, 2, tag=40)
+    ref = np.repeat(one, 1500, axis=0)
+    tgt = workloads.make_codes(cfg, 257, 2, tag=41)
+    idx, dist = MATCHERS[matcher](dev_codes(tgt), dev_codes(ref))
+    _, rd = orc.match(tgt, ref)
+    torch.cuda.synchronize()
+    assert not idx.cpu().numpy().any() and np.array_equal(dist.cpu().numpy(), rd)
 
 
 # -------------------------------------------------------------------- gather
