@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--sweep", default="0.10,0.25,0.50", help="recompute fractions also timed ('' to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
+    ap.add_argument("--encode", choices=("fused", "two-pass"), default="fused",
+                    help="RoPE + LSH of the target in one kernel, or rope_embed then lsh_encode")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
     ap.add_argument("--match-compare", action="store_true",
@@ -79,6 +81,7 @@ class Path:
         import workloads
         self.torch, self.ss, self.cfg = torch, ss, cfg
         self.matcher = ss.match_mfma
+        self.fused_encode = True
         dev = "cuda"
         bf = torch.bfloat16
         T, d, L = cfg.n_tok, cfg.dim, cfg.n_layers
@@ -150,10 +153,14 @@ class Path:
         m = mark or (lambda name: None)
         hq, hkv = self.hq, self.hkv
         m("start")
-        ss.rope_embed(self.e_tgt, out=self.e_rot)
-        m("rope")
-        ss.lsh_encode(self.e_rot, self.planes, out=self.codes_t)
-        m("lsh")
+        if self.fused_encode:
+            ss.rope_lsh_encode(self.e_tgt, self.planes, out=self.codes_t)
+            m("rope_lsh")
+        else:
+            ss.rope_embed(self.e_tgt, out=self.e_rot)
+            m("rope")
+            ss.lsh_encode(self.e_rot, self.planes, out=self.codes_t)
+            m("lsh")
         self.matcher(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
         m("match")
         ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
@@ -384,6 +391,7 @@ def main():
     cfg = CONFIGS[2]
     path = Path(torch, ss, cfg)
     path.matcher = ss.match_mfma if args.matcher == "mfma" else ss.match
+    path.fused_encode = args.encode == "fused"
 
     if args.copy_calibration_mib:
         # fill the source, then a 1 GiB buffer that pushes it out of L2 and the
@@ -445,7 +453,7 @@ def main():
         "config": {"workload": f"5120-token target vs 5120-token cached reference, 32 Llama-3-8B-shaped attention "
                                f"layers (hidden 4096, 32q/8kv heads, head_dim 128), 128-bit LSH, recompute "
                                f"fraction {args.frac}", "n_tok": T, "layers": L, "recompute_frac": args.frac,
-                   "n_recompute": n_sel, "matcher": args.matcher},
+                   "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode},
         "partial_prefill_tokens_per_s": T / (pp_ms * 1e-3),
         "match_token_pairs_per_s": T * T / (match_ms * 1e-3),
         "stage_ms": {k: round(sum(v) / len(v), 4) for k, v in stages.items()},

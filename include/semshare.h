@@ -80,6 +80,23 @@ semshare_status_t semshare_lsh_encode(const void* x, const void* planes, uint64_
                                       semshare_dtype_t dtype, void* stream);
 
 /*
+ * RoPE and LSH in one pass (Section 4.3: the codes of the RoPE-embedded
+ * embeddings; Appendix A.1 Eq. (1) and A.2): the codes that
+ * semshare_rope_embed (row t at position pos0 + t, RoPE base `base`)
+ * followed by semshare_lsh_encode give, without writing the rotated rows
+ * to memory.  Each rotated pair is rounded to bf16 before the projection,
+ * as the stored rows would be.
+ *   x       [n_tok][dim] bf16, raw (not yet rotated) embeddings
+ *   planes  [n_bits][dim] bf16;   codes [n_tok][n_bits / 64] uint64 (output)
+ *   n_bits  64 or 128; 256 and fp32 return SEMSHARE_E_UNSUPPORTED.
+ *   dim: multiple of 64, <= 2^20.   pos0 >= 0, pos0 + n_tok <= 2^40.
+ *   Buffers 16-byte aligned.
+ */
+semshare_status_t semshare_rope_lsh_encode(const void* x, const void* planes, uint64_t* codes,
+                                          int64_t n_tok, int32_t dim, int32_t n_bits, int64_t pos0,
+                                          double base, semshare_dtype_t dtype, void* stream);
+
+/*
  * Fuzzy token matching (Sections 4.2 and 4.3): for every target token, the
  * reference token whose LSH code is nearest in Hamming distance; on equal
  * distance the lowest reference index wins, so the answer is unique.  A

@@ -81,6 +81,32 @@ semshare_status_t semshare_lsh_encode(const void* x, const void* planes, uint64_
                     "lsh_encode launch");
 }
 
+semshare_status_t semshare_rope_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok,
+                                          int32_t dim, int32_t n_bits, int64_t pos0, double base,
+                                          semshare_dtype_t dtype, void* stream) {
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: unknown dtype %d", dtype);
+    if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: n_tok < 0");
+    if (n_bits != 64 && n_bits != 128 && n_bits != 256)
+        return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: n_bits must be 64, 128 or 256 (got %d)", n_bits);
+    if (dim <= 0 || (dim & 1)) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: dim must be even and > 0 (got %d)", dim);
+    if (!(base > 0.0) || !std::isfinite(base)) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: base must be finite and > 0");
+    if (pos0 < 0) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: pos0 < 0");
+    if (pos0 + n_tok > (int64_t(1) << 40)) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: positions exceed 2^40");
+    if (dtype != SEMSHARE_BF16 || n_bits == 256)
+        return fail(SEMSHARE_E_UNSUPPORTED, "rope_lsh_encode: built for bf16 with 64 or 128 bits "
+                                            "(use rope_embed + lsh_encode otherwise)");
+    if (dim % 64) return fail(SEMSHARE_E_UNSUPPORTED, "rope_lsh_encode: needs dim %% 64 == 0 (got %d)", dim);
+    if (dim > (1 << 20)) return fail(SEMSHARE_E_UNSUPPORTED, "rope_lsh_encode: needs dim <= 2^20 (got %d)", dim);
+    if (n_tok > (int64_t(1) << 31) - 64) return fail(SEMSHARE_E_UNSUPPORTED, "rope_lsh_encode: n_tok too large");
+    if (n_tok == 0) return ok();
+    if (!x || !planes || !codes) return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: null buffer");
+    if (!aligned16(x) || !aligned16(planes) || !aligned16(codes))
+        return fail(SEMSHARE_E_INVAL, "rope_lsh_encode: buffers must be 16-byte aligned");
+    return from_hip(semshare::launch_rope_lsh_encode(x, planes, codes, n_tok, dim, n_bits, pos0, base,
+                                                     (hipStream_t)stream),
+                    "rope_lsh_encode launch");
+}
+
 }  // extern "C"
 
 namespace {

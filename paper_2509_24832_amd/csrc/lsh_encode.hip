@@ -23,6 +23,8 @@
 namespace semshare {
 namespace {
 
+constexpr int kCUs = 256;  // compute units of the chip
+
 // Loads 32 bf16 (64 B) starting at p into four 8-element MFMA operands.
 __device__ __forceinline__ void load_chunk(const uint16_t* p, bf16x8_t (&v)[4]) {
     const uint4* q = reinterpret_cast<const uint4*>(p);
@@ -117,10 +119,14 @@ __global__ __launch_bounds__(64 * NB) void lsh_encode_ring_kernel(const uint16_t
         }
     };
     const int nk = dim / 64;
-    // the ring always holds kStages - 1 chunks in flight; past the last chunk
+    // workgroups walk the K chunks from staggered starts, so that they do not
+    // all fetch the same hyperplane chunk (the same L2 channels) at once; the
+    // ring always holds kStages - 1 chunks in flight, and past the last chunk
     // the last one is fetched again into a stage nobody reads any more
+    const int k0 = (int)((blockIdx.x * 5u) % (unsigned)nk);
+    auto chunk_of = [&](int i) { const int c = k0 + (i < nk ? i : nk - 1); return c < nk ? c : c - nk; };
 #pragma unroll
-    for (int c = 0; c < C::kStages - 1; ++c) issue(c < nk ? c : nk - 1, c);
+    for (int c = 0; c < C::kStages - 1; ++c) issue(chunk_of(c), c);
 
     // read offsets: A rows l32, B rows 32 + 32 wave + l32; step s of a chunk
     // reads 16-byte chunk 4 half + s, at its swizzled place
@@ -134,8 +140,7 @@ __global__ __launch_bounds__(64 * NB) void lsh_encode_ring_kernel(const uint16_t
     for (int kt = 0; kt < nk; ++kt) {
         wait_vmcnt<(C::kStages - 2) * C::kLoadsPerWave>();  // chunk kt has landed
         ring_barrier();  // ... for every wave, and every wave is done with chunk kt - 1
-        const int nx = kt + C::kStages - 1;
-        issue(nx < nk ? nx : nk - 1, st == 0 ? C::kStages - 1 : st - 1);  // into chunk kt - 1's stage
+        issue(chunk_of(kt + C::kStages - 1), st == 0 ? C::kStages - 1 : st - 1);  // into chunk kt - 1's stage
         const uint32_t sb = smem_base + st * C::kStage;
         bf16x8_t a[4], b[4];
 #pragma unroll
@@ -158,6 +163,161 @@ __global__ __launch_bounds__(64 * NB) void lsh_encode_ring_kernel(const uint16_t
         const int64_t t_lo = row0 + r_lo, t_hi = t_lo + 4;
         if (lane == 0 && t_lo < n_tok) codes32[t_lo * words32 + wave] = (uint32_t)bits;
         if (lane == 1 && t_hi < n_tok) codes32[t_hi * words32 + wave] = (uint32_t)(bits >> 32);
+    }
+}
+
+// RoPE fused into the encode (Section 4.3: the codes are taken of the
+// RoPE-embedded rows): the same ring, but each workgroup owns R <= 32 rows
+// (R chosen so that the rows spread over every CU) and rotates the x rows of
+// a chunk in LDS once it has landed, one chunk ahead of the products.
+// The workgroup has twice the MFMA waves: the extra ones load nothing and
+// multiply nothing, they halve the rotation work of each wave and give every
+// SIMD a second wave.  Thread k rotates the pairs k, k + 128 NB, ... of the
+// chunk's R x 32 (even, odd) pairs; since 128 NB is a multiple of 32 its pair
+// column k % 32 is fixed, so its theta follows the chunks by one fp64 multiply (theta_{k+32}
+// = theta_k * base^(-64 / dim)).  The angle is reduced in fp64 revolutions
+// and rotated with the hardware sine and cosine; the rotated pair is rounded
+// to bf16, as the unfused path stores it.  The codes therefore equal those of
+// rope_embed + lsh_encode except where a projection lies within rounding
+// distance of zero.
+template <int NB>  // n_bits / 32 = MFMA waves (2 or 4); as many more waves only rotate
+__global__ __launch_bounds__(128 * NB) void rope_lsh_ring_kernel(const uint16_t* __restrict__ x,
+                                                                const uint16_t* __restrict__ planes,
+                                                                uint32_t* __restrict__ codes32, int64_t n_tok,
+                                                                int32_t dim, int32_t rows, int64_t pos0,
+                                                                double log2_base) {
+    using C = LshCfg<NB>;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[C::kStages * C::kStage];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = lane >> 5, l32 = lane & 31;
+    const int64_t row0 = (int64_t)blockIdx.x * rows;
+    const int64_t last = (row0 + rows < n_tok ? row0 + rows : n_tok) - 1 - row0;  // last live row of the tile
+    const uint32_t smem_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)smem;
+
+    const bool mma_wave = wave < NB;  // waves NB .. 2 NB - 1 load nothing and only rotate
+    // direct-load sources as in lsh_encode_ring_kernel; x rows past the
+    // tile's last live row repeat it (computed, never stored)
+    uint32_t off[C::kLoadsPerWave];
+    bool is_x[C::kLoadsPerWave];
+#pragma unroll
+    for (int j = 0; j < C::kLoadsPerWave; ++j) {
+        const int i = (mma_wave ? wave : 0) * C::kLoadsPerWave + j;
+        const int r = 8 * i + (lane >> 3);
+        const uint32_t chunk = (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+        is_x[j] = r < 32;
+        if (r < 32) {
+            const int64_t t = r < last ? r : last;
+            off[j] = (uint32_t)(t * dim + 8 * chunk) * 2u;
+        } else {
+            off[j] = (uint32_t)((r - 32) * dim + 8 * chunk) * 2u;
+        }
+    }
+    const uint16_t* xb = x + row0 * (int64_t)dim;
+    auto issue = [&](int kt, int st) {
+        if (!mma_wave) return;
+#pragma unroll
+        for (int j = 0; j < C::kLoadsPerWave; ++j) {
+            const int i = wave * C::kLoadsPerWave + j;
+            g2lds(is_x[j] ? (const void*)(xb + (int64_t)kt * 64) : (const void*)(planes + (int64_t)kt * 64), off[j],
+                  smem_base + st * C::kStage + i * 1024);
+        }
+    };
+    const int nk = dim / 64;
+    // staggered chunk order, as in lsh_encode_ring_kernel
+    const int k0 = (int)((blockIdx.x * 5u) % (unsigned)nk);
+    auto chunk_of = [&](int i) { const int c = k0 + (i < nk ? i : nk - 1); return c < nk ? c : c - nk; };
+#pragma unroll
+    for (int c = 0; c < C::kStages - 1; ++c) issue(chunk_of(c), c);
+
+    // this thread's pair column, its theta (in revolutions: theta / 2 pi) at
+    // chunk 0 and at the first chunk it rotates, and the step per chunk
+    const int kl = tid & 31;
+    const double theta_rev0 = exp2(-(2.0 * (double)kl / (double)dim) * log2_base) * 0.15915494309189535;
+    double theta_rev = exp2(-(2.0 * (double)(32 * k0 + kl) / (double)dim) * log2_base) * 0.15915494309189535;
+    const double theta_step = exp2(-(64.0 / (double)dim) * log2_base);
+    int rot_chunk = k0;
+    const int n_pairs = (int)(last + 1) * 32;
+    const uint32_t rot_col = (uint32_t)((kl & 3) * 4);
+    // rotates the live x rows of the chunk in stage `st_r` in place: the angle
+    // m theta in revolutions, reduced in fp64, then v_sin_f32 / v_cos_f32
+    // (which take revolutions)
+    auto rotate = [&](int st_r) {
+        // up to four pairs per thread (R <= 32 rows x 32 pairs over >= 256
+        // threads): all loads first, then four independent chains, then the
+        // stores, so one wave per SIMD still overlaps their latencies
+        const uint32_t sb = smem_base + st_r * C::kStage;
+        constexpr int kIt = 32 * 32 / (128 * NB);
+        uint32_t w[kIt];
+        __attribute__((address_space(3))) uint32_t* q[kIt];
+#pragma unroll
+        for (int i = 0; i < kIt; ++i) {
+            const int r = (tid + 128 * NB * i) >> 5;
+            const uint32_t addr = sb + (uint32_t)r * 128u + ((uint32_t)((kl >> 2) ^ ((r >> 1) & 7)) << 4) + rot_col;
+            q[i] = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)addr;
+            w[i] = tid + 128 * NB * i < n_pairs ? *q[i] : 0u;
+        }
+#pragma unroll
+        for (int i = 0; i < kIt; ++i) {
+            const int r = (tid + 128 * NB * i) >> 5;
+            const double tr = (double)(pos0 + row0 + r) * theta_rev;
+            const float rev = (float)(tr - floor(tr));
+            const float sn = __builtin_amdgcn_sinf(rev), cs = __builtin_amdgcn_cosf(rev);
+            const float x0 = bf16_lo(w[i]), x1 = bf16_hi(w[i]);
+            w[i] = pack_bf16x2(cs * x0 - sn * x1, sn * x0 + cs * x1);
+        }
+#pragma unroll
+        for (int i = 0; i < kIt; ++i)
+            if (tid + 128 * NB * i < n_pairs) *q[i] = w[i];
+        if (++rot_chunk == nk) {  // the order wraps to chunk 0
+            rot_chunk = 0;
+            theta_rev = theta_rev0;
+        } else {
+            theta_rev *= theta_step;
+        }
+    };
+
+    const uint32_t a_ro = l32 * 128, b_ro = (32 + 32 * wave + l32) * 128;
+    uint32_t koff[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) koff[s] = (uint32_t)(((4 * half + s) ^ ((l32 >> 1) & 7)) << 4);
+
+    // pipeline: chunk kt + 1 is rotated while chunk kt is multiplied; one
+    // barrier per chunk publishes the rotation and frees the oldest stage
+    wait_vmcnt<(C::kStages - 2) * C::kLoadsPerWave>();  // chunk 0 has landed
+    ring_barrier();
+    rotate(0);
+    f32x16_t acc = {};
+    int st = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_vmcnt<(C::kStages - 3) * C::kLoadsPerWave>();  // chunk kt + 1 has landed
+        ring_barrier();  // chunk kt rotated; every wave is done with chunk kt - 1
+        issue(chunk_of(kt + C::kStages - 1), st == 0 ? C::kStages - 1 : st - 1);
+        if (mma_wave) {
+            const uint32_t sb = smem_base + st * C::kStage;
+            bf16x8_t a[4], b[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                a[s] = *(lds_bf16x8_t*)(uintptr_t)(sb + a_ro + koff[s]);
+                b[s] = *(lds_bf16x8_t*)(uintptr_t)(sb + b_ro + koff[s]);
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], b[s], acc, 0, 0, 0);
+        }
+        st = st + 1 == C::kStages ? 0 : st + 1;
+        if (kt + 1 < nk) rotate(st);
+    }
+    wait_vmcnt<0>();
+    if (!mma_wave) return;
+
+    constexpr int words32 = NB;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const uint64_t bits = __ballot(acc[v] > 0.0f);
+        const int r_lo = 8 * (v / 4) + (v % 4);
+        if (lane == 0 && r_lo <= last) codes32[(row0 + r_lo) * words32 + wave] = (uint32_t)bits;
+        if (lane == 1 && r_lo + 4 <= last) codes32[(row0 + r_lo + 4) * words32 + wave] = (uint32_t)(bits >> 32);
     }
 }
 
@@ -231,6 +391,25 @@ __global__ __launch_bounds__(256) void lsh_encode_f32_kernel(const float* __rest
 }
 
 }  // namespace
+
+hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok, int32_t dim,
+                                  int32_t n_bits, int64_t pos0, double base, hipStream_t s) {
+    // rows per workgroup: enough workgroups for every CU (the rotation is
+    // per-row VALU work), at most the 32 rows of an MFMA tile
+    int64_t rows = (n_tok + kCUs - 1) / kCUs;
+    if (rows > 32) rows = 32;
+    if (rows < 1) rows = 1;
+    const dim3 grid((unsigned)((n_tok + rows - 1) / rows));
+    const auto* xp = static_cast<const uint16_t*>(x);
+    const auto* pp = static_cast<const uint16_t*>(planes);
+    auto* cp = reinterpret_cast<uint32_t*>(codes);
+    const double lb = log2(base);
+    if (n_bits == 64)
+        hipLaunchKernelGGL(rope_lsh_ring_kernel<2>, grid, dim3(256), 0, s, xp, pp, cp, n_tok, dim, (int32_t)rows, pos0, lb);
+    else
+        hipLaunchKernelGGL(rope_lsh_ring_kernel<4>, grid, dim3(512), 0, s, xp, pp, cp, n_tok, dim, (int32_t)rows, pos0, lb);
+    return hipGetLastError();
+}
 
 hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok,
                              int32_t dim, int32_t n_bits, int dtype, hipStream_t s) {

@@ -70,6 +70,9 @@ hipError_t launch_rope_embed(const void* x, void* y, int64_t n_tok, int32_t dim,
 hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok,
                              int32_t dim, int32_t n_bits, int dtype, hipStream_t s);
 
+hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok, int32_t dim,
+                                  int32_t n_bits, int64_t pos0, double base, hipStream_t s);
+
 hipError_t launch_match(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
                         int32_t n_words, int32_t* idx, int32_t* dist, hipStream_t s);
 

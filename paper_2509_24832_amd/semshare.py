@@ -53,6 +53,7 @@ def load() -> ctypes.CDLL:
         "semshare_version": (I32, []),
         "semshare_rope_embed": (I32, [P, P, I64, I32, I64, F64, I32, P]),
         "semshare_lsh_encode": (I32, [P, P, P, I64, I32, I32, I32, P]),
+        "semshare_rope_lsh_encode": (I32, [P, P, P, I64, I32, I32, I64, F64, I32, P]),
         "semshare_match": (I32, [P, I64, P, I64, I32, P, P, P]),
         "semshare_match_mfma": (I32, [P, I64, P, I64, I32, P, P, P]),
         "semshare_gather_kv": (I32, [P, P, P, I64, I64, P, P, I32, I32, I32, I32, P]),
@@ -156,6 +157,21 @@ def lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.Tensor
              if out is None else _dev(out, "out", torch.int64))
     _call("semshare_lsh_encode", _ptr(x), _ptr(planes), _ptr(codes), x.shape[0], x.shape[1], n_bits, _dt(x),
           _stream())
+    return codes
+
+
+def rope_lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.Tensor] = None, pos0: int = 0,
+                    base: float = 10000.0) -> torch.Tensor:
+    """LSH codes of the RoPE-embedded rows of x (row r at position pos0 + r), in one pass."""
+    _dev(x, "x")
+    _dev(planes, "planes", x.dtype)
+    if x.dim() != 2 or planes.dim() != 2 or planes.shape[1] != x.shape[1]:
+        raise ValueError("x [n_tok, dim] and planes [n_bits, dim] required")
+    n_bits = planes.shape[0]
+    codes = (torch.empty((x.shape[0], max(n_bits // 64, 1)), dtype=torch.int64, device=x.device)
+             if out is None else _dev(out, "out", torch.int64))
+    _call("semshare_rope_lsh_encode", _ptr(x), _ptr(planes), _ptr(codes), x.shape[0], x.shape[1], n_bits,
+          int(pos0), float(base), _dt(x), _stream())
     return codes
 
 

@@ -73,6 +73,20 @@ def test_lsh_validation(lib):
     assert _st("semshare_lsh_encode", None, None, None, 0, 64, 64, 1, None) == b.OK
 
 
+def test_rope_lsh_encode_validation(lib):
+    e = "semshare_rope_lsh_encode"
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4096, 128, 0, 10000.0, 0, None) == b.E_UNSUPPORTED  # fp32
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4096, 256, 0, 10000.0, 1, None) == b.E_UNSUPPORTED  # 256 bits
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4096, 96, 0, 10000.0, 1, None) == b.E_INVAL  # n_bits
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4095, 128, 0, 10000.0, 1, None) == b.E_INVAL  # odd dim
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4032 + 32, 128, 0, 10000.0, 1, None) == b.E_UNSUPPORTED  # dim % 64
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4096, 128, -1, 10000.0, 1, None) == b.E_INVAL  # pos0
+    assert _st(e, FAKE, FAKE, FAKE, 4, 4096, 128, 0, float("nan"), 1, None) == b.E_INVAL  # base
+    assert _st(e, FAKE, FAKE, None, 4, 4096, 128, 0, 10000.0, 1, None) == b.E_INVAL  # null codes
+    assert _st(e, FAKE_ODD, FAKE, FAKE, 4, 4096, 128, 0, 10000.0, 1, None) == b.E_INVAL  # alignment
+    assert _st(e, None, None, None, 0, 4096, 128, 0, 10000.0, 1, None) == b.OK
+
+
 @pytest.mark.parametrize("entry", ["semshare_match", "semshare_match_mfma"])
 def test_match_validation(lib, entry):
     assert _st(entry, FAKE, 4, FAKE, 4, 0, FAKE, None, None) == b.E_INVAL  # n_words

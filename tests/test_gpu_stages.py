@@ -81,6 +81,43 @@ def test_lsh_encode_matches_oracle(cid, n_tok, dim, n_bits):
     assert flips <= max(2, n_tok * n_bits // 20000)
 
 
+@pytest.mark.parametrize("n_tok,dim,n_bits,pos0", [
+    (1024, 4096, 128, 0),
+    (1000, 4096, 64, 0),      # ragged last tile
+    (777, 4096, 128, 100),    # positions from 100
+    (3000, 512, 128, 0),      # 12 rows per workgroup
+    (33, 128, 128, 32700),    # large angles
+    (5, 64, 64, 0),           # one row per workgroup, one K chunk
+    (256 * 33 + 7, 256, 128, 0),  # 33 rows wanted per workgroup: capped at 32
+])
+def test_rope_lsh_encode_matches_oracle(n_tok, dim, n_bits, pos0):
+    # the fused pass against the oracle's RoPE (rounded to bf16, as stored) then LSH
+    cfg = CONFIGS[1]
+    announce(f"rope+lsh n_tok={n_tok} dim={dim} n_bits={n_bits} pos0={pos0}")
+    x = workloads.make_rows(cfg, n_tok, dim, tag=7)
+    planes = workloads.make_planes(cfg, n_bits=n_bits, dim=dim)
+    codes = host_codes(ss.rope_lsh_encode(dev(x, "bf16"), dev(planes, "bf16"), pos0=pos0))
+    xr = orc.rope_embed(x, pos0=pos0, dtype="bf16").astype(np.float32)
+    ref = orc.lsh_encode(xr, planes)
+    proj = orc.lsh_project(xr, planes)
+    flips, outside = code_mismatch_ok(codes, ref, proj, xr.astype(np.float64), planes.astype(np.float64))
+    assert outside == 0, f"{flips} flips, {outside} outside the 1e-5 band"
+    assert flips <= max(2, n_tok * n_bits // 20000)
+
+
+def test_rope_lsh_encode_equals_two_pass_path():
+    # fused and unfused GPU paths on the 5120-token headline shape: codes agree
+    # except for projections inside the flip band
+    cfg = CONFIGS[2]
+    announce("rope+lsh vs rope_embed + lsh_encode 5120 x 4096")
+    x = dev(workloads.make_rows(cfg, 5120, 4096, tag=8), "bf16")
+    planes = dev(workloads.make_planes(cfg, n_bits=128, dim=4096), "bf16")
+    fused = host_codes(ss.rope_lsh_encode(x, planes))
+    two = host_codes(ss.lsh_encode(ss.rope_embed(x), planes))
+    diff = np.unpackbits((fused ^ two).view(np.uint8)).sum()
+    assert diff <= 5120 * 128 // 20000
+
+
 def test_lsh_zero_rows_give_zero_codes():
     cfg = CONFIGS[1]
     x = np.zeros((40, 128), np.float32)
