@@ -47,6 +47,8 @@ def parse():
                     help="RoPE + LSH of the target in one kernel, or rope_embed then lsh_encode")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
+    ap.add_argument("--dynamic-recompute", action="store_true",
+                    help="time the average attention score per token and the dynamic recompute set instead")
     ap.add_argument("--match-compare", action="store_true",
                     help="time the XOR/popcount and int8-MFMA matchers side by side instead of the hot path")
     ap.add_argument("--bank-similarity", action="store_true",
@@ -363,6 +365,55 @@ def match_compare_line(torch, np, ss, configs, args):
     print(json.dumps(out), flush=True)
 
 
+def dynamic_recompute_line(torch, np, ss, cfg, args):
+    """The dynamic recompute step on the headline shape (Section 3 Insight 2,
+    Section 4.3.3): average attention score per token of the fully computed
+    first layer (5120 tokens, 32 q / 8 kv heads, head_dim 128, bf16, seeded
+    synthetic q and K), then AR at 55%, hot / cold and the recompute set.
+    Bound: MFMA; the two passes over the causal score matrix do 2 x 2 D flops
+    per (head, query, key <= query) pair = 4 D H_q T (T + 1) / 2."""
+    import workloads
+    T, hq, hkv, D = 5120, 32, 8, 128
+    q = torch.from_numpy(workloads.make_rows(cfg, T, hq * D, tag=70)).to("cuda").to(torch.bfloat16).view(T, hq, D)
+    k = torch.from_numpy(workloads.make_rows(cfg, T, hkv * D, tag=71)).to("cuda").to(torch.bfloat16).view(T, hkv, D)
+    sigma = torch.from_numpy(np.random.default_rng(72).exponential(size=T).astype(np.float32)).cuda()
+    mass = torch.empty(T, dtype=torch.float32, device="cuda")
+    ws = torch.empty(int(ss.semshare.load().semshare_attention_mass_workspace(T, hq)), dtype=torch.uint8, device="cuda")
+    sel = torch.empty(T, dtype=torch.int32, device="cuda")
+    counts = torch.empty(3, dtype=torch.int32, device="cuda")
+
+    def run():
+        ss.attention_mass(q, k, hq, hkv, mass=mass, workspace=ws)
+        ss.dynamic_recompute(mass, sigma, sel_pos=sel, counts=counts)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    t_mass = t_sel = 0.0
+    for _ in range(args.steps):
+        ev[0].record()
+        ss.attention_mass(q, k, hq, hkv, mass=mass, workspace=ws)
+        ev[1].record()
+        ss.dynamic_recompute(mass, sigma, sel_pos=sel, counts=counts)
+        ev[2].record()
+        torch.cuda.synchronize()
+        t_mass += ev[0].elapsed_time(ev[1])
+        t_sel += ev[1].elapsed_time(ev[2])
+    us_mass, us_sel = t_mass / args.steps * 1e3, t_sel / args.steps * 1e3
+    flops = 4 * D * hq * T * (T + 1) / 2
+    c = counts.cpu().numpy().tolist()
+    out = {"metric": "dynamic_recompute_us", "value": us_mass + us_sel, "unit": "us", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "higher_is_better": False, "data": "synthetic", "dtype": "bf16",
+           "config": {"workload": "average attention score per token + AR 55% + hot/cold recompute set, 5120 tokens, "
+                                  "32q/8kv heads, head_dim 128"},
+           "attention_mass_us": round(us_mass, 2), "dynamic_select_us": round(us_sel, 2),
+           "AR": c[0], "n_recompute": c[1], "n_hot_recompute": c[2],
+           "roofline": {"kernel": "mass_lse_kernel + mass_col_kernel + mass_final_kernel", "bound": "mfma",
+                        "achieved": flops / (us_mass * 1e-6) / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": flops / (us_mass * 1e-6) / 1e12 / BF16_PEAK_TFLOPS}}
+    print(json.dumps(out), flush=True)
+
+
 def cfg_codes(np, cfg, n, w, tag):
     """Seeded synthetic code words (uniform bits), the generator of the configs."""
     import workloads
@@ -387,6 +438,9 @@ def main():
         return
     if args.match_compare:
         match_compare_line(torch, np, ss, CONFIGS, args)
+        return
+    if args.dynamic_recompute:
+        dynamic_recompute_line(torch, np, ss, CONFIGS[2], args)
         return
     cfg = CONFIGS[2]
     path = Path(torch, ss, cfg)

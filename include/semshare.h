@@ -308,6 +308,45 @@ semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, i
                                             int32_t* sel_pos, void* stream);
 
 /*
+ * Average attention score of every token at a fully computed layer (Section
+ * 3, Insight 2: the attention of each head averaged over the heads, then
+ * over the query rows): mass[j] = sum_h sum_{i >= j} P_h[i][j] / (n_q_heads
+ * n_tok), P_h the causal softmax of q_i . k_j * sm_scale (GQA: head h reads
+ * kv head h / (n_q_heads / n_kv_heads)).  The masses sum to 1.
+ *   q        [n_tok][n_q_heads][head_dim] bf16 (RoPE'd queries of every row)
+ *   k_cache  [n_tok][n_kv_heads][head_dim] bf16
+ *   mass     [n_tok] float32 (output)
+ *   sm_scale 0 => 1/sqrt(head_dim).   bf16 and head_dim 128 only, else
+ *   SEMSHARE_E_UNSUPPORTED.   workspace: semshare_attention_mass_workspace()
+ *   bytes, 4-byte aligned; q and k_cache 16-byte aligned.
+ */
+size_t semshare_attention_mass_workspace(int64_t n_tok, int32_t n_q_heads);
+semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int32_t n_q_heads,
+                                          int32_t n_kv_heads, int32_t head_dim, float sm_scale, float* mass,
+                                          void* workspace, size_t workspace_bytes, semshare_dtype_t dtype,
+                                          void* stream);
+
+/*
+ * Dynamic recompute set (Section 4.3.3 with the Attention Recovery equation
+ * of Section 3): the tokens sorted by mass (descending; the lower position
+ * first on ties); AR = the smallest count k >= 1 whose top-k mass reaches
+ * thres of the total (the paper uses 55%), compared in fp64 on sums taken in
+ * 2^-40 fixed point of the masses clamped to [0, 1]; those AR tokens are
+ * hot, the rest cold.  Recomputed are floor(w_hot AR + 1/2) hot and
+ * floor(w_cold (n_tok - AR) + 1/2) cold tokens (the paper: w_h = 0.5,
+ * w_c = 0.1), in each group those with the largest sigma (lower position
+ * first on ties), written to sel_pos in ascending position order.
+ *   mass, sigma  [n_tok] float32 (sigma >= 0, as deviation_out gives)
+ *   sel_pos      [n_tok] int32 (output; the first counts[1] are written)
+ *   counts       [3] int32 (output, device): AR, number selected, of them hot
+ *   n_tok <= 8192 (one workgroup), else SEMSHARE_E_UNSUPPORTED.
+ *   thres, w_hot, w_cold in [0, 1].
+ */
+semshare_status_t semshare_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres,
+                                             double w_hot, double w_cold, int32_t* sel_pos, int32_t* counts,
+                                             void* stream);
+
+/*
  * Reference retrieval over a bank of prompts (Appendix A.3 similarity
  * score; Section 5 applies reuse when it exceeds 0.8).  The bank holds
  * n_prompts reference prompts, prompt b being the codes

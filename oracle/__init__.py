@@ -248,3 +248,70 @@ def bank_similarity(tgt_codes, ref_codes, offsets, dmin: float = 0.0, dmax: floa
 def similarity(dist, dmin: float = 0.0, dmax: float = 30.0) -> float:
     d = np.ascontiguousarray(dist, dtype=np.int32)
     return float(_load().orc_similarity(_ptr(d), d.size, float(dmin), float(dmax)))
+
+
+def attention_mass(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, sm_scale: float = 0.0) -> np.ndarray:
+    """Average attention score of every token at a fully computed layer
+    (Section 3, Insight 2): the causal softmax attention of each head, averaged
+    over the heads and then over the query rows (the first dimension).  fp64;
+    one T x T score matrix per head (numpy matmul as the product step)."""
+    q = _f64(q).reshape(q.shape[0], n_q_heads, head_dim)
+    k = _f64(k_cache).reshape(k_cache.shape[0], n_kv_heads, head_dim)
+    T = q.shape[0]
+    scale = sm_scale if sm_scale else 1.0 / np.sqrt(head_dim)
+    G = n_q_heads // n_kv_heads
+    causal = np.tril(np.ones((T, T), dtype=bool))
+    total = np.zeros(T)
+    for h in range(n_q_heads):
+        s = (q[:, h, :] @ k[:, h // G, :].T) * scale
+        s = np.where(causal, s, -np.inf)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        total += p.sum(axis=0)
+    return total / (n_q_heads * T)
+
+
+def _mass_fixed(m32: np.ndarray) -> np.ndarray:
+    """Masses clamped to [0, 1] in 2^-40 fixed point (int64): sums of these are
+    exact, so the threshold decision does not depend on summation order."""
+    c = np.clip(m32.astype(np.float64), 0.0, 1.0)
+    return np.floor(c * 2.0 ** 40).astype(np.int64)
+
+
+def attention_recovery(mass, thres: float = 0.55) -> Tuple[int, np.ndarray]:
+    """Attention Recovery (Section 3, Insight 2 equation): the tokens ordered by
+    mass, largest first (lower position first on ties); AR is the smallest k >= 1
+    whose top-k mass reaches thres of the total (compared in fp64 on 2^-40
+    fixed-point sums).  Returns (AR, order)."""
+    m32 = np.asarray(mass, dtype=np.float32)
+    n = m32.shape[0]
+    if n == 0:
+        return 0, np.zeros(0, dtype=np.int64)
+    key = np.clip(m32, np.float32(0), np.float32(1))
+    order = np.array(sorted(range(n), key=lambda j: (-float(key[j]), j)), dtype=np.int64)
+    fx = _mass_fixed(m32)
+    total = int(fx.sum())
+    target = thres * float(total)
+    run = 0
+    for k, j in enumerate(order, start=1):
+        run += int(fx[j])
+        if float(run) >= target:
+            return k, order
+    return n, order
+
+
+def dynamic_recompute(mass, sigma, thres: float = 0.55, w_hot: float = 0.5,
+                      w_cold: float = 0.1) -> Tuple[int, np.ndarray, int]:
+    """Dynamic recompute set (Section 4.3.3): the AR first tokens by mass are
+    hot, the rest cold; floor(w_hot AR + 1/2) hot and floor(w_cold (T - AR) + 1/2)
+    cold tokens with the largest deviation (lower position first on ties) are
+    recomputed.  Returns (AR, selected positions ascending, hot count chosen)."""
+    ar, order = attention_recovery(mass, thres)
+    n = len(order)
+    sig = np.maximum(np.asarray(sigma, dtype=np.float32), np.float32(0))
+    hot = set(int(j) for j in order[:ar])
+    n_hot = int(np.floor(w_hot * ar + 0.5))
+    n_cold = int(np.floor(w_cold * (n - ar) + 0.5))
+    by_sigma = lambda js: sorted(js, key=lambda j: (-float(sig[j]), j))
+    chosen = by_sigma([j for j in range(n) if j in hot])[:n_hot] + by_sigma([j for j in range(n) if j not in hot])[:n_cold]
+    return ar, np.array(sorted(chosen), dtype=np.int64), n_hot

@@ -107,6 +107,53 @@ semshare_status_t semshare_rope_lsh_encode(const void* x, const void* planes, ui
                     "rope_lsh_encode launch");
 }
 
+size_t semshare_attention_mass_workspace(int64_t n_tok, int32_t n_q_heads) {
+    if (n_tok < 0 || n_q_heads <= 0) return 0;
+    return semshare::attention_mass_workspace(n_tok, n_q_heads);
+}
+
+semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int32_t n_q_heads,
+                                          int32_t n_kv_heads, int32_t head_dim, float sm_scale, float* mass,
+                                          void* workspace, size_t workspace_bytes, semshare_dtype_t dtype,
+                                          void* stream) {
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "attention_mass: unknown dtype %d", dtype);
+    if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "attention_mass: n_tok < 0");
+    if (n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads)
+        return fail(SEMSHARE_E_INVAL, "attention_mass: n_q_heads must be a positive multiple of n_kv_heads");
+    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "attention_mass: sm_scale must be finite and >= 0");
+    if (dtype != SEMSHARE_BF16 || head_dim != 128)
+        return fail(SEMSHARE_E_UNSUPPORTED, "attention_mass: built for bf16 with head_dim 128");
+    if (n_tok > (int64_t(1) << 24) || (int64_t)n_q_heads * n_tok > (int64_t(1) << 31))
+        return fail(SEMSHARE_E_UNSUPPORTED, "attention_mass: too many tokens");
+    if (n_tok == 0) return ok();
+    if (!q || !k_cache || !mass || !workspace) return fail(SEMSHARE_E_INVAL, "attention_mass: null buffer");
+    if (!aligned16(q) || !aligned16(k_cache) || reinterpret_cast<uintptr_t>(workspace) % 4 ||
+        reinterpret_cast<uintptr_t>(mass) % 4)
+        return fail(SEMSHARE_E_INVAL, "attention_mass: q and k_cache must be 16-byte aligned, mass and workspace 4-byte");
+    if (workspace_bytes < semshare::attention_mass_workspace(n_tok, n_q_heads))
+        return fail(SEMSHARE_E_INVAL, "attention_mass: workspace too small (%zu < %zu)", workspace_bytes,
+                    semshare::attention_mass_workspace(n_tok, n_q_heads));
+    const float scale = sm_scale == 0.0f ? 1.0f / sqrtf((float)head_dim) : sm_scale;
+    return from_hip(semshare::launch_attention_mass(q, k_cache, n_tok, n_q_heads, n_kv_heads, scale, mass, workspace,
+                                                    (hipStream_t)stream),
+                    "attention_mass launch");
+}
+
+semshare_status_t semshare_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres,
+                                             double w_hot, double w_cold, int32_t* sel_pos, int32_t* counts,
+                                             void* stream) {
+    if (n_tok < 0 || n_tok > semshare::kMaxDynTok)
+        return fail(n_tok < 0 ? SEMSHARE_E_INVAL : SEMSHARE_E_UNSUPPORTED, "dynamic_recompute: n_tok must be in [0, %d]",
+                    semshare::kMaxDynTok);
+    if (!(thres >= 0.0 && thres <= 1.0) || !(w_hot >= 0.0 && w_hot <= 1.0) || !(w_cold >= 0.0 && w_cold <= 1.0))
+        return fail(SEMSHARE_E_INVAL, "dynamic_recompute: thres, w_hot and w_cold must lie in [0, 1]");
+    if (!counts || (n_tok > 0 && (!mass || !sigma || !sel_pos)))
+        return fail(SEMSHARE_E_INVAL, "dynamic_recompute: null buffer");
+    return from_hip(semshare::launch_dynamic_recompute(mass, sigma, n_tok, thres, w_hot, w_cold, sel_pos, counts,
+                                                       (hipStream_t)stream),
+                    "dynamic_recompute launch");
+}
+
 }  // extern "C"
 
 namespace {

@@ -1,0 +1,330 @@
+// Average attention score per token and the dynamic recompute set (Section 3
+// Insight 2 and its Attention Recovery equation; Section 4.3.3: hot / cold
+// tokens from AR at a 55% threshold, Recomputed = w_c * c + w_h * h).
+//
+// Mass of token j at a fully computed layer: the causal softmax attention
+// P_h[i][j] of every head h, averaged over the heads and over the query rows
+// i (rows before j contribute zero).  Two MFMA passes over the causal score
+// matrix, bf16 operands and fp32 accumulation, exponentials in base 2:
+//   mass_lse_kernel  one wave per (4 query blocks of 32, head): S^T = K Q^T,
+//                    so each lane owns a query column and keeps its row's
+//                    running max and sum over its 16 keys per block; the
+//                    two lane halves merge at the end -> lse2[h][i].
+//   mass_col_kernel  one wave per (4 key blocks of 32, head): S = Q K^T, so
+//                    each lane owns a key column and sums exp2(s - lse2[i])
+//                    over its 16 rows per block -> part[h][j].
+//   mass_final_kernel sums the heads in a fixed order and divides by H_q T.
+// Each wave keeps the operands of its 4 fixed blocks (queries, resp. keys)
+// in VGPRs and streams the other operand from global memory, one 32 x 128
+// tile feeding 4 x 8 MFMAs.
+//
+// dyn_select_kernel (one workgroup): tokens sorted by mass (descending, lower
+// position first on ties); AR is the smallest count whose prefix reaches
+// thres of the total, the sums taken in 2^-40 fixed point so that the
+// integer decision does not depend on the summation order; the AR first
+// tokens are hot.  Then round(w_h AR) hot and round(w_c (T - AR)) cold tokens
+// with the largest deviation sigma (lower position first on ties) form the
+// recompute set, written in ascending position order.
+#include "semshare_internal.h"
+
+namespace semshare {
+namespace {
+
+constexpr int kNB = 4;  // fixed 32-blocks per wave
+constexpr float kNegInf = -__builtin_inff();
+
+__device__ __forceinline__ bf16x8_t ld8(const uint16_t* p) {
+    return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
+}
+
+// lane -> row of the 32 x 32 MFMA output held in accumulator v
+__device__ __forceinline__ int out_row(int v, int half) { return 8 * (v >> 2) + 4 * half + (v & 3); }
+
+__global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                                                       int64_t T, int32_t Hq, int32_t Hkv, float scale_log2e,
+                                                       float* __restrict__ lse2) {
+    const int lane = threadIdx.x, half = lane >> 5, l32 = lane & 31;
+    const int h = blockIdx.y, kvh = h / (Hq / Hkv);
+    const int64_t nb = (T + 31) / 32;
+    const int64_t qb0 = (int64_t)blockIdx.x * kNB;
+    bf16x8_t bq[kNB][8];
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+        int64_t qi = (qb0 + b) * 32 + l32;
+        if (qi >= T) qi = T - 1;
+        const uint16_t* row = q + (qi * Hq + h) * 128 + 8 * half;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) bq[b][ks] = ld8(row + 16 * ks);
+    }
+    float m[kNB], l[kNB];
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) { m[b] = kNegInf; l[b] = 0.0f; }
+    const int64_t kb_end = qb0 + kNB < nb ? qb0 + kNB : nb;
+    for (int64_t kb = 0; kb < kb_end; ++kb) {
+        int64_t kj = kb * 32 + l32;
+        if (kj >= T) kj = T - 1;
+        const uint16_t* krow = k + (kj * Hkv + kvh) * 128 + 8 * half;
+        bf16x8_t ak[8];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) ak[ks] = ld8(krow + 16 * ks);
+#pragma unroll
+        for (int b = 0; b < kNB; ++b) {
+            if (kb > qb0 + b) continue;  // wave-uniform: the block lies above the diagonal
+            f32x16_t acc = {};
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], acc, 0, 0, 0);
+            // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32]
+            const int64_t qi = (qb0 + b) * 32 + l32;
+            float t[16], bm = kNegInf;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t key = kb * 32 + out_row(v, half);
+                t[v] = key <= qi ? acc[v] * scale_log2e : kNegInf;
+                bm = fmaxf(bm, t[v]);
+            }
+            const float mn = fmaxf(m[b], bm);
+            if (mn == kNegInf) continue;  // no key of this half seen yet
+            float sum = 0.0f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sum += exp2f(t[v] - mn);
+            l[b] = l[b] * exp2f(m[b] - mn) + sum;
+            m[b] = mn;
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+        const float om = __shfl_xor(m[b], 32), ol = __shfl_xor(l[b], 32);
+        const float M = fmaxf(m[b], om);
+        const float L = (m[b] == kNegInf ? 0.0f : l[b] * exp2f(m[b] - M)) + (om == kNegInf ? 0.0f : ol * exp2f(om - M));
+        const int64_t qi = (qb0 + b) * 32 + l32;
+        if (half == 0 && qi < T) lse2[(int64_t)h * T + qi] = M + log2f(L);
+    }
+}
+
+__global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                                                       int64_t T, int32_t Hq, int32_t Hkv, float scale_log2e,
+                                                       const float* __restrict__ lse2, float* __restrict__ part) {
+    const int lane = threadIdx.x, half = lane >> 5, l32 = lane & 31;
+    const int h = blockIdx.y, kvh = h / (Hq / Hkv);
+    const int64_t nb = (T + 31) / 32;
+    const int64_t kb0 = (int64_t)blockIdx.x * kNB;
+    bf16x8_t bk[kNB][8];
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+        int64_t kj = (kb0 + b) * 32 + l32;
+        if (kj >= T) kj = T - 1;
+        const uint16_t* row = k + (kj * Hkv + kvh) * 128 + 8 * half;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) bk[b][ks] = ld8(row + 16 * ks);
+    }
+    float col[kNB];
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) col[b] = 0.0f;
+    const float* lse_h = lse2 + (int64_t)h * T;
+    for (int64_t qb = kb0; qb < nb; ++qb) {
+        int64_t qi = qb * 32 + l32;
+        if (qi >= T) qi = T - 1;
+        const uint16_t* qrow = q + (qi * Hq + h) * 128 + 8 * half;
+        bf16x8_t aq[8];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) aq[ks] = ld8(qrow + 16 * ks);
+        float L[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int64_t r = qb * 32 + out_row(v, half);
+            L[v] = r < T ? lse_h[r] : __builtin_inff();
+        }
+#pragma unroll
+        for (int b = 0; b < kNB; ++b) {
+            if (qb < kb0 + b) continue;  // wave-uniform: every row of the block precedes the keys
+            f32x16_t acc = {};
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[ks], bk[b][ks], acc, 0, 0, 0);
+            // acc[v] = S[query = 32 qb + out_row(v)][key = 32 (kb0 + b) + l32]
+            const int64_t key = (kb0 + b) * 32 + l32;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t r = qb * 32 + out_row(v, half);
+                col[b] += key <= r ? exp2f(acc[v] * scale_log2e - L[v]) : 0.0f;  // rows past T: L = inf -> 0
+            }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+        const float c = col[b] + __shfl_xor(col[b], 32);
+        const int64_t key = (kb0 + b) * 32 + l32;
+        if (half == 0 && key < T) part[(int64_t)h * T + key] = c;
+    }
+}
+
+__global__ void mass_final_kernel(const float* __restrict__ part, int64_t T, int32_t Hq, float* __restrict__ mass) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= T) return;
+    float s = 0.0f;
+    for (int h = 0; h < Hq; ++h) s += part[(int64_t)h * T + j];
+    mass[j] = s / ((float)Hq * (float)T);
+}
+
+// ------------------------------------------------------------ selection
+constexpr int kSelThreads = 1024;
+
+__device__ __forceinline__ void bitonic_sort(uint64_t* key, int n2) {
+    for (int size = 2; size <= n2; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int t = threadIdx.x; t < n2 / 2; t += kSelThreads) {
+                const int i = 2 * t - (t & (stride - 1));  // lower element of the pair
+                const int j = i + stride;
+                const bool up = (i & size) == 0;
+                const uint64_t a = key[i], b = key[j];
+                if ((a > b) == up) { key[i] = b; key[j] = a; }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// exclusive block scan of one int64 per thread; returns the total too
+__device__ __forceinline__ int64_t block_scan_i64(int64_t v, int64_t* tot, int64_t* sw) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int64_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(x, d);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) sw[w] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t run = 0;
+        for (int i = 0; i < kSelThreads / 64; ++i) { const int64_t c = sw[i]; sw[i] = run; run += c; }
+        sw[kSelThreads / 64] = run;
+    }
+    __syncthreads();
+    const int64_t ex = sw[w] + x - v;
+    *tot = sw[kSelThreads / 64];
+    __syncthreads();
+    return ex;
+}
+
+__device__ __forceinline__ float clamp01(float m) { return m > 0.0f ? (m < 1.0f ? m : 1.0f) : 0.0f; }
+
+__global__ __launch_bounds__(kSelThreads) void dyn_select_kernel(const float* __restrict__ mass,
+                                                                  const float* __restrict__ sigma, int32_t n,
+                                                                  double thres, double w_hot, double w_cold,
+                                                                  int32_t* __restrict__ sel_pos,
+                                                                  int32_t* __restrict__ counts) {
+    __shared__ uint64_t key[kMaxDynTok];
+    __shared__ uint8_t hot[kMaxDynTok];
+    __shared__ int64_t sw[kSelThreads / 64 + 1];
+    __shared__ int s_ar;
+    int n2 = 1;
+    while (n2 < n) n2 <<= 1;
+    // 1. mass descending, lower position first
+    for (int i = threadIdx.x; i < n2; i += kSelThreads) {
+        if (i < n) {
+            const uint32_t mb = __float_as_uint(clamp01(mass[i]));
+            key[i] = ((uint64_t)(0xFFFFFFFFu - mb) << 32) | (uint32_t)i;
+        } else {
+            key[i] = ~0ull;
+        }
+    }
+    if (threadIdx.x == 0) s_ar = n;
+    __syncthreads();
+    bitonic_sort(key, n2);
+    // 2. AR: first count whose fixed-point prefix reaches thres * total
+    constexpr int kPer = kMaxDynTok / kSelThreads;
+    const int base = threadIdx.x * kPer;
+    int64_t fx[kPer];
+    int64_t local = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const int i = base + e;
+        fx[e] = 0;
+        if (i < n) {
+            const int pos = (int)(key[i] & 0xFFFFFFFFu);
+            fx[e] = (int64_t)floor((double)clamp01(mass[pos]) * 1099511627776.0);  // 2^40
+        }
+        local += fx[e];
+    }
+    int64_t total;
+    int64_t run = block_scan_i64(local, &total, sw);
+    const double target = thres * (double)total;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const int i = base + e;
+        run += fx[e];
+        if (i < n && (double)run >= target) {
+            atomicMin(&s_ar, i + 1);
+            break;
+        }
+    }
+    __syncthreads();
+    const int ar = n > 0 ? s_ar : 0;
+    for (int i = threadIdx.x; i < n; i += kSelThreads) hot[(int)(key[i] & 0xFFFFFFFFu)] = i < ar ? 1 : 0;
+    __syncthreads();
+    const int n_hot = (int)floor(w_hot * (double)ar + 0.5);
+    const int n_cold = (int)floor(w_cold * (double)(n - ar) + 0.5);
+    // 3. hot group first, then cold; sigma descending, lower position first
+    for (int i = threadIdx.x; i < n2; i += kSelThreads) {
+        if (i < n) {
+            const uint32_t sb = __float_as_uint(sigma[i] > 0.0f ? sigma[i] : 0.0f) & 0x7FFFFFFFu;
+            key[i] = ((uint64_t)(hot[i] ? 0u : 1u) << 62) | ((uint64_t)(0x7FFFFFFFu - sb) << 20) | (uint32_t)i;
+        } else {
+            key[i] = ~0ull;
+        }
+    }
+    __syncthreads();
+    bitonic_sort(key, n2);
+    // hot occupies sorted [0, ar), cold [ar, n): mark the chosen positions
+    for (int i = threadIdx.x; i < n; i += kSelThreads) {
+        const int pos = (int)(key[i] & 0xFFFFFu);
+        const bool take = i < ar ? i < n_hot : i - ar < n_cold;
+        hot[pos] = take ? 1 : 0;  // reused: selected flag by position
+    }
+    __syncthreads();
+    // 4. compaction in position order
+    int64_t cnt = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) cnt += (base + e < n && hot[base + e]) ? 1 : 0;
+    int64_t tot2;
+    int64_t o = block_scan_i64(cnt, &tot2, sw);
+#pragma unroll
+    for (int e = 0; e < kPer; ++e)
+        if (base + e < n && hot[base + e]) sel_pos[o++] = base + e;
+    if (threadIdx.x == 0) {
+        counts[0] = ar;
+        counts[1] = (int32_t)tot2;
+        counts[2] = n_hot;
+    }
+}
+
+}  // namespace
+
+size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads) {
+    return (size_t)2 * (size_t)n_q_heads * (size_t)n_tok * sizeof(float);
+}
+
+hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                                 float sm_scale, float* mass, void* workspace, hipStream_t s) {
+    float* lse2 = static_cast<float*>(workspace);
+    float* part = lse2 + (int64_t)n_q_heads * n_tok;
+    const float sl2e = sm_scale * 1.4426950408889634f;
+    const int64_t nb = (n_tok + 31) / 32;
+    const dim3 grid((unsigned)((nb + kNB - 1) / kNB), (unsigned)n_q_heads);
+    const auto* qp = static_cast<const uint16_t*>(q);
+    const auto* kp = static_cast<const uint16_t*>(k);
+    hipLaunchKernelGGL(mass_lse_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2);
+    hipLaunchKernelGGL(mass_col_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2, part);
+    hipLaunchKernelGGL(mass_final_kernel, dim3((unsigned)((n_tok + 255) / 256)), dim3(256), 0, s, part, n_tok,
+                       n_q_heads, mass);
+    return hipGetLastError();
+}
+
+hipError_t launch_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres, double w_hot,
+                                    double w_cold, int32_t* sel_pos, int32_t* counts, hipStream_t s) {
+    hipLaunchKernelGGL(dyn_select_kernel, dim3(1), dim3(kSelThreads), 0, s, mass, sigma, n_tok, thres, w_hot, w_cold,
+                       sel_pos, counts);
+    return hipGetLastError();
+}
+
+}  // namespace semshare

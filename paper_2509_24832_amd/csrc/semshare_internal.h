@@ -73,6 +73,15 @@ hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes,
 hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok, int32_t dim,
                                   int32_t n_bits, int64_t pos0, double base, hipStream_t s);
 
+// token count limit of the dynamic recompute selection (one workgroup, keys in LDS)
+constexpr int kMaxDynTok = 8192;
+
+size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads);
+hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
+                                 float sm_scale, float* mass, void* workspace, hipStream_t s);
+hipError_t launch_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres, double w_hot,
+                                    double w_cold, int32_t* sel_pos, int32_t* counts, hipStream_t s);
+
 hipError_t launch_match(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,
                         int32_t n_words, int32_t* idx, int32_t* dist, hipStream_t s);
 

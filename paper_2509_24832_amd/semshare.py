@@ -61,6 +61,9 @@ def load() -> ctypes.CDLL:
                                            P, P, P, SZ, I32, P]),
         "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
         "semshare_select_recompute": (I32, [P, I64, I64, P, P]),
+        "semshare_attention_mass_workspace": (SZ, [I64, I32]),
+        "semshare_attention_mass": (I32, [P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
+        "semshare_dynamic_recompute": (I32, [P, P, I32, F64, F64, F64, P, P, P]),
         "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
@@ -173,6 +176,41 @@ def rope_lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.T
     _call("semshare_rope_lsh_encode", _ptr(x), _ptr(planes), _ptr(codes), x.shape[0], x.shape[1], n_bits,
           int(pos0), float(base), _dt(x), _stream())
     return codes
+
+
+def attention_mass(q: torch.Tensor, k_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int, sm_scale: float = 0.0,
+                   mass: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Average attention score per token: q [T, Hq, D], k_cache [T, Hkv, D] -> mass [T] float32."""
+    _dev(q, "q")
+    _dev(k_cache, "k_cache", q.dtype)
+    T = q.shape[0]
+    d = q.shape[-1]
+    if mass is None:
+        mass = torch.empty(T, dtype=torch.float32, device=q.device)
+    _dev(mass, "mass", torch.float32)
+    need = int(load().semshare_attention_mass_workspace(T, n_q_heads))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _call("semshare_attention_mass", _ptr(q), _ptr(k_cache), T, n_q_heads, n_kv_heads, d, float(sm_scale), _ptr(mass),
+          _ptr(workspace), workspace.numel() * workspace.element_size(), _dt(q), _stream())
+    return mass
+
+
+def dynamic_recompute(mass: torch.Tensor, sigma: torch.Tensor, thres: float = 0.55, w_hot: float = 0.5,
+                      w_cold: float = 0.1, sel_pos: Optional[torch.Tensor] = None,
+                      counts: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Hot tokens by Attention Recovery and the recompute set: returns (sel_pos [T] int32 with the first
+    counts[1] valid, counts [3] int32 = AR, number selected, hot among them), both on the device."""
+    _dev(mass, "mass", torch.float32)
+    _dev(sigma, "sigma", torch.float32)
+    T = mass.shape[0]
+    if sel_pos is None:
+        sel_pos = torch.empty(max(T, 1), dtype=torch.int32, device=mass.device)
+    if counts is None:
+        counts = torch.empty(3, dtype=torch.int32, device=mass.device)
+    _call("semshare_dynamic_recompute", _ptr(mass), _ptr(sigma), T, float(thres), float(w_hot), float(w_cold),
+          _ptr(sel_pos), _ptr(counts), _stream())
+    return sel_pos, counts
 
 
 def _match(entry: str, tgt_codes, ref_codes, idx, dist, want_dist):

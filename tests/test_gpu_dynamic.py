@@ -1,0 +1,89 @@
+"""GPU parity of the average attention score per token and of the dynamic
+recompute set against the oracle (Section 3 Insight 2, Section 4.3.3)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import paper_2509_24832_amd as ss
+import workloads
+from workloads import CONFIGS
+
+from helpers import announce, dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+def _qk(cfg, T, hq, hkv, tag):
+    q = orc.round_to(workloads.make_rows(cfg, T, hq * 128, tag=tag), "bf16").astype(np.float32)
+    k = orc.round_to(workloads.make_rows(cfg, T, hkv * 128, tag=tag + 1), "bf16").astype(np.float32)
+    return q.reshape(T, hq, 128), k.reshape(T, hkv, 128)
+
+
+@pytest.mark.parametrize("T,hq,hkv", [(64, 4, 4), (300, 32, 8), (1024, 32, 8), (33, 8, 2)])
+def test_attention_mass_matches_oracle(T, hq, hkv):
+    cfg = CONFIGS[1]
+    announce(f"attention mass T={T} hq={hq} hkv={hkv}")
+    q, k = _qk(cfg, T, hq, hkv, tag=50 + T)
+    m = host(ss.attention_mass(dev(q, "bf16"), dev(k, "bf16"), hq, hkv))
+    ref = orc.attention_mass(q, k, hq, hkv, 128)
+    # fp32 scores of exact bf16 products, exp2 within a few ulp, fp32 sums over <= T rows
+    assert np.allclose(m, ref, rtol=1e-4, atol=1e-8), np.abs(m - ref).max()
+    assert abs(m.astype(np.float64).sum() - 1.0) < 1e-4
+
+
+def test_attention_mass_headline_shape_properties():
+    # 5120 tokens, 32 / 8 heads: the masses sum to 1, and with q = 0 every row is
+    # uniform over its keys, so mass_j = (H_T - H_j) / T exactly in exact arithmetic
+    T, hq, hkv = 5120, 32, 8
+    cfg = CONFIGS[2]
+    announce("attention mass 5120 x 32/8")
+    q, k = _qk(cfg, T, hq, hkv, tag=60)
+    m = host(ss.attention_mass(dev(q, "bf16"), dev(k, "bf16"), hq, hkv)).astype(np.float64)
+    assert abs(m.sum() - 1.0) < 1e-3 and (m > 0).all()
+    mz = host(ss.attention_mass(torch.zeros(T, hq, 128, dtype=torch.bfloat16, device="cuda"), dev(k, "bf16"),
+                                hq, hkv)).astype(np.float64)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, T + 1))])
+    assert np.allclose(mz, (H[T] - H[:T]) / T, rtol=2e-4, atol=0)
+    # sampled keys against the oracle's definition, one key at a time: the
+    # oracle's full T x T pass is too slow here, so check a leading block
+    small = 512
+    ref = orc.attention_mass(q[:small], k[:small], hq, hkv, 128) * small / T
+    # the first 512 rows' share of the first 512 keys is a lower bound of their mass
+    assert (m[:small] >= ref * (1 - 1e-4) - 1e-9).all()
+
+
+def _dyn_inputs(T, seed, ties):
+    r = np.random.default_rng(seed)
+    if ties:
+        m = r.integers(1, 5, T).astype(np.float32) / np.float32(4 * T)
+        s = r.integers(0, 3, T).astype(np.float32)
+    else:
+        m = (r.exponential(size=T) / T).astype(np.float32)
+        s = r.exponential(size=T).astype(np.float32)
+    return m, s
+
+
+@pytest.mark.parametrize("T,seed,ties", [(1, 0, False), (7, 1, False), (100, 2, True), (1000, 3, False),
+                                         (5120, 4, False), (5120, 5, True), (8192, 6, False)])
+def test_dynamic_recompute_matches_oracle(T, seed, ties):
+    announce(f"dynamic recompute T={T} ties={ties}")
+    m, s = _dyn_inputs(T, seed, ties)
+    sel, counts = ss.dynamic_recompute(torch.from_numpy(m).cuda(), torch.from_numpy(s).cuda())
+    c = counts.cpu().numpy()
+    ar, ref_sel, n_hot = orc.dynamic_recompute(m, s)
+    assert c[0] == ar and c[2] == n_hot and c[1] == len(ref_sel)
+    assert np.array_equal(sel.cpu().numpy()[: c[1]], ref_sel)
+
+
+def test_dynamic_recompute_weights_and_empty():
+    m, s = _dyn_inputs(500, 9, False)
+    mt, st = torch.from_numpy(m).cuda(), torch.from_numpy(s).cuda()
+    announce("dynamic recompute w = 1 / w = 0 / empty")
+    sel, counts = ss.dynamic_recompute(mt, st, w_hot=1.0, w_cold=1.0)
+    assert counts.cpu().numpy()[1] == 500 and np.array_equal(sel.cpu().numpy(), np.arange(500))
+    _, counts = ss.dynamic_recompute(mt, st, w_hot=0.0, w_cold=0.0)
+    assert counts.cpu().numpy()[1] == 0
+    e = torch.empty(0, dtype=torch.float32, device="cuda")
+    _, counts = ss.dynamic_recompute(e, e)
+    assert counts.cpu().numpy().tolist() == [0, 0, 0]

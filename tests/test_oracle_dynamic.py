@@ -1,0 +1,104 @@
+"""Oracle pins for the average attention score per token, Attention Recovery
+and the dynamic recompute set (Section 3 Insight 2 and its AR equation;
+Section 4.3.3).  CPU only."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as orc
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+@pytest.mark.parametrize("T,hq,hkv", [(1, 2, 1), (9, 4, 2), (40, 4, 4)])
+def test_mass_sums_to_one(T, hq, hkv):
+    # every softmax row sums to 1, so the mean over heads and rows does too
+    r = _rng(T)
+    q, k = r.normal(size=(T, hq, 8)), r.normal(size=(T, hkv, 8))
+    m = orc.attention_mass(q, k, hq, hkv, 8)
+    assert m.shape == (T,) and abs(m.sum() - 1.0) < 1e-12 and (m > 0).all()
+
+
+def test_mass_zero_queries_is_harmonic():
+    # q = 0: row i spreads 1/(i+1) over keys 0..i, so mass_j = (H_T - H_j) / T
+    T = 23
+    k = _rng(1).normal(size=(T, 1, 16))
+    m = orc.attention_mass(np.zeros((T, 2, 16)), k, 2, 1, 16)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, T + 1))])
+    assert np.allclose(m, (H[T] - H[:T]) / T, rtol=0, atol=1e-15)
+
+
+def test_mass_one_dominant_key_closed_form():
+    # scores a against key 0 and 0 against every other key: P_i0 = e^a / (e^a + i)
+    T, D, a = 17, 4, 3.0
+    q = np.zeros((T, 1, D)); q[:, 0, 0] = 1.0
+    k = np.zeros((T, 1, D)); k[0, 0, 0] = a * np.sqrt(D)
+    m = orc.attention_mass(q, k, 1, 1, D)
+    i = np.arange(T)
+    assert abs(m[0] - np.mean(np.exp(a) / (np.exp(a) + i))) < 1e-14
+    # every other key j gets 1 / (e^a + i) from each row i >= j
+    for j in range(1, T):
+        assert abs(m[j] - np.sum(1.0 / (np.exp(a) + i[j:])) / T) < 1e-14
+
+
+def test_mass_gqa_equals_mha_with_repeated_kv():
+    r = _rng(3)
+    T, hq, hkv, D = 12, 4, 2, 8
+    q, k = r.normal(size=(T, hq, D)), r.normal(size=(T, hkv, D))
+    m_gqa = orc.attention_mass(q, k, hq, hkv, D)
+    m_mha = orc.attention_mass(q, np.repeat(k, hq // hkv, axis=1), hq, hq, D)
+    assert np.allclose(m_gqa, m_mha, rtol=0, atol=1e-15)
+
+
+def _ar_exact(m32, thres):
+    # exact rationals on the fp32 values (no fixed point): smallest k reaching thres
+    vals = [Fraction(float(min(max(x, 0.0), 1.0))) for x in m32]
+    order = sorted(range(len(vals)), key=lambda j: (-vals[j], j))
+    total = sum(vals)
+    run = Fraction(0)
+    for n, j in enumerate(order, start=1):
+        run += vals[j]
+        if run >= Fraction(thres) * total:
+            return n
+    return len(vals)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_attention_recovery_equals_exact_rationals(seed):
+    r = _rng(100 + seed)
+    n = int(r.integers(1, 60))
+    m = (r.exponential(size=n) / n).astype(np.float32)
+    ar, order = orc.attention_recovery(m, 0.55)
+    assert ar == _ar_exact(m, 0.55)
+    assert sorted(order.tolist()) == list(range(n))
+
+
+def test_attention_recovery_closed_forms():
+    assert orc.attention_recovery(np.full(10, 0.1, np.float32), 0.55)[0] == 6  # ceil(0.55 * 10)
+    assert orc.attention_recovery(np.full(200, 0.005, np.float32), 0.55)[0] == 110
+    one = np.full(50, 0.001, np.float32); one[31] = 0.9
+    ar, order = orc.attention_recovery(one, 0.55)
+    assert ar == 1 and order[0] == 31
+    assert orc.attention_recovery(np.zeros(5, np.float32), 0.55)[0] == 1  # 0 >= 0 at once
+    assert orc.attention_recovery(np.zeros(0, np.float32), 0.55)[0] == 0
+    ties = np.array([0.2, 0.3, 0.2, 0.3], np.float32)
+    assert orc.attention_recovery(ties, 0.55)[1].tolist() == [1, 3, 0, 2]  # lower position first on ties
+
+
+def test_dynamic_recompute_counts_and_ties():
+    n = 40
+    m = np.full(n, 1.0 / n, np.float32)           # AR = 22: positions 0..21 hot
+    sig = np.ones(n, np.float32)                  # all equal: the lowest positions of each group
+    ar, sel, n_hot = orc.dynamic_recompute(m, sig, 0.55, 0.5, 0.1)
+    assert ar == 22 and n_hot == 11
+    assert sel.tolist() == list(range(11)) + [22, 23]  # floor(0.1 * 18 + 1/2) = 2 cold
+    # the deviation decides within each group
+    sig2 = np.arange(n, dtype=np.float32)
+    _, sel2, _ = orc.dynamic_recompute(m, sig2, 0.55, 0.5, 0.1)
+    assert sel2.tolist() == list(range(11, 22)) + [38, 39]
+    # w = 1 recomputes everything, w = 0 nothing
+    assert orc.dynamic_recompute(m, sig2, 0.55, 1.0, 1.0)[1].tolist() == list(range(n))
+    assert orc.dynamic_recompute(m, sig2, 0.55, 0.0, 0.0)[1].size == 0
