@@ -6,17 +6,17 @@
 // P_h[i][j] of every head h, averaged over the heads and over the query rows
 // i (rows before j contribute zero).  Two MFMA passes over the causal score
 // matrix, bf16 operands and fp32 accumulation, exponentials in base 2:
-//   mass_lse_kernel  one wave per (4 query blocks of 32, head): S^T = K Q^T,
+//   mass_lse_kernel  one wave per (2 query blocks of 32, head): S^T = K Q^T,
 //                    so each lane owns a query column and keeps its row's
 //                    running max and sum over its 16 keys per block; the
 //                    two lane halves merge at the end -> lse2[h][i].
-//   mass_col_kernel  one wave per (4 key blocks of 32, head): S = Q K^T, so
+//   mass_col_kernel  one wave per (2 key blocks of 32, head): S = Q K^T, so
 //                    each lane owns a key column and sums exp2(s - lse2[i])
 //                    over its 16 rows per block -> part[h][j].
 //   mass_final_kernel sums the heads in a fixed order and divides by H_q T.
-// Each wave keeps the operands of its 4 fixed blocks (queries, resp. keys)
+// Each wave keeps the operands of its 2 fixed blocks (queries, resp. keys)
 // in VGPRs and streams the other operand from global memory, one 32 x 128
-// tile feeding 4 x 8 MFMAs.
+// tile feeding 2 x 8 MFMAs, the next tile's loads in flight meanwhile.
 //
 // dyn_select_kernel (one workgroup): tokens sorted by mass (descending, lower
 // position first on ties); AR is the smallest count whose prefix reaches
@@ -30,7 +30,7 @@
 namespace semshare {
 namespace {
 
-constexpr int kNB = 4;  // fixed 32-blocks per wave
+constexpr int kNB = 2;  // fixed 32-blocks per wave (two waves per SIMD fit)
 constexpr float kNegInf = -__builtin_inff();
 
 __device__ __forceinline__ bf16x8_t ld8(const uint16_t* p) {
@@ -60,42 +60,61 @@ __global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict
 #pragma unroll
     for (int b = 0; b < kNB; ++b) { m[b] = kNegInf; l[b] = 0.0f; }
     const int64_t kb_end = qb0 + kNB < nb ? qb0 + kNB : nb;
-    for (int64_t kb = 0; kb < kb_end; ++kb) {
+    auto load_k = [&](int64_t kb, bf16x8_t (&ak)[8]) {
         int64_t kj = kb * 32 + l32;
         if (kj >= T) kj = T - 1;
         const uint16_t* krow = k + (kj * Hkv + kvh) * 128 + 8 * half;
-        bf16x8_t ak[8];
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) ak[ks] = ld8(krow + 16 * ks);
+    };
+    auto tile = [&](int64_t kb, const bf16x8_t (&ak)[8]) {
 #pragma unroll
         for (int b = 0; b < kNB; ++b) {
             if (kb > qb0 + b) continue;  // wave-uniform: the block lies above the diagonal
             f32x16_t acc = {};
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], acc, 0, 0, 0);
-            // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32]
-            const int64_t qi = (qb0 + b) * 32 + l32;
+            // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32];
+            // only the diagonal block has keys after its queries
             float t[16], bm = kNegInf;
+            if (kb == qb0 + b) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t key = kb * 32 + out_row(v, half);
-                t[v] = key <= qi ? acc[v] * scale_log2e : kNegInf;
-                bm = fmaxf(bm, t[v]);
+                for (int v = 0; v < 16; ++v) {
+                    t[v] = out_row(v, half) <= l32 ? acc[v] * scale_log2e : kNegInf;
+                    bm = fmaxf(bm, t[v]);
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    t[v] = acc[v] * scale_log2e;
+                    bm = fmaxf(bm, t[v]);
+                }
             }
             const float mn = fmaxf(m[b], bm);
             if (mn == kNegInf) continue;  // no key of this half seen yet
             float sum = 0.0f;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sum += exp2f(t[v] - mn);
-            l[b] = l[b] * exp2f(m[b] - mn) + sum;
+            for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(t[v] - mn);
+            l[b] = l[b] * __builtin_amdgcn_exp2f(m[b] - mn) + sum;
             m[b] = mn;
         }
+    };
+    // the next tile's loads are in flight while the current one is used
+    bf16x8_t ka[8], kc[8];
+    load_k(0, ka);
+    for (int64_t kb = 0; kb < kb_end; kb += 2) {
+        if (kb + 1 < kb_end) load_k(kb + 1, kc);
+        tile(kb, ka);
+        if (kb + 1 >= kb_end) break;
+        if (kb + 2 < kb_end) load_k(kb + 2, ka);
+        tile(kb + 1, kc);
     }
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
         const float om = __shfl_xor(m[b], 32), ol = __shfl_xor(l[b], 32);
         const float M = fmaxf(m[b], om);
-        const float L = (m[b] == kNegInf ? 0.0f : l[b] * exp2f(m[b] - M)) + (om == kNegInf ? 0.0f : ol * exp2f(om - M));
+        const float L = (m[b] == kNegInf ? 0.0f : l[b] * __builtin_amdgcn_exp2f(m[b] - M)) +
+                        (om == kNegInf ? 0.0f : ol * __builtin_amdgcn_exp2f(om - M));
         const int64_t qi = (qb0 + b) * 32 + l32;
         if (half == 0 && qi < T) lse2[(int64_t)h * T + qi] = M + log2f(L);
     }
@@ -121,33 +140,47 @@ __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict
 #pragma unroll
     for (int b = 0; b < kNB; ++b) col[b] = 0.0f;
     const float* lse_h = lse2 + (int64_t)h * T;
-    for (int64_t qb = kb0; qb < nb; ++qb) {
+    auto load_q = [&](int64_t qb, bf16x8_t (&aq)[8], float (&L)[16]) {
         int64_t qi = qb * 32 + l32;
         if (qi >= T) qi = T - 1;
         const uint16_t* qrow = q + (qi * Hq + h) * 128 + 8 * half;
-        bf16x8_t aq[8];
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) aq[ks] = ld8(qrow + 16 * ks);
-        float L[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int64_t r = qb * 32 + out_row(v, half);
             L[v] = r < T ? lse_h[r] : __builtin_inff();
         }
+    };
+    auto tile = [&](int64_t qb, const bf16x8_t (&aq)[8], const float (&L)[16]) {
 #pragma unroll
         for (int b = 0; b < kNB; ++b) {
             if (qb < kb0 + b) continue;  // wave-uniform: every row of the block precedes the keys
             f32x16_t acc = {};
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[ks], bk[b][ks], acc, 0, 0, 0);
-            // acc[v] = S[query = 32 qb + out_row(v)][key = 32 (kb0 + b) + l32]
-            const int64_t key = (kb0 + b) * 32 + l32;
+            // acc[v] = S[query = 32 qb + out_row(v)][key = 32 (kb0 + b) + l32];
+            // only the diagonal block has rows before its keys; rows past T
+            // carry L = inf and add 0
+            if (qb == kb0 + b) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t r = qb * 32 + out_row(v, half);
-                col[b] += key <= r ? exp2f(acc[v] * scale_log2e - L[v]) : 0.0f;  // rows past T: L = inf -> 0
+                for (int v = 0; v < 16; ++v)
+                    col[b] += l32 <= out_row(v, half) ? __builtin_amdgcn_exp2f(acc[v] * scale_log2e - L[v]) : 0.0f;
+            } else {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) col[b] += __builtin_amdgcn_exp2f(acc[v] * scale_log2e - L[v]);
             }
         }
+    };
+    bf16x8_t qa[8], qc[8];
+    float La[16], Lc[16];
+    if (kb0 < nb) load_q(kb0, qa, La);
+    for (int64_t qb = kb0; qb < nb; qb += 2) {
+        if (qb + 1 < nb) load_q(qb + 1, qc, Lc);
+        tile(qb, qa, La);
+        if (qb + 1 >= nb) break;
+        if (qb + 2 < nb) load_q(qb + 2, qa, La);
+        tile(qb + 1, qc, Lc);
     }
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
