@@ -402,12 +402,44 @@ def dynamic_recompute_line(torch, np, ss, cfg, args):
     us_mass, us_sel = t_mass / args.steps * 1e3, t_sel / args.steps * 1e3
     flops = 4 * D * hq * T * (T + 1) / 2
     c = counts.cpu().numpy().tolist()
+    # retention (first layer): window of the last (1 - AR/T) rows, ranking,
+    # and the compaction of a 32-layer K/V cache to the kept rows
+    ar = c[0]
+    row_begin = min(T - 1, T - int(np.floor((1.0 - ar / T) * T + 0.5)))
+    L = 32
+    kc = torch.randn(L, T, hkv, D, device="cuda").to(torch.bfloat16)
+    vc = torch.randn(L, T, hkv, D, device="cuda").to(torch.bfloat16)
+    score = torch.empty(T, dtype=torch.float32, device="cuda")
+    t_win = t_ret = t_cmp = 0.0
+    for it in range(args.warmup + args.steps):
+        ev[0].record()
+        ss.attention_mass(q, k, hq, hkv, mass=score, workspace=ws, row_begin=row_begin)
+        ev[1].record()
+        rank, kept, n_kept = ss.retention(mass, score, sel, counts, 0.8)
+        ev[2].record()
+        torch.cuda.synchronize()
+        nk = int(n_kept.cpu().numpy()[0])
+        e3, e4 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e3.record()
+        ok, ov = ss.gather_kv(kc, vc, kept[:nk])
+        e4.record()
+        torch.cuda.synchronize()
+        if it >= args.warmup:
+            t_win += ev[0].elapsed_time(ev[1])
+            t_ret += ev[1].elapsed_time(ev[2])
+            t_cmp += e3.elapsed_time(e4)
+    n = args.steps
     out = {"metric": "dynamic_recompute_us", "value": us_mass + us_sel, "unit": "us", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "higher_is_better": False, "data": "synthetic", "dtype": "bf16",
            "config": {"workload": "average attention score per token + AR 55% + hot/cold recompute set, 5120 tokens, "
-                                  "32q/8kv heads, head_dim 128"},
+                                  "32q/8kv heads, head_dim 128; then first-layer retention and a 32-layer cache "
+                                  "compaction"},
            "attention_mass_us": round(us_mass, 2), "dynamic_select_us": round(us_sel, 2),
            "AR": c[0], "n_recompute": c[1], "n_hot_recompute": c[2],
+           "retention": {"window_rows": T - row_begin, "window_mass_us": round(t_win / n * 1e3, 2),
+                         "rank_us": round(t_ret / n * 1e3, 2), "n_kept": nk,
+                         "compaction_us": round(t_cmp / n * 1e3, 2),
+                         "compaction_GB_per_s": 2 * 2 * L * nk * hkv * D * 2 / (t_cmp / n * 1e-3) / 1e9},
            "roofline": {"kernel": "mass_lse_kernel + mass_col_kernel + mass_final_kernel", "bound": "mfma",
                         "achieved": flops / (us_mass * 1e-6) / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                         "frac": flops / (us_mass * 1e-6) / 1e12 / BF16_PEAK_TFLOPS}}

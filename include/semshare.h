@@ -310,9 +310,12 @@ semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, i
 /*
  * Average attention score of every token at a fully computed layer (Section
  * 3, Insight 2: the attention of each head averaged over the heads, then
- * over the query rows): mass[j] = sum_h sum_{i >= j} P_h[i][j] / (n_q_heads
- * n_tok), P_h the causal softmax of q_i . k_j * sm_scale (GQA: head h reads
- * kv head h / (n_q_heads / n_kv_heads)).  The masses sum to 1.
+ * over the query rows): mass[j] = sum_h sum_{i >= max(j, row_begin)}
+ * P_h[i][j] / (n_q_heads (n_tok - row_begin)), P_h the causal softmax of
+ * q_i . k_j * sm_scale (GQA: head h reads kv head h / (n_q_heads /
+ * n_kv_heads)).  row_begin = 0 averages every row (the masses sum to 1);
+ * row_begin > 0 averages the last n_tok - row_begin rows only, the window
+ * the retention step ranks by (Section 4.3.4).  0 <= row_begin < n_tok.
  *   q        [n_tok][n_q_heads][head_dim] bf16 (RoPE'd queries of every row)
  *   k_cache  [n_tok][n_kv_heads][head_dim] bf16
  *   mass     [n_tok] float32 (output)
@@ -321,10 +324,32 @@ semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, i
  *   bytes, 4-byte aligned; q and k_cache 16-byte aligned.
  */
 size_t semshare_attention_mass_workspace(int64_t n_tok, int32_t n_q_heads);
-semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int32_t n_q_heads,
-                                          int32_t n_kv_heads, int32_t head_dim, float sm_scale, float* mass,
-                                          void* workspace, size_t workspace_bytes, semshare_dtype_t dtype,
-                                          void* stream);
+semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int64_t row_begin,
+                                          int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float sm_scale,
+                                          float* mass, void* workspace, size_t workspace_bytes,
+                                          semshare_dtype_t dtype, void* stream);
+
+/*
+ * Token retention on the first layer (Section 4.3.4; Appendix A.6 gives the
+ * per-layer counts Retain[i] = T prod alpha[j]): hot tokens (the counts[0]
+ * first by mass, as semshare_dynamic_recompute orders them) and the
+ * recomputed tokens sel_pos[0 .. counts[1]) are never evicted; they rank
+ * first, in position order, followed by every other token by score
+ * (descending, lower position first on ties), score being the average
+ * attention over the last (1 - AR / T) of the rows (semshare_attention_mass
+ * with row_begin).  Kept are the first R = max(floor(max(min_keep, AR / T)
+ * n_tok + 1/2), number of never-evicted tokens) of that ranking (the paper:
+ * min_keep = 0.8), written to kept_pos in ascending order; *n_kept = R.
+ * rank[p] is the place of position p in the ranking, so a later layer that
+ * keeps Retain[i] tokens keeps those with rank < Retain[i] (nested sets).
+ * Compacting the cache is semshare_gather_kv with idx = kept_pos.
+ *   mass, score  [n_tok] float32;  sel_pos, counts: the outputs of
+ *   semshare_dynamic_recompute (device).   rank, kept_pos [n_tok] int32,
+ *   n_kept [1] int32 (outputs, device).   n_tok <= 8192.
+ */
+semshare_status_t semshare_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
+                                     const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos,
+                                     int32_t* n_kept, void* stream);
 
 /*
  * Dynamic recompute set (Section 4.3.3 with the Attention Recovery equation

@@ -250,11 +250,13 @@ def similarity(dist, dmin: float = 0.0, dmax: float = 30.0) -> float:
     return float(_load().orc_similarity(_ptr(d), d.size, float(dmin), float(dmax)))
 
 
-def attention_mass(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, sm_scale: float = 0.0) -> np.ndarray:
+def attention_mass(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, sm_scale: float = 0.0,
+                   row_begin: int = 0) -> np.ndarray:
     """Average attention score of every token at a fully computed layer
     (Section 3, Insight 2): the causal softmax attention of each head, averaged
-    over the heads and then over the query rows (the first dimension).  fp64;
-    one T x T score matrix per head (numpy matmul as the product step)."""
+    over the heads and then over the query rows (the first dimension) from
+    row_begin on (Section 4.3.4 ranks retention by the last rows).  fp64; one
+    T x T score matrix per head (numpy matmul as the product step)."""
     q = _f64(q).reshape(q.shape[0], n_q_heads, head_dim)
     k = _f64(k_cache).reshape(k_cache.shape[0], n_kv_heads, head_dim)
     T = q.shape[0]
@@ -267,8 +269,8 @@ def attention_mass(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, s
         s = np.where(causal, s, -np.inf)
         p = np.exp(s - s.max(axis=1, keepdims=True))
         p /= p.sum(axis=1, keepdims=True)
-        total += p.sum(axis=0)
-    return total / (n_q_heads * T)
+        total += p[row_begin:].sum(axis=0)
+    return total / (n_q_heads * (T - row_begin))
 
 
 def _mass_fixed(m32: np.ndarray) -> np.ndarray:
@@ -315,3 +317,22 @@ def dynamic_recompute(mass, sigma, thres: float = 0.55, w_hot: float = 0.5,
     by_sigma = lambda js: sorted(js, key=lambda j: (-float(sig[j]), j))
     chosen = by_sigma([j for j in range(n) if j in hot])[:n_hot] + by_sigma([j for j in range(n) if j not in hot])[:n_cold]
     return ar, np.array(sorted(chosen), dtype=np.int64), n_hot
+
+
+def retention(mass, score, ar: int, sel_pos, min_keep: float = 0.8) -> Tuple[np.ndarray, np.ndarray, int]:
+    """First-layer retention (Section 4.3.4): hot tokens (the ar first by mass)
+    and recomputed tokens are never evicted and rank first in position order;
+    the others follow by score, largest first (lower position first on ties).
+    The first max(floor(max(min_keep, ar / T) T + 1/2), never-evicted) are kept.
+    Returns (rank of every position, kept positions ascending, count kept)."""
+    n = len(mass)
+    _, order = attention_recovery(mass)
+    forced = set(int(j) for j in order[:ar]) | set(int(j) for j in sel_pos)
+    sc = np.maximum(np.asarray(score, dtype=np.float32), np.float32(0))
+    rest = sorted((j for j in range(n) if j not in forced), key=lambda j: (-float(sc[j]), j))
+    ranking = sorted(forced) + rest
+    ratio = ar / n if n and ar / n > min_keep else min_keep
+    keep = min(max(int(np.floor(ratio * n + 0.5)), len(forced)), n)
+    rank = np.empty(n, dtype=np.int64)
+    rank[np.array(ranking, dtype=np.int64)] = np.arange(n)
+    return rank, np.array(sorted(ranking[:keep]), dtype=np.int64), keep

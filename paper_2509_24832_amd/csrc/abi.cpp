@@ -112,12 +112,14 @@ size_t semshare_attention_mass_workspace(int64_t n_tok, int32_t n_q_heads) {
     return semshare::attention_mass_workspace(n_tok, n_q_heads);
 }
 
-semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int32_t n_q_heads,
-                                          int32_t n_kv_heads, int32_t head_dim, float sm_scale, float* mass,
-                                          void* workspace, size_t workspace_bytes, semshare_dtype_t dtype,
-                                          void* stream) {
+semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int64_t row_begin,
+                                          int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float sm_scale,
+                                          float* mass, void* workspace, size_t workspace_bytes,
+                                          semshare_dtype_t dtype, void* stream) {
     if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "attention_mass: unknown dtype %d", dtype);
     if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "attention_mass: n_tok < 0");
+    if (row_begin < 0 || (n_tok > 0 && row_begin >= n_tok))
+        return fail(SEMSHARE_E_INVAL, "attention_mass: row_begin must lie in [0, n_tok)");
     if (n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads)
         return fail(SEMSHARE_E_INVAL, "attention_mass: n_q_heads must be a positive multiple of n_kv_heads");
     if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "attention_mass: sm_scale must be finite and >= 0");
@@ -134,9 +136,23 @@ semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, in
         return fail(SEMSHARE_E_INVAL, "attention_mass: workspace too small (%zu < %zu)", workspace_bytes,
                     semshare::attention_mass_workspace(n_tok, n_q_heads));
     const float scale = sm_scale == 0.0f ? 1.0f / sqrtf((float)head_dim) : sm_scale;
-    return from_hip(semshare::launch_attention_mass(q, k_cache, n_tok, n_q_heads, n_kv_heads, scale, mass, workspace,
-                                                    (hipStream_t)stream),
+    return from_hip(semshare::launch_attention_mass(q, k_cache, n_tok, row_begin, n_q_heads, n_kv_heads, scale, mass,
+                                                    workspace, (hipStream_t)stream),
                     "attention_mass launch");
+}
+
+semshare_status_t semshare_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
+                                     const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos,
+                                     int32_t* n_kept, void* stream) {
+    if (n_tok < 0 || n_tok > semshare::kMaxDynTok)
+        return fail(n_tok < 0 ? SEMSHARE_E_INVAL : SEMSHARE_E_UNSUPPORTED, "retention: n_tok must be in [0, %d]",
+                    semshare::kMaxDynTok);
+    if (!(min_keep >= 0.0 && min_keep <= 1.0)) return fail(SEMSHARE_E_INVAL, "retention: min_keep must lie in [0, 1]");
+    if (!counts || !n_kept || (n_tok > 0 && (!mass || !score || !sel_pos || !rank || !kept_pos)))
+        return fail(SEMSHARE_E_INVAL, "retention: null buffer");
+    return from_hip(semshare::launch_retention(mass, score, n_tok, sel_pos, counts, min_keep, rank, kept_pos, n_kept,
+                                               (hipStream_t)stream),
+                    "retention launch");
 }
 
 semshare_status_t semshare_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres,

@@ -121,8 +121,9 @@ __global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict
 }
 
 __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-                                                       int64_t T, int32_t Hq, int32_t Hkv, float scale_log2e,
-                                                       const float* __restrict__ lse2, float* __restrict__ part) {
+                                                       int64_t T, int64_t row_begin, int32_t Hq, int32_t Hkv,
+                                                       float scale_log2e, const float* __restrict__ lse2,
+                                                       float* __restrict__ part) {
     const int lane = threadIdx.x, half = lane >> 5, l32 = lane & 31;
     const int h = blockIdx.y, kvh = h / (Hq / Hkv);
     const int64_t nb = (T + 31) / 32;
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int64_t r = qb * 32 + out_row(v, half);
-            L[v] = r < T ? lse_h[r] : __builtin_inff();
+            L[v] = r < T && r >= row_begin ? lse_h[r] : __builtin_inff();  // rows outside the window add 0
         }
     };
     auto tile = [&](int64_t qb, const bf16x8_t (&aq)[8], const float (&L)[16]) {
@@ -174,8 +175,9 @@ __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict
     };
     bf16x8_t qa[8], qc[8];
     float La[16], Lc[16];
-    if (kb0 < nb) load_q(kb0, qa, La);
-    for (int64_t qb = kb0; qb < nb; qb += 2) {
+    const int64_t qb_first = kb0 > row_begin / 32 ? kb0 : row_begin / 32;
+    if (qb_first < nb) load_q(qb_first, qa, La);
+    for (int64_t qb = qb_first; qb < nb; qb += 2) {
         if (qb + 1 < nb) load_q(qb + 1, qc, Lc);
         tile(qb, qa, La);
         if (qb + 1 >= nb) break;
@@ -190,12 +192,13 @@ __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict
     }
 }
 
-__global__ void mass_final_kernel(const float* __restrict__ part, int64_t T, int32_t Hq, float* __restrict__ mass) {
+__global__ void mass_final_kernel(const float* __restrict__ part, int64_t T, int64_t n_rows, int32_t Hq,
+                                  float* __restrict__ mass) {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (j >= T) return;
     float s = 0.0f;
     for (int h = 0; h < Hq; ++h) s += part[(int64_t)h * T + j];
-    mass[j] = s / ((float)Hq * (float)T);
+    mass[j] = s / ((float)Hq * (float)n_rows);
 }
 
 // ------------------------------------------------------------ selection
@@ -331,14 +334,101 @@ __global__ __launch_bounds__(kSelThreads) void dyn_select_kernel(const float* __
     }
 }
 
+// Retention (Section 4.3.4, Appendix A.6): hot tokens (the AR first by
+// mass) and recomputed tokens are never evicted and rank first, in position
+// order; the other tokens follow by score (descending, lower position first).
+// The first R = max(floor(max(min_keep, AR / T) T + 1/2), forced) are kept.
+__global__ __launch_bounds__(kSelThreads) void retention_kernel(const float* __restrict__ mass,
+                                                                 const float* __restrict__ score, int32_t n,
+                                                                 const int32_t* __restrict__ sel_pos,
+                                                                 const int32_t* __restrict__ counts, double min_keep,
+                                                                 int32_t* __restrict__ rank,
+                                                                 int32_t* __restrict__ kept_pos,
+                                                                 int32_t* __restrict__ n_kept) {
+    __shared__ uint64_t key[kMaxDynTok];
+    __shared__ uint8_t flag[kMaxDynTok];
+    __shared__ int64_t sw[kSelThreads / 64 + 1];
+    int n2 = 1;
+    while (n2 < n) n2 <<= 1;
+    const int ar = counts[0] < n ? counts[0] : n;
+    const int n_sel = counts[1] < n ? counts[1] : n;
+    // hot set: the mass order of the dynamic selection
+    for (int i = threadIdx.x; i < n2; i += kSelThreads) {
+        if (i < n) {
+            const uint32_t mb = __float_as_uint(clamp01(mass[i]));
+            key[i] = ((uint64_t)(0xFFFFFFFFu - mb) << 32) | (uint32_t)i;
+        } else {
+            key[i] = ~0ull;
+        }
+    }
+    __syncthreads();
+    bitonic_sort(key, n2);
+    for (int i = threadIdx.x; i < n; i += kSelThreads) flag[(int)(key[i] & 0xFFFFFFFFu)] = i < ar ? 1 : 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n_sel; i += kSelThreads) {
+        const int p = sel_pos[i];
+        if (p >= 0 && p < n) flag[p] = 1;
+    }
+    __syncthreads();
+    // forced first by position, then the rest by score
+    for (int i = threadIdx.x; i < n2; i += kSelThreads) {
+        if (i < n) {
+            if (flag[i]) {
+                key[i] = (uint64_t)i;
+            } else {
+                const uint32_t sb = __float_as_uint(score[i] > 0.0f ? score[i] : 0.0f) & 0x7FFFFFFFu;
+                key[i] = (1ull << 62) | ((uint64_t)(0x7FFFFFFFu - sb) << 20) | (uint32_t)i;
+            }
+        } else {
+            key[i] = ~0ull;
+        }
+    }
+    __syncthreads();
+    bitonic_sort(key, n2);
+    constexpr int kPer = kMaxDynTok / kSelThreads;
+    const int base = threadIdx.x * kPer;
+    int64_t nf = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) nf += (base + e < n && flag[base + e]) ? 1 : 0;
+    int64_t n_forced;
+    (void)block_scan_i64(nf, &n_forced, sw);
+    const double ratio = n > 0 && (double)ar / (double)n > min_keep ? (double)ar / (double)n : min_keep;
+    int keep = (int)floor(ratio * (double)n + 0.5);
+    if (keep < (int)n_forced) keep = (int)n_forced;
+    if (keep > n) keep = n;
+    for (int i = threadIdx.x; i < n; i += kSelThreads) {
+        const int pos = (int)(key[i] & 0xFFFFFu);
+        rank[pos] = i;
+        flag[pos] = i < keep ? 1 : 0;  // reused: kept
+    }
+    __syncthreads();
+    int64_t cnt = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) cnt += (base + e < n && flag[base + e]) ? 1 : 0;
+    int64_t tot;
+    int64_t o = block_scan_i64(cnt, &tot, sw);
+#pragma unroll
+    for (int e = 0; e < kPer; ++e)
+        if (base + e < n && flag[base + e]) kept_pos[o++] = base + e;
+    if (threadIdx.x == 0) *n_kept = keep;
+}
+
 }  // namespace
+
+hipError_t launch_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
+                            const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos, int32_t* n_kept,
+                            hipStream_t s) {
+    hipLaunchKernelGGL(retention_kernel, dim3(1), dim3(kSelThreads), 0, s, mass, score, n_tok, sel_pos, counts,
+                       min_keep, rank, kept_pos, n_kept);
+    return hipGetLastError();
+}
 
 size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads) {
     return (size_t)2 * (size_t)n_q_heads * (size_t)n_tok * sizeof(float);
 }
 
-hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
-                                 float sm_scale, float* mass, void* workspace, hipStream_t s) {
+hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int64_t row_begin, int32_t n_q_heads,
+                                 int32_t n_kv_heads, float sm_scale, float* mass, void* workspace, hipStream_t s) {
     float* lse2 = static_cast<float*>(workspace);
     float* part = lse2 + (int64_t)n_q_heads * n_tok;
     const float sl2e = sm_scale * 1.4426950408889634f;
@@ -347,9 +437,10 @@ hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, in
     const auto* qp = static_cast<const uint16_t*>(q);
     const auto* kp = static_cast<const uint16_t*>(k);
     hipLaunchKernelGGL(mass_lse_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2);
-    hipLaunchKernelGGL(mass_col_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2, part);
+    hipLaunchKernelGGL(mass_col_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, row_begin, n_q_heads, n_kv_heads, sl2e,
+                       lse2, part);
     hipLaunchKernelGGL(mass_final_kernel, dim3((unsigned)((n_tok + 255) / 256)), dim3(256), 0, s, part, n_tok,
-                       n_q_heads, mass);
+                       n_tok - row_begin, n_q_heads, mass);
     return hipGetLastError();
 }
 

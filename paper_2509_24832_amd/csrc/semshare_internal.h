@@ -77,8 +77,11 @@ hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* c
 constexpr int kMaxDynTok = 8192;
 
 size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads);
-hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
-                                 float sm_scale, float* mass, void* workspace, hipStream_t s);
+hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int64_t row_begin, int32_t n_q_heads,
+                                 int32_t n_kv_heads, float sm_scale, float* mass, void* workspace, hipStream_t s);
+hipError_t launch_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
+                            const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos, int32_t* n_kept,
+                            hipStream_t s);
 hipError_t launch_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres, double w_hot,
                                     double w_cold, int32_t* sel_pos, int32_t* counts, hipStream_t s);
 

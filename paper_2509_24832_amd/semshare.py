@@ -62,7 +62,8 @@ def load() -> ctypes.CDLL:
         "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
         "semshare_select_recompute": (I32, [P, I64, I64, P, P]),
         "semshare_attention_mass_workspace": (SZ, [I64, I32]),
-        "semshare_attention_mass": (I32, [P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
+        "semshare_attention_mass": (I32, [P, P, I64, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
+        "semshare_retention": (I32, [P, P, I32, P, P, F64, P, P, P, P]),
         "semshare_dynamic_recompute": (I32, [P, P, I32, F64, F64, F64, P, P, P]),
         "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
@@ -179,8 +180,10 @@ def rope_lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.T
 
 
 def attention_mass(q: torch.Tensor, k_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int, sm_scale: float = 0.0,
-                   mass: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Average attention score per token: q [T, Hq, D], k_cache [T, Hkv, D] -> mass [T] float32."""
+                   mass: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   row_begin: int = 0) -> torch.Tensor:
+    """Average attention score per token over the query rows >= row_begin: q [T, Hq, D], k_cache [T, Hkv, D]
+    -> mass [T] float32."""
     _dev(q, "q")
     _dev(k_cache, "k_cache", q.dtype)
     T = q.shape[0]
@@ -191,7 +194,8 @@ def attention_mass(q: torch.Tensor, k_cache: torch.Tensor, n_q_heads: int, n_kv_
     need = int(load().semshare_attention_mass_workspace(T, n_q_heads))
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
-    _call("semshare_attention_mass", _ptr(q), _ptr(k_cache), T, n_q_heads, n_kv_heads, d, float(sm_scale), _ptr(mass),
+    _call("semshare_attention_mass", _ptr(q), _ptr(k_cache), T, int(row_begin), n_q_heads, n_kv_heads, d,
+          float(sm_scale), _ptr(mass),
           _ptr(workspace), workspace.numel() * workspace.element_size(), _dt(q), _stream())
     return mass
 
@@ -211,6 +215,22 @@ def dynamic_recompute(mass: torch.Tensor, sigma: torch.Tensor, thres: float = 0.
     _call("semshare_dynamic_recompute", _ptr(mass), _ptr(sigma), T, float(thres), float(w_hot), float(w_cold),
           _ptr(sel_pos), _ptr(counts), _stream())
     return sel_pos, counts
+
+
+def retention(mass: torch.Tensor, score: torch.Tensor, sel_pos: torch.Tensor, counts: torch.Tensor,
+              min_keep: float = 0.8) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """First-layer retention: returns (rank [T], kept_pos [T] with the first n_kept valid, n_kept [1]), on the device."""
+    _dev(mass, "mass", torch.float32)
+    _dev(score, "score", torch.float32)
+    _dev(sel_pos, "sel_pos", torch.int32)
+    _dev(counts, "counts", torch.int32)
+    T = mass.shape[0]
+    rank = torch.empty(max(T, 1), dtype=torch.int32, device=mass.device)
+    kept = torch.empty(max(T, 1), dtype=torch.int32, device=mass.device)
+    n_kept = torch.empty(1, dtype=torch.int32, device=mass.device)
+    _call("semshare_retention", _ptr(mass), _ptr(score), T, _ptr(sel_pos), _ptr(counts), float(min_keep), _ptr(rank),
+          _ptr(kept), _ptr(n_kept), _stream())
+    return rank, kept, n_kept
 
 
 def _match(entry: str, tgt_codes, ref_codes, idx, dist, want_dist):

@@ -91,14 +91,14 @@ def test_attention_mass_and_dynamic_validation(lib):
     e = "semshare_attention_mass"
     ws = int(lib.semshare_attention_mass_workspace(100, 32))
     assert ws == 2 * 32 * 100 * 4
-    assert _st(e, FAKE, FAKE, 100, 32, 8, 128, 0.0, FAKE, FAKE, ws, 0, None) == b.E_UNSUPPORTED  # fp32
-    assert _st(e, FAKE, FAKE, 100, 32, 8, 64, 0.0, FAKE, FAKE, ws, 1, None) == b.E_UNSUPPORTED  # head_dim
-    assert _st(e, FAKE, FAKE, 100, 32, 6, 128, 0.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # GQA
-    assert _st(e, FAKE, FAKE, 100, 32, 8, 128, -1.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # scale
-    assert _st(e, FAKE, FAKE, 100, 32, 8, 128, 0.0, FAKE, FAKE, ws - 4, 1, None) == b.E_INVAL  # workspace
-    assert _st(e, FAKE_ODD, FAKE, 100, 32, 8, 128, 0.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # alignment
-    assert _st(e, FAKE, FAKE, 100, 32, 8, 128, 0.0, None, FAKE, ws, 1, None) == b.E_INVAL  # null mass
-    assert _st(e, None, None, 0, 32, 8, 128, 0.0, None, None, 0, 1, None) == b.OK
+    assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, FAKE, FAKE, ws, 0, None) == b.E_UNSUPPORTED  # fp32
+    assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 64, 0.0, FAKE, FAKE, ws, 1, None) == b.E_UNSUPPORTED  # head_dim
+    assert _st(e, FAKE, FAKE, 100, 0, 32, 6, 128, 0.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # GQA
+    assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 128, -1.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # scale
+    assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, FAKE, FAKE, ws - 4, 1, None) == b.E_INVAL  # workspace
+    assert _st(e, FAKE_ODD, FAKE, 100, 0, 32, 8, 128, 0.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # alignment
+    assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, None, FAKE, ws, 1, None) == b.E_INVAL  # null mass
+    assert _st(e, None, None, 0, 0, 32, 8, 128, 0.0, None, None, 0, 1, None) == b.OK
     d = "semshare_dynamic_recompute"
     assert _st(d, FAKE, FAKE, 8193, 0.55, 0.5, 0.1, FAKE, FAKE, None) == b.E_UNSUPPORTED
     assert _st(d, FAKE, FAKE, -1, 0.55, 0.5, 0.1, FAKE, FAKE, None) == b.E_INVAL

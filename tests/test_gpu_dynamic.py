@@ -87,3 +87,30 @@ def test_dynamic_recompute_weights_and_empty():
     e = torch.empty(0, dtype=torch.float32, device="cuda")
     _, counts = ss.dynamic_recompute(e, e)
     assert counts.cpu().numpy().tolist() == [0, 0, 0]
+
+
+@pytest.mark.parametrize("T,row_begin", [(300, 137), (1024, 900), (64, 63)])
+def test_window_mass_matches_oracle(T, row_begin):
+    cfg = CONFIGS[1]
+    announce(f"window mass T={T} row_begin={row_begin}")
+    q, k = _qk(cfg, T, 8, 2, tag=80 + T)
+    m = host(ss.attention_mass(dev(q, "bf16"), dev(k, "bf16"), 8, 2, row_begin=row_begin))
+    ref = orc.attention_mass(q, k, 8, 2, 128, row_begin=row_begin)
+    assert np.allclose(m, ref, rtol=1e-4, atol=1e-8), np.abs(m - ref).max()
+
+
+@pytest.mark.parametrize("T,seed,ties,min_keep", [(1, 0, False, 0.8), (50, 1, True, 0.8), (1000, 2, False, 0.8),
+                                                  (5120, 3, False, 0.8), (5120, 4, True, 0.5), (8192, 5, False, 1.0)])
+def test_retention_matches_oracle(T, seed, ties, min_keep):
+    announce(f"retention T={T} ties={ties} min_keep={min_keep}")
+    m, s = _dyn_inputs(T, seed, ties)
+    score = _dyn_inputs(T, seed + 100, ties)[0]
+    mt, st, sct = (torch.from_numpy(a).cuda() for a in (m, s, score))
+    sel, counts = ss.dynamic_recompute(mt, st)          # the GPU's own selection feeds the GPU retention
+    rank, kept, n_kept = ss.retention(mt, sct, sel, counts, min_keep)
+    ar, ref_sel, _ = orc.dynamic_recompute(m, s)        # the oracle's own selection feeds the oracle
+    ref_rank, ref_kept, ref_keep = orc.retention(m, score, ar, ref_sel, min_keep)
+    nk = int(n_kept.cpu().numpy()[0])
+    assert nk == ref_keep
+    assert np.array_equal(rank.cpu().numpy()[:T], ref_rank)
+    assert np.array_equal(kept.cpu().numpy()[:nk], ref_kept)

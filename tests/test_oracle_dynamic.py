@@ -102,3 +102,40 @@ def test_dynamic_recompute_counts_and_ties():
     # w = 1 recomputes everything, w = 0 nothing
     assert orc.dynamic_recompute(m, sig2, 0.55, 1.0, 1.0)[1].tolist() == list(range(n))
     assert orc.dynamic_recompute(m, sig2, 0.55, 0.0, 0.0)[1].size == 0
+
+
+def test_window_mass_last_row_is_its_softmax():
+    # row_begin = T - 1: the mass is the last row's softmax averaged over heads
+    r = _rng(7)
+    T, hq, D = 11, 2, 8
+    q, k = r.normal(size=(T, hq, D)), r.normal(size=(T, 1, D))
+    m = orc.attention_mass(q, k, hq, 1, D, row_begin=T - 1)
+    want = np.zeros(T)
+    for h in range(hq):
+        s = k[:, 0, :] @ q[T - 1, h, :] / np.sqrt(D)
+        e = np.exp(s - s.max())
+        want += e / e.sum()
+    assert np.allclose(m, want / hq, rtol=0, atol=1e-15) and abs(m.sum() - 1) < 1e-12
+    # the window average of every row is the full mass
+    assert np.allclose(orc.attention_mass(q, k, hq, 1, D, row_begin=0), orc.attention_mass(q, k, hq, 1, D))
+
+
+def test_retention_rules():
+    n = 50
+    m = np.full(n, 1.0 / n, np.float32)               # AR = 28 at 0.55: positions 0..27 hot
+    ar, sel, _ = orc.dynamic_recompute(m, np.arange(n, dtype=np.float32))
+    assert ar == 28
+    score = np.arange(n, dtype=np.float32)[::-1].copy()  # lower positions score higher
+    rank, kept, keep = orc.retention(m, score, ar, sel, 0.8)
+    forced = set(range(28)) | set(sel.tolist())
+    assert keep == 40                                   # floor(0.8 * 50 + 1/2)
+    assert set(kept.tolist()) >= forced                 # never evicted
+    assert sorted(rank[sorted(forced)].tolist()) == list(range(len(forced)))  # forced rank first
+    rest = [j for j in range(n) if j not in forced]
+    assert [j for j in np.argsort(rank) if j not in forced] == rest  # then by score (descending)
+    assert kept.tolist() == sorted(np.argsort(rank)[:keep].tolist())
+    # min_keep 1 keeps all; a large AR overrides min_keep; nested sets for fewer kept
+    assert orc.retention(m, score, ar, sel, 1.0)[2] == n
+    assert orc.retention(m, score, 45, [], 0.8)[2] == 45
+    assert orc.retention(m, score, 45, sel, 0.8)[2] == 47  # 45 hot + the 2 cold recomputed: all kept
+    assert set(np.argsort(rank)[:30].tolist()) <= set(kept.tolist())
