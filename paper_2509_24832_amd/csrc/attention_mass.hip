@@ -204,18 +204,57 @@ __global__ void mass_final_kernel(const float* __restrict__ part, int64_t T, int
 // ------------------------------------------------------------ selection
 constexpr int kSelThreads = 1024;
 
+__device__ __forceinline__ void cmp_swap(uint64_t& a, uint64_t& b, bool up) {
+    if ((a > b) == up) {
+        const uint64_t t = a;
+        a = b;
+        b = t;
+    }
+}
+
+// Bitonic sort (ascending) of n2 = 2^k keys in LDS by the whole workgroup.
+// Thread t owns elements [8t, 8t + 8) and wave w the 512 elements [512w,
+// 512w + 512): passes with stride >= 512 exchange across waves (a workgroup
+// barrier each), strides 8 .. 256 stay inside a wave's segment (the wave's
+// own LDS traffic is ordered, so no barrier), strides 4, 2, 1 inside a
+// thread's registers.
 __device__ __forceinline__ void bitonic_sort(uint64_t* key, int n2) {
+    const int t = threadIdx.x;
     for (int size = 2; size <= n2; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int t = threadIdx.x; t < n2 / 2; t += kSelThreads) {
-                const int i = 2 * t - (t & (stride - 1));  // lower element of the pair
-                const int j = i + stride;
-                const bool up = (i & size) == 0;
-                const uint64_t a = key[i], b = key[j];
-                if ((a > b) == up) { key[i] = b; key[j] = a; }
+        int stride = size >> 1;
+        for (; stride >= 512; stride >>= 1) {  // across waves
+            for (int p = t; p < n2 / 2; p += kSelThreads) {
+                const int i = 2 * p - (p & (stride - 1));
+                cmp_swap(key[i], key[i + stride], (i & size) == 0);
             }
             __syncthreads();
         }
+        const int seg = 512 * (t >> 6), lane = t & 63;
+        if (seg < n2) {
+            for (; stride >= 8; stride >>= 1) {  // inside the wave's segment
+                for (int p = lane; p < 256; p += 64) {
+                    const int i = seg + 2 * p - (p & (stride - 1));
+                    if (i + stride < n2) cmp_swap(key[i], key[i + stride], (i & size) == 0);
+                }
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+            }
+            if (8 * t < n2) {  // strides 4, 2, 1 in registers
+                uint64_t r[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) r[e] = key[8 * t + e];
+#pragma unroll
+                for (int st = 4; st >= 1; st >>= 1) {
+                    if (st >= size) continue;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if ((e & st) == 0) cmp_swap(r[e], r[e + st], ((8 * t + e) & size) == 0);
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) key[8 * t + e] = r[e];
+            }
+        }
+        __syncthreads();
     }
 }
 
