@@ -76,25 +76,24 @@ __global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict
             for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], acc, 0, 0, 0);
             // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32];
             // only the diagonal block has keys after its queries
-            float t[16], bm = kNegInf;
+            // the max is taken on the raw scores (the scale is positive) and
+            // the scale folded into one fma per score
+            float bm = kNegInf;
             if (kb == qb0 + b) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    t[v] = out_row(v, half) <= l32 ? acc[v] * scale_log2e : kNegInf;
-                    bm = fmaxf(bm, t[v]);
+                    if (out_row(v, half) > l32) acc[v] = kNegInf;
+                    bm = fmaxf(bm, acc[v]);
                 }
             } else {
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    t[v] = acc[v] * scale_log2e;
-                    bm = fmaxf(bm, t[v]);
-                }
+                for (int v = 0; v < 16; ++v) bm = fmaxf(bm, acc[v]);
             }
-            const float mn = fmaxf(m[b], bm);
+            const float mn = fmaxf(m[b], bm * scale_log2e);
             if (mn == kNegInf) continue;  // no key of this half seen yet
             float sum = 0.0f;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(t[v] - mn);
+            for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -mn));
             l[b] = l[b] * __builtin_amdgcn_exp2f(m[b] - mn) + sum;
             m[b] = mn;
         }
