@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
     ap.add_argument("--encode", choices=("fused", "two-pass"), default="fused",
                     help="RoPE + LSH of the target in one kernel, or rope_embed then lsh_encode")
+    ap.add_argument("--gather", choices=("except", "all"), default="except",
+                    help="layers after the first gather after the selection, skipping the recomputed rows (except), "
+                         "or every layer and row before it (all)")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
     ap.add_argument("--dynamic-recompute", action="store_true",
@@ -84,6 +87,7 @@ class Path:
         self.torch, self.ss, self.cfg = torch, ss, cfg
         self.matcher = ss.match_mfma
         self.fused_encode = True
+        self.gather_except = True
         dev = "cuda"
         bf = torch.bfloat16
         T, d, L = cfg.n_tok, cfg.dim, cfg.n_layers
@@ -165,7 +169,10 @@ class Path:
             m("lsh")
         self.matcher(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
         m("match")
-        ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
+        if self.gather_except:  # layer 0 now; layers 1.. after the selection, without the recomputed rows
+            ss.gather_kv(self.ref_k[:1], self.ref_v[:1], self.idx, out_k=self.asm_k[:1], out_v=self.asm_v[:1])
+        else:
+            ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
         m("gather")
         wq, wk, wv = self.w[0]
         ss.qkv_rope(self.e_tgt, self.allpos, wq, wk, wv, self.asm_k[0], self.asm_v[0], hq, hkv, q_out=self.q_full,
@@ -178,6 +185,10 @@ class Path:
         ss.attention_plan(self.sel, self.T, hq, hkv, self.D, out=self.plan)
         ss.rope_table(self.sel, self.T, self.D, out=self.rope_sel)
         m("select")
+        if self.gather_except:
+            ss.gather_kv(self.ref_k[1:], self.ref_v[1:], self.idx, out_k=self.asm_k[1:], out_v=self.asm_v[1:],
+                         except_pos=self.sel)
+            m("gather_rest")
         ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
         m("xsel")
         for l in range(1, self.L):
@@ -478,6 +489,7 @@ def main():
     path = Path(torch, ss, cfg)
     path.matcher = ss.match_mfma if args.matcher == "mfma" else ss.match
     path.fused_encode = args.encode == "fused"
+    path.gather_except = args.gather == "except"
 
     if args.copy_calibration_mib:
         # fill the source, then a 1 GiB buffer that pushes it out of L2 and the
@@ -507,8 +519,9 @@ def main():
     attn0_flops = 4.0 * D * hq * T * (T + 1) / 2.0
     qkv_flops = 2.0 * n_sel * (hq + 2 * hkv) * D * d
     attn_ms, qkv_ms, attn0_ms = avg("attn"), avg("qkv"), avg("attn0")
-    gather_bytes = 2.0 * 2 * L * T * hkv * D * 2  # read + write, K and V
-    gather_ms = avg("gather")
+    gather_rows = T + (L - 1) * (T - n_sel) if args.gather == "except" else L * T
+    gather_bytes = 2.0 * 2 * gather_rows * hkv * D * 2  # read + write, K and V
+    gather_ms = avg("gather") + (avg("gather_rest") if "gather_rest" in stages else 0.0)
     match_ms = avg("match")
     pp_ms = (avg("qkv0") + attn0_ms + (L - 1) * (attn_ms + qkv_ms))
     # the dominant call: prefill_attention (attention kernel + combine of cut row tiles),
@@ -539,7 +552,7 @@ def main():
         "config": {"workload": f"5120-token target vs 5120-token cached reference, 32 Llama-3-8B-shaped attention "
                                f"layers (hidden 4096, 32q/8kv heads, head_dim 128), 128-bit LSH, recompute "
                                f"fraction {args.frac}", "n_tok": T, "layers": L, "recompute_frac": args.frac,
-                   "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode},
+                   "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode, "gather": args.gather},
         "partial_prefill_tokens_per_s": T / (pp_ms * 1e-3),
         "match_token_pairs_per_s": T * T / (match_ms * 1e-3),
         "stage_ms": {k: round(sum(v) / len(v), 4) for k, v in stages.items()},

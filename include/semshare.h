@@ -143,6 +143,20 @@ semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const
                                      semshare_dtype_t dtype, void* stream);
 
 /*
+ * semshare_gather_kv for every target row except those listed: the rows
+ * except_pos[0 .. n_except) (ascending target positions) of every layer are
+ * left as they are.  Once the recompute set is known (Section 4.3.3), the
+ * layers after the first need not copy the rows their partial prefill
+ * overwrites.  Arguments and errors as semshare_gather_kv; 0 <= n_except <=
+ * n_tgt, except_pos sorted ascending (device), may be NULL when n_except = 0.
+ */
+semshare_status_t semshare_gather_kv_except(const void* ref_k, const void* ref_v, const int32_t* idx,
+                                            int64_t n_tgt, int64_t n_ref, void* out_k, void* out_v,
+                                            int32_t n_layers, int32_t n_kv_heads, int32_t head_dim,
+                                            semshare_dtype_t dtype, const int32_t* except_pos,
+                                            int64_t n_except, void* stream);
+
+/*
  * One attention layer of partial prefill (Sections 4.2 and 4.3.3): only the
  * selected tokens are recomputed, against the assembled (rearranged) cache.
  *  1. q = RoPE_p(x Wq^T), k = RoPE_p(x Wk^T) per head and v = x Wv^T for

@@ -235,6 +235,31 @@ semshare_status_t semshare_gather_kv(const void* ref_k, const void* ref_v, const
                     "gather_kv launch");
 }
 
+semshare_status_t semshare_gather_kv_except(const void* ref_k, const void* ref_v, const int32_t* idx,
+                                     int64_t n_tgt, int64_t n_ref, void* out_k, void* out_v,
+                                     int32_t n_layers, int32_t n_kv_heads, int32_t head_dim,
+                                     semshare_dtype_t dtype, const int32_t* except_pos,
+                                            int64_t n_except, void* stream) {
+    if (n_except < 0 || n_except > n_tgt || (n_except > 0 && !except_pos))
+        return fail(SEMSHARE_E_INVAL, "gather_kv_except: n_except must lie in [0, n_tgt] with a list");
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "gather_kv_except: unknown dtype %d", dtype);
+    if (n_tgt < 0 || n_ref < 0 || n_layers < 0) return fail(SEMSHARE_E_INVAL, "gather_kv_except: negative size");
+    if (n_kv_heads <= 0 || head_dim <= 0) return fail(SEMSHARE_E_INVAL, "gather_kv_except: n_kv_heads and head_dim must be > 0");
+    if ((ref_v == nullptr) != (out_v == nullptr))
+        return fail(SEMSHARE_E_INVAL, "gather_kv_except: ref_v and out_v must both be set or both be NULL");
+    const int64_t row_bytes = (int64_t)n_kv_heads * head_dim * (int64_t)dtype_size(dtype);
+    if (row_bytes % 16) return fail(SEMSHARE_E_UNSUPPORTED, "gather_kv_except: row size %lld bytes is not a multiple of 16", (long long)row_bytes);
+    if ((int64_t)n_layers * n_tgt > (int64_t(1) << 30) || n_ref > (int64_t(1) << 31) - 1)
+        return fail(SEMSHARE_E_UNSUPPORTED, "gather_kv_except: too many rows");
+    if (n_tgt == 0 || n_layers == 0) return ok();
+    if (!ref_k || !out_k || !idx) return fail(SEMSHARE_E_INVAL, "gather_kv_except: null buffer");
+    if (!aligned16(ref_k) || !aligned16(out_k) || (ref_v && (!aligned16(ref_v) || !aligned16(out_v))))
+        return fail(SEMSHARE_E_INVAL, "gather_kv_except: buffers must be 16-byte aligned");
+    return from_hip(semshare::launch_gather_rows(ref_k, ref_v, idx, n_tgt, n_ref, out_k, out_v, n_layers, row_bytes,
+                                                 (hipStream_t)stream, except_pos, n_except),
+                    "gather_kv_except launch");
+}
+
 }  // extern "C"
 
 namespace {

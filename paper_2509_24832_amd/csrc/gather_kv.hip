@@ -7,7 +7,9 @@
 // through the caches: a source row the index repeats is then read from them
 // (32 layers x 5120 rows with a uniformly random index, 63% distinct: 185 us
 // against 230 us with non-temporal loads; the same time with no repeats).  Rows whose index
-// lies outside [0, n_ref) are written as zeros and never read.
+// lies outside [0, n_ref) are written as zeros and never read.  The variant
+// with an exception list leaves the listed target rows untouched (the rows a
+// partial prefill recomputes and overwrites anyway).
 #include "semshare_internal.h"
 
 namespace semshare {
@@ -25,7 +27,9 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4* __restric
                                                           u32x4* __restrict__ dst_a,
                                                           u32x4* __restrict__ dst_b,
                                                           uint32_t rows_per_tensor,
-                                                          uint32_t rows_total, uint32_t cpr) {
+                                                          uint32_t rows_total, uint32_t cpr,
+                                                          const int32_t* __restrict__ except_pos,
+                                                          uint32_t n_except) {
     const int lane = threadIdx.x & 63;
     const uint32_t wave = blockIdx.x * 4u + (threadIdx.x >> 6);
     const uint32_t row0 = wave * kRowsPerWave;
@@ -43,6 +47,14 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4* __restric
         const uint32_t rem = second ? r - rows_per_tensor : r;
         const uint32_t l = rem / n_tgt, t = rem - l * n_tgt;
         const int32_t j = idx[t];
+        if (n_except) {  // target rows listed (ascending) in except_pos are left as they are
+            uint32_t lo = 0, hi = n_except;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if ((uint32_t)except_pos[mid] < t) lo = mid + 1; else hi = mid;
+            }
+            if (lo < n_except && (uint32_t)except_pos[lo] == t) live[u] = false;
+        }
         readable[u] = j >= 0 && (uint32_t)j < n_ref;
         const uint32_t jj = readable[u] ? (uint32_t)j : 0u;
         src[u] = (second ? src_b : src_a) + ((size_t)l * n_ref + jj) * cpr;
@@ -74,7 +86,8 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const u32x4* __restric
 
 hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_t* idx,
                               int64_t n_tgt, int64_t n_ref, void* dst_a, void* dst_b,
-                              int32_t n_layers, int64_t row_bytes, hipStream_t s) {
+                              int32_t n_layers, int64_t row_bytes, hipStream_t s,
+                              const int32_t* except_pos, int64_t n_except) {
     const int64_t rows_per_tensor = (int64_t)n_layers * n_tgt;
     const int64_t rows_total = rows_per_tensor * (src_b ? 2 : 1);
     const int64_t waves = (rows_total + kRowsPerWave - 1) / kRowsPerWave;
@@ -83,7 +96,7 @@ hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_
                        static_cast<const u32x4*>(src_a), static_cast<const u32x4*>(src_b), idx,
                        (uint32_t)n_tgt, (uint32_t)n_ref, static_cast<u32x4*>(dst_a),
                        static_cast<u32x4*>(dst_b), (uint32_t)rows_per_tensor, (uint32_t)rows_total,
-                       (uint32_t)(row_bytes / 16));
+                       (uint32_t)(row_bytes / 16), except_pos, (uint32_t)n_except);
     return hipGetLastError();
 }
 

@@ -93,7 +93,8 @@ hipError_t launch_match_mfma(const uint64_t* tgt, int64_t n_tgt, const uint64_t*
 
 hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_t* idx,
                               int64_t n_tgt, int64_t n_ref, void* dst_a, void* dst_b,
-                              int32_t n_layers, int64_t row_bytes, hipStream_t s);
+                              int32_t n_layers, int64_t row_bytes, hipStream_t s,
+                              const int32_t* except_pos = nullptr, int64_t n_except = 0);
 
 hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
                                    int32_t* sel_pos, hipStream_t s);

@@ -57,6 +57,7 @@ def load() -> ctypes.CDLL:
         "semshare_match": (I32, [P, I64, P, I64, I32, P, P, P]),
         "semshare_match_mfma": (I32, [P, I64, P, I64, I32, P, P, P]),
         "semshare_gather_kv": (I32, [P, P, P, I64, I64, P, P, I32, I32, I32, I32, P]),
+        "semshare_gather_kv_except": (I32, [P, P, P, I64, I64, P, P, I32, I32, I32, I32, P, I64, P]),
         "semshare_partial_prefill": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, F32,
                                            P, P, P, SZ, I32, P]),
         "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
@@ -265,8 +266,10 @@ def match_mfma(tgt_codes: torch.Tensor, ref_codes: torch.Tensor, idx: Optional[t
 
 
 def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Tensor,
-              out_k: Optional[torch.Tensor] = None, out_v: Optional[torch.Tensor] = None):
-    """out[l][t] = ref[l][idx[t]]; ref_* [L, n_ref, Hkv, D] -> out_* [L, n_tgt, Hkv, D]."""
+              out_k: Optional[torch.Tensor] = None, out_v: Optional[torch.Tensor] = None,
+              except_pos: Optional[torch.Tensor] = None, n_except: Optional[int] = None):
+    """out[l][t] = ref[l][idx[t]]; ref_* [L, n_ref, Hkv, D] -> out_* [L, n_tgt, Hkv, D].  With except_pos
+    (ascending int32 target rows; the first n_except of it) those rows are left as they are."""
     _dev(ref_k, "ref_k")
     _dev(idx, "idx", torch.int32)
     if ref_k.dim() != 4:
@@ -288,8 +291,14 @@ def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Ten
         out_v = None
     if tuple(out_k.shape) != shape or (out_v is not None and tuple(out_v.shape) != shape):
         raise ValueError("output shape mismatch")
-    _call("semshare_gather_kv", _ptr(ref_k), _ptr(ref_v), _ptr(idx), n_tgt, n_ref, _ptr(out_k), _ptr(out_v), L,
-          hkv, d, _dt(ref_k), _stream())
+    if except_pos is None:
+        _call("semshare_gather_kv", _ptr(ref_k), _ptr(ref_v), _ptr(idx), n_tgt, n_ref, _ptr(out_k), _ptr(out_v), L,
+              hkv, d, _dt(ref_k), _stream())
+    else:
+        _dev(except_pos, "except_pos", torch.int32)
+        ne = except_pos.shape[0] if n_except is None else int(n_except)
+        _call("semshare_gather_kv_except", _ptr(ref_k), _ptr(ref_v), _ptr(idx), n_tgt, n_ref, _ptr(out_k),
+              _ptr(out_v), L, hkv, d, _dt(ref_k), _ptr(except_pos), ne, _stream())
     return out_k, out_v
 
 

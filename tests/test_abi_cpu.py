@@ -118,6 +118,14 @@ def test_match_validation(lib, entry):
     assert _st(entry, None, 0, None, 4, 2, None, None, None) == b.OK
 
 
+def test_gather_except_validation(lib):
+    e = "semshare_gather_kv_except"
+    assert _st(e, FAKE, None, FAKE, 4, 4, FAKE, None, 2, 8, 128, 1, None, 1, None) == b.E_INVAL  # list missing
+    assert _st(e, FAKE, None, FAKE, 4, 4, FAKE, None, 2, 8, 128, 1, FAKE, 5, None) == b.E_INVAL  # n_except > n_tgt
+    assert _st(e, FAKE, None, FAKE, 4, 4, FAKE, None, 2, 8, 128, 1, FAKE, -1, None) == b.E_INVAL
+    assert _st(e, FAKE, None, FAKE, 0, 4, FAKE, None, 2, 8, 128, 1, None, 0, None) == b.OK
+
+
 def test_gather_validation(lib):
     args = dict(n_tgt=4, n_ref=4, L=2, h=8, d=128, dt=1)
     assert _st("semshare_gather_kv", FAKE, FAKE, FAKE, 4, 4, FAKE, None, 2, 8, 128, 1, None) == b.E_INVAL  # v pair

@@ -237,6 +237,25 @@ def test_gather_kv_bitwise(cid, L, n_ref, n_tgt):
     assert np.array_equal(host(ov), orc.gather_rows(v, idx))
 
 
+@pytest.mark.parametrize("n_except", [0, 1, 250, 1000])
+def test_gather_except_leaves_listed_rows(n_except):
+    cfg = CONFIGS[1]
+    L, n_ref, n_tgt = 3, 777, 1000
+    announce(f"gather except n_except={n_except}")
+    k, v = workloads.make_cache(cfg, L, n_ref, tag=9)
+    idx = np.random.default_rng(9).integers(0, n_ref, n_tgt).astype(np.int32)
+    exc = np.sort(np.random.default_rng(10).choice(n_tgt, n_except, replace=False)).astype(np.int32)
+    ok = torch.full((L, n_tgt) + k.shape[2:], 7.0, dtype=torch.bfloat16, device="cuda")
+    ov = torch.full((L, n_tgt) + k.shape[2:], -3.0, dtype=torch.bfloat16, device="cuda")
+    ss.gather_kv(dev(k, "bf16"), dev(v, "bf16"), dev_i32(idx), out_k=ok, out_v=ov, except_pos=dev_i32(exc))
+    gk, gv = host(ok), host(ov)
+    keep = np.ones(n_tgt, bool)
+    keep[exc] = False
+    assert np.array_equal(gk[:, keep], orc.gather_rows(k, idx)[:, keep])
+    assert np.array_equal(gv[:, keep], orc.gather_rows(v, idx)[:, keep])
+    assert (gk[:, ~keep] == 7.0).all() and (gv[:, ~keep] == -3.0).all()
+
+
 def test_gather_identity_k_only_and_out_of_range():
     cfg = CONFIGS[1]
     k, _ = workloads.make_cache(cfg, 2, 64, tag=5)
