@@ -15,6 +15,7 @@ from __future__ import annotations
 import ctypes
 import os
 import subprocess
+from fractions import Fraction
 from typing import Optional, Tuple
 
 import numpy as np
@@ -273,42 +274,52 @@ def attention_mass(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, s
     return total / (n_q_heads * (T - row_begin))
 
 
-def _mass_fixed(m32: np.ndarray) -> np.ndarray:
-    """Masses clamped to [0, 1] in 2^-40 fixed point (int64): sums of these are
-    exact, so the threshold decision does not depend on summation order."""
-    c = np.clip(m32.astype(np.float64), 0.0, 1.0)
-    return np.floor(c * 2.0 ** 40).astype(np.int64)
+def _exact_units(m32: np.ndarray) -> list:
+    """Every fp32 value is an integer multiple of 2^-149 (the smallest
+    subnormal); these integers make every sum of masses exact."""
+    out = []
+    for v in m32.tolist():
+        num, den = float(v).as_integer_ratio()
+        out.append(num * ((1 << 149) // den))
+    return out
 
 
 def attention_recovery(mass, thres: float = 0.55) -> Tuple[int, np.ndarray]:
     """Attention Recovery (Section 3, Insight 2 equation): the tokens ordered by
     mass, largest first (lower position first on ties); AR is the smallest k >= 1
-    whose top-k mass reaches thres of the total (compared in fp64 on 2^-40
-    fixed-point sums).  Returns (AR, order)."""
+    whose top-k mass reaches thres of the total.  The sums and the comparison
+    are exact (integers in units of 2^-149 and the exact rational value of
+    thres), so the answer is the plain definition on the given fp32 masses.
+    Masses must be finite and in [0, 1] (averages of probabilities).
+    Returns (AR, order)."""
     m32 = np.asarray(mass, dtype=np.float32)
     n = m32.shape[0]
     if n == 0:
         return 0, np.zeros(0, dtype=np.int64)
-    key = np.clip(m32, np.float32(0), np.float32(1))
-    order = np.array(sorted(range(n), key=lambda j: (-float(key[j]), j)), dtype=np.int64)
-    fx = _mass_fixed(m32)
-    total = int(fx.sum())
-    target = thres * float(total)
+    if not np.all(np.isfinite(m32)) or np.any(m32 < 0) or np.any(m32 > 1):
+        raise ValueError("masses must be finite and lie in [0, 1]")
+    order = np.array(sorted(range(n), key=lambda j: (-float(m32[j]), j)), dtype=np.int64)
+    units = _exact_units(m32)
+    p, q = Fraction(thres).as_integer_ratio()
+    total = sum(units)
     run = 0
-    for k, j in enumerate(order, start=1):
-        run += int(fx[j])
-        if float(run) >= target:
+    for k, j in enumerate(order.tolist(), start=1):
+        run += units[j]
+        if run * q >= p * total:  # run >= thres * total, exactly
             return k, order
     return n, order
 
 
 def dynamic_recompute(mass, sigma, thres: float = 0.55, w_hot: float = 0.5,
-                      w_cold: float = 0.1) -> Tuple[int, np.ndarray, int]:
+                      w_cold: float = 0.1, ar: Optional[int] = None) -> Tuple[int, np.ndarray, int]:
     """Dynamic recompute set (Section 4.3.3): the AR first tokens by mass are
     hot, the rest cold; floor(w_hot AR + 1/2) hot and floor(w_cold (T - AR) + 1/2)
     cold tokens with the largest deviation (lower position first on ties) are
-    recomputed.  Returns (AR, selected positions ascending, hot count chosen)."""
-    ar, order = attention_recovery(mass, thres)
+    recomputed.  ``ar`` replaces the computed AR (to follow another valid
+    reading of a tie at the threshold).  Returns (AR, selected positions
+    ascending, hot count chosen)."""
+    ar_exact, order = attention_recovery(mass, thres)
+    ar = ar_exact if ar is None else int(ar)
     n = len(order)
     sig = np.maximum(np.asarray(sigma, dtype=np.float32), np.float32(0))
     hot = set(int(j) for j in order[:ar])

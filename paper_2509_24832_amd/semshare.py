@@ -269,7 +269,8 @@ def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Ten
               out_k: Optional[torch.Tensor] = None, out_v: Optional[torch.Tensor] = None,
               except_pos: Optional[torch.Tensor] = None, n_except: Optional[int] = None):
     """out[l][t] = ref[l][idx[t]]; ref_* [L, n_ref, Hkv, D] -> out_* [L, n_tgt, Hkv, D].  With except_pos
-    (ascending int32 target rows; the first n_except of it) those rows are left as they are."""
+    (strictly ascending int32 target rows; the first n_except of it, 0 <= n_except <= except_pos.numel())
+    those rows are left as they are."""
     _dev(ref_k, "ref_k")
     _dev(idx, "idx", torch.int32)
     if ref_k.dim() != 4:
@@ -297,6 +298,8 @@ def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Ten
     else:
         _dev(except_pos, "except_pos", torch.int32)
         ne = except_pos.shape[0] if n_except is None else int(n_except)
+        if except_pos.dim() != 1 or not 0 <= ne <= except_pos.numel():
+            raise ValueError(f"n_except must lie in [0, {except_pos.numel()}] (got {ne})")
         _call("semshare_gather_kv_except", _ptr(ref_k), _ptr(ref_v), _ptr(idx), n_tgt, n_ref, _ptr(out_k),
               _ptr(out_v), L, hkv, d, _dt(ref_k), _ptr(except_pos), ne, _stream())
     return out_k, out_v

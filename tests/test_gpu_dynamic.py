@@ -61,7 +61,35 @@ def _dyn_inputs(T, seed, ties):
     else:
         m = (r.exponential(size=T) / T).astype(np.float32)
         s = r.exponential(size=T).astype(np.float32)
-    return m, s
+    return np.minimum(m, np.float32(1.0)), s
+
+
+def _ar_valid(m32, ar_gpu, thres=0.55):
+    """The kernel sums masses in 2^-40 fixed point and forms thres * total in
+    fp64, so its AR can differ from the exact one only where the exact top-k
+    sum S_k lies within eps = n 2^-40 + S 2^-53 of thres * S.  True when ar_gpu
+    is the exact AR or such a neighbour: S_ar >= thres S - eps and
+    S_(ar-1) <= thres S + eps."""
+    from fractions import Fraction
+    vals = [Fraction(float(v)) for v in np.asarray(m32, np.float32)]
+    n = len(vals)
+    order = sorted(range(n), key=lambda j: (-vals[j], j))
+    total = sum(vals)
+    eps = Fraction(n, 2 ** 40) + total / 2 ** 53
+    goal = Fraction(thres) * total
+    s_prev = sum(vals[j] for j in order[:ar_gpu - 1])
+    s_ar = s_prev + vals[order[ar_gpu - 1]]
+    return 1 <= ar_gpu <= n and s_ar >= goal - eps and (ar_gpu == 1 or s_prev <= goal + eps)
+
+
+def _oracle_dyn(m, s, ar_gpu, **kw):
+    """The oracle's recompute set; where the GPU's AR is a valid neighbour of
+    the exact one (see _ar_valid), the oracle continues from the GPU's AR."""
+    ar, sel, n_hot = orc.dynamic_recompute(m, s, **kw)
+    if ar_gpu != ar:
+        assert _ar_valid(m, ar_gpu, kw.get("thres", 0.55)), (ar_gpu, ar)
+        ar, sel, n_hot = orc.dynamic_recompute(m, s, ar=ar_gpu, **kw)
+    return ar, sel, n_hot
 
 
 @pytest.mark.parametrize("T,seed,ties", [(1, 0, False), (7, 1, False), (100, 2, True), (1000, 3, False),
@@ -71,7 +99,7 @@ def test_dynamic_recompute_matches_oracle(T, seed, ties):
     m, s = _dyn_inputs(T, seed, ties)
     sel, counts = ss.dynamic_recompute(torch.from_numpy(m).cuda(), torch.from_numpy(s).cuda())
     c = counts.cpu().numpy()
-    ar, ref_sel, n_hot = orc.dynamic_recompute(m, s)
+    ar, ref_sel, n_hot = _oracle_dyn(m, s, int(c[0]))
     assert c[0] == ar and c[2] == n_hot and c[1] == len(ref_sel)
     assert np.array_equal(sel.cpu().numpy()[: c[1]], ref_sel)
 
@@ -87,6 +115,20 @@ def test_dynamic_recompute_weights_and_empty():
     e = torch.empty(0, dtype=torch.float32, device="cuda")
     _, counts = ss.dynamic_recompute(e, e)
     assert counts.cpu().numpy().tolist() == [0, 0, 0]
+
+
+def test_dynamic_recompute_ar_within_the_fixed_point_band():
+    # [1/4] * 4 + [2^-60] at thres 1/2: the exact AR is 3 (the total exceeds 1
+    # by 2^-60), a 2^-40 fixed point sees 2; both are within the kernel's band
+    m = np.array([0.25] * 4 + [2.0 ** -60], np.float32)
+    s = np.arange(5, dtype=np.float32)
+    announce("dynamic recompute: AR tie inside the fixed-point band")
+    sel, counts = ss.dynamic_recompute(torch.from_numpy(m).cuda(), torch.from_numpy(s).cuda(), thres=0.5)
+    c = counts.cpu().numpy()
+    assert orc.attention_recovery(m, 0.5)[0] == 3
+    assert c[0] in (2, 3) and _ar_valid(m, int(c[0]), 0.5)
+    ar, ref_sel, n_hot = _oracle_dyn(m, s, int(c[0]), thres=0.5)
+    assert c[1] == len(ref_sel) and np.array_equal(sel.cpu().numpy()[: c[1]], ref_sel)
 
 
 @pytest.mark.parametrize("T,row_begin", [(300, 137), (1024, 900), (64, 63)])
@@ -108,7 +150,7 @@ def test_retention_matches_oracle(T, seed, ties, min_keep):
     mt, st, sct = (torch.from_numpy(a).cuda() for a in (m, s, score))
     sel, counts = ss.dynamic_recompute(mt, st)          # the GPU's own selection feeds the GPU retention
     rank, kept, n_kept = ss.retention(mt, sct, sel, counts, min_keep)
-    ar, ref_sel, _ = orc.dynamic_recompute(m, s)        # the oracle's own selection feeds the oracle
+    ar, ref_sel, _ = _oracle_dyn(m, s, int(counts.cpu().numpy()[0]))  # the oracle's selection feeds the oracle
     ref_rank, ref_kept, ref_keep = orc.retention(m, score, ar, ref_sel, min_keep)
     nk = int(n_kept.cpu().numpy()[0])
     assert nk == ref_keep

@@ -1,8 +1,6 @@
 """Oracle pins for the average attention score per token, Attention Recovery
 and the dynamic recompute set (Section 3 Insight 2 and its AR equation;
 Section 4.3.3).  CPU only."""
-from fractions import Fraction
-
 import numpy as np
 import pytest
 
@@ -53,32 +51,55 @@ def test_mass_gqa_equals_mha_with_repeated_kv():
     assert np.allclose(m_gqa, m_mha, rtol=0, atol=1e-15)
 
 
-def _ar_exact(m32, thres):
-    # exact rationals on the fp32 values (no fixed point): smallest k reaching thres
-    vals = [Fraction(float(min(max(x, 0.0), 1.0))) for x in m32]
-    order = sorted(range(len(vals)), key=lambda j: (-vals[j], j))
-    total = sum(vals)
-    run = Fraction(0)
-    for n, j in enumerate(order, start=1):
-        run += vals[j]
-        if run >= Fraction(thres) * total:
-            return n
-    return len(vals)
+def test_attention_recovery_is_exact_below_any_fixed_point():
+    # the top-k sum is compared with thres * total exactly: a difference of
+    # 2^-60 (or one fp32 subnormal, 2^-149) decides, which neither fp64 sums
+    # nor a 2^-40 fixed point can see
+    q = np.float32(0.25)
+    assert orc.attention_recovery(np.array([q, q, q, q], np.float32), 0.5)[0] == 2  # equality reaches
+    for tiny in (2.0 ** -60, 2.0 ** -149):
+        m = np.array([q, q, q, q, tiny], np.float32)
+        assert float(m[4]) == tiny
+        # total = 1 + tiny, half of it exceeds the top-2 sum 0.5 by tiny / 2
+        assert orc.attention_recovery(m, 0.5)[0] == 3
+    # thres 0.75 of [0.5, 0.25, 0.25 - 2^-30]: top-2 = 0.75 >= 0.75 (1 - 2^-32)
+    m = np.array([0.5, 0.25, 0.25 - 2.0 ** -30], np.float32)
+    assert orc.attention_recovery(m, 0.75)[0] == 2
 
 
-@pytest.mark.parametrize("seed", range(6))
-def test_attention_recovery_equals_exact_rationals(seed):
-    r = _rng(100 + seed)
-    n = int(r.integers(1, 60))
-    m = (r.exponential(size=n) / n).astype(np.float32)
+@pytest.mark.parametrize("T,seed", [(57, 0), (5120, 1), (8192, 2)])
+def test_attention_recovery_property_by_correctly_rounded_sums(T, seed):
+    # AR is the first k whose top-k mass reaches thres of the total: checked with
+    # math.fsum (correctly rounded) sums where the margin exceeds their rounding
+    import math
+    r = _rng(200 + seed)
+    m = (r.exponential(size=T) / T).astype(np.float32)
+    m = np.minimum(m, np.float32(1.0))
     ar, order = orc.attention_recovery(m, 0.55)
-    assert ar == _ar_exact(m, 0.55)
-    assert sorted(order.tolist()) == list(range(n))
+    vals = m.astype(np.float64)
+    assert sorted(order.tolist()) == list(range(T))
+    assert all(vals[order[i]] >= vals[order[i + 1]] for i in range(T - 1))
+    total = math.fsum(vals)
+    s_ar = math.fsum(vals[order[:ar]])
+    s_prev = math.fsum(vals[order[:ar - 1]])
+    eps = 4 * T * 2.0 ** -53 * total
+    assert s_ar >= 0.55 * total - eps and s_prev < 0.55 * total + eps
+    assert s_ar - 0.55 * total > -eps and (ar == 1 or 0.55 * total - s_prev > -eps)
+
+
+def test_attention_recovery_rejects_masses_outside_unit_interval():
+    for bad in ([0.5, -0.1], [1.5], [np.nan], [np.inf]):
+        with pytest.raises(ValueError):
+            orc.attention_recovery(np.array(bad, np.float32))
 
 
 def test_attention_recovery_closed_forms():
     assert orc.attention_recovery(np.full(10, 0.1, np.float32), 0.55)[0] == 6  # ceil(0.55 * 10)
-    assert orc.attention_recovery(np.full(200, 0.005, np.float32), 0.55)[0] == 110
+    assert orc.attention_recovery(np.full(201, 0.004, np.float32), 0.55)[0] == 111  # ceil(110.55)
+    # thres is the exact value of its double: fl(0.55) exceeds 55/100, so 200
+    # equal masses need 111 tokens (0.55 * 200 is 110 plus 8.9e-15)
+    assert orc.attention_recovery(np.full(200, 0.005, np.float32), 0.55)[0] == 111
+    assert orc.attention_recovery(np.full(200, 0.005, np.float32), 0.5)[0] == 100  # exact binary fraction
     one = np.full(50, 0.001, np.float32); one[31] = 0.9
     ar, order = orc.attention_recovery(one, 0.55)
     assert ar == 1 and order[0] == 31
@@ -89,19 +110,21 @@ def test_attention_recovery_closed_forms():
 
 
 def test_dynamic_recompute_counts_and_ties():
-    n = 40
-    m = np.full(n, 1.0 / n, np.float32)           # AR = 22: positions 0..21 hot
+    n = 42
+    m = np.full(n, 1.0 / n, np.float32)           # AR = ceil(0.55 * 42) = 24: positions 0..23 hot
     sig = np.ones(n, np.float32)                  # all equal: the lowest positions of each group
     ar, sel, n_hot = orc.dynamic_recompute(m, sig, 0.55, 0.5, 0.1)
-    assert ar == 22 and n_hot == 11
-    assert sel.tolist() == list(range(11)) + [22, 23]  # floor(0.1 * 18 + 1/2) = 2 cold
+    assert ar == 24 and n_hot == 12
+    assert sel.tolist() == list(range(12)) + [24, 25]  # floor(0.1 * 18 + 1/2) = 2 cold
     # the deviation decides within each group
     sig2 = np.arange(n, dtype=np.float32)
     _, sel2, _ = orc.dynamic_recompute(m, sig2, 0.55, 0.5, 0.1)
-    assert sel2.tolist() == list(range(11, 22)) + [38, 39]
+    assert sel2.tolist() == list(range(12, 24)) + [40, 41]
     # w = 1 recomputes everything, w = 0 nothing
     assert orc.dynamic_recompute(m, sig2, 0.55, 1.0, 1.0)[1].tolist() == list(range(n))
     assert orc.dynamic_recompute(m, sig2, 0.55, 0.0, 0.0)[1].size == 0
+    # an AR given by the caller replaces the computed one
+    assert orc.dynamic_recompute(m, sig2, 0.55, 0.5, 0.1, ar=10)[0] == 10
 
 
 def test_window_mass_last_row_is_its_softmax():
