@@ -40,7 +40,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--frac", type=float, default=0.25, help="recompute fraction of the headline line")
-    ap.add_argument("--sweep", default="0.10,0.25,0.50", help="recompute fractions also timed ('' to skip)")
+    ap.add_argument("--sweep", default="0.10,0.25,0.50,1.00",
+                    help="recompute fractions also timed ('' to skip); 1.00 is the full-prefill analogue")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
     ap.add_argument("--encode", choices=("fused", "two-pass"), default="fused",
@@ -280,7 +281,8 @@ def cpu_baseline(cfg, frac, budget_s):
     per_key_attn = (time.perf_counter() - t) / float((sel[rows] + 1).sum())
     est["qkv0"] = per_row_qkv * T
     est["attn0"] = per_key_attn * T * (T + 1) / 2
-    est["select"] = 0.0
+    sigma = rng.exponential(size=T)
+    t = time.perf_counter(); orc.select_recompute(sigma, n_sel); est["select"] = time.perf_counter() - t
     est["qkv"] = per_row_qkv * n_sel * (L - 1)
     est["attn"] = per_key_attn * float((sel + 1).sum()) * (L - 1)
     total = sum(est.values())
@@ -572,7 +574,8 @@ def main():
         for f in [float(x) for x in args.sweep.split(",") if x]:
             path.set_frac(f)
             m_f, _, _ = time_steps(torch, path, max(3, args.steps // 2), 2, instrument=False)
-            sweep[f"{f:.2f}"] = {"ms_per_step": m_f, "tokens_per_s": T / (m_f * 1e-3)}
+            sweep[f"{f:.2f}"] = {"ms_per_step": m_f, "tokens_per_s": T / (m_f * 1e-3), "n_recompute": path.n_sel,
+                                 "recomputed_tokens_per_s": (T + (L - 1) * path.n_sel) / (m_f * 1e-3)}
         res["recompute_sweep"] = sweep
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, args.frac, args.cpu_budget_s)

@@ -62,6 +62,7 @@ def _load() -> ctypes.CDLL:
         "orc_partial_prefill": (None, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, F64,
                                        P, P, INT]),
         "orc_select_recompute": (None, [P, I64, I64, P]),
+        "orc_attention_mass": (None, [P, P, I64, I32, I32, I32, F64, I64, P, I64, P]),
         "orc_similarity": (F64, [P, I64, F64, F64]),
         "orc_bank_similarity": (None, [P, I64, P, P, INT, INT, F64, F64, P, P]),
         "orc_num_threads": (INT, []),
@@ -272,6 +273,26 @@ def attention_mass(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, s
         p /= p.sum(axis=1, keepdims=True)
         total += p[row_begin:].sum(axis=0)
     return total / (n_q_heads * (T - row_begin))
+
+
+def attention_mass_cols(q, k_cache, n_q_heads: int, n_kv_heads: int, head_dim: int, sm_scale: float = 0.0,
+                        row_begin: int = 0, cols=None) -> np.ndarray:
+    """attention_mass (same definition, plain C loops in fp64) for the key
+    columns ``cols`` only (all keys when None): every row's softmax
+    normaliser first, then the requested column sums."""
+    T = q.shape[0]
+    q = _f64(q).reshape(T, n_q_heads * head_dim)
+    k = _f64(k_cache).reshape(T, n_kv_heads * head_dim)
+    scale = sm_scale if sm_scale else 1.0 / np.sqrt(head_dim)
+    if not 0 <= row_begin < max(T, 1):
+        raise ValueError("row_begin must lie in [0, T)")
+    c = None if cols is None else np.ascontiguousarray(cols, dtype=np.int64)
+    if c is not None and c.size and (c.min() < 0 or c.max() >= T):
+        raise ValueError("column out of range")
+    out = np.empty(T if c is None else c.size)
+    _load().orc_attention_mass(_ptr(q), _ptr(k), T, n_q_heads, n_kv_heads, head_dim, float(scale), int(row_begin),
+                               _ptr(c), 0 if c is None else c.size, _ptr(out))
+    return out
 
 
 def _exact_units(m32: np.ndarray) -> list:

@@ -277,6 +277,7 @@ void orc_attention_rows(const double* q, const int32_t* sel_pos, int64_t n_sel,
         const int64_t s = rows ? rows[r] : r;
         const int64_t p = sel_pos[s];
         double* sc = (double*)malloc(sizeof(double) * (size_t)(p + 1));
+        double* acc = (double*)malloc(sizeof(double) * (size_t)head_dim);
         for (int32_t h = 0; h < n_q_heads; ++h) {
             const int32_t g = h / G;
             const double* qh = q + s * (int64_t)nq + (int64_t)h * head_dim;
@@ -290,16 +291,71 @@ void orc_attention_rows(const double* q, const int32_t* sel_pos, int64_t n_sel,
             }
             double den = 0.0;
             for (int64_t j = 0; j <= p; ++j) { sc[j] = exp(sc[j] - mx); den += sc[j]; }
+            /* every output element sums its products in ascending key order */
             double* o = out + s * (int64_t)nq + (int64_t)h * head_dim;
-            for (int32_t i = 0; i < head_dim; ++i) {
-                double acc = 0.0;
-                for (int64_t j = 0; j <= p; ++j)
-                    acc += sc[j] * v_cache[j * (int64_t)nkv + (int64_t)g * head_dim + i];
-                o[i] = orc_round(acc / den, dt);
+            for (int32_t i = 0; i < head_dim; ++i) acc[i] = 0.0;
+            for (int64_t j = 0; j <= p; ++j) {
+                const double* vj = v_cache + j * (int64_t)nkv + (int64_t)g * head_dim;
+                for (int32_t i = 0; i < head_dim; ++i) acc[i] += sc[j] * vj[i];
             }
+            for (int32_t i = 0; i < head_dim; ++i) o[i] = orc_round(acc[i] / den, dt);
+        }
+        free(sc);
+        free(acc);
+    }
+}
+
+/* Average attention score of every token at a fully computed layer (Section
+ * 3, Insight 2): P_h[i][j] is the causal softmax over keys j <= i of
+ * <q[i][h], k[j][h/G]> * scale, and mass[j] = sum_h sum_{i >= max(j, row_begin)}
+ * P_h[i][j] / (Hq (T - row_begin)).  Two passes: the normaliser
+ * (max and sum of exponentials) of every (row, head), then the column sums
+ * of the requested keys cols[0 .. n_cols) (all keys when cols == NULL;
+ * mass[c] belongs to cols[c]).  q is [T][Hq][D], k is [T][Hkv][D]. */
+void orc_attention_mass(const double* q, const double* k, int64_t T, int32_t n_q_heads, int32_t n_kv_heads,
+                        int32_t head_dim, double scale, int64_t row_begin, const int64_t* cols, int64_t n_cols,
+                        double* mass) {
+    const int32_t G = n_q_heads / n_kv_heads;
+    double* lse = (double*)malloc(sizeof(double) * (size_t)(T * n_q_heads));
+#pragma omp parallel
+    {
+        double* sc = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t r = 0; r < T * n_q_heads; ++r) {
+            const int64_t i = r / n_q_heads;
+            const int32_t h = (int32_t)(r % n_q_heads);
+            const double* qi = q + (i * n_q_heads + h) * (int64_t)head_dim;
+            double mx = -INFINITY, sum = 0.0;
+            for (int64_t j = 0; j <= i; ++j) {
+                const double* kj = k + (j * n_kv_heads + h / G) * (int64_t)head_dim;
+                double dot = 0.0;
+                for (int32_t d = 0; d < head_dim; ++d) dot += qi[d] * kj[d];
+                sc[j] = dot * scale;
+                if (sc[j] > mx) mx = sc[j];
+            }
+            for (int64_t j = 0; j <= i; ++j) sum += exp(sc[j] - mx);
+            lse[r] = mx + log(sum);
         }
         free(sc);
     }
+    const int64_t count = cols ? n_cols : T;
+    const double norm = (double)n_q_heads * (double)(T - row_begin);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t c = 0; c < count; ++c) {
+        const int64_t j = cols ? cols[c] : c;
+        double tot = 0.0;
+        for (int32_t h = 0; h < n_q_heads; ++h) {
+            const double* kj = k + (j * n_kv_heads + h / G) * (int64_t)head_dim;
+            for (int64_t i = j > row_begin ? j : row_begin; i < T; ++i) {
+                const double* qi = q + (i * n_q_heads + h) * (int64_t)head_dim;
+                double dot = 0.0;
+                for (int32_t d = 0; d < head_dim; ++d) dot += qi[d] * kj[d];
+                tot += exp(dot * scale - lse[i * n_q_heads + h]);
+            }
+        }
+        mass[c] = tot / norm;
+    }
+    free(lse);
 }
 
 /* One layer of partial prefill (Sections 4.2 and 4.3.3): recompute q/k/v of

@@ -88,3 +88,22 @@ def rotated_pair_bound(b: np.ndarray, head_dim: int) -> np.ndarray:
     bound of the first plus bound of the second member (|cos|, |sin| <= 1)."""
     pair = b[:, 0::2] + b[:, 1::2]
     return np.repeat(pair, 2, axis=1)
+
+
+def check_cache_rows(dt, got, ref, before, sel, x_sel, w, rotated):
+    """Selected rows within the derived bound of the oracle; other rows untouched."""
+    n_tok = got.shape[0]
+    got = got.reshape(n_tok, -1)
+    ref = ref.reshape(n_tok, -1)
+    before = before.reshape(n_tok, -1)
+    keep = np.ones(n_tok, bool)
+    keep[sel] = False
+    assert np.array_equal(got[keep], before[keep])
+    b = fp32_dot_error_bound(x_sel, w)
+    if rotated:
+        b = rotated_pair_bound(b, 0) + 1e-6 * np.abs(ref[sel])
+    spacing = bf16_ulp(ref[sel]) if dt == "bf16" else 2.0 ** -23 * np.abs(ref[sel])
+    err = np.abs(got[sel] - ref[sel])
+    assert np.all(err <= spacing + b), f"max excess {(err - spacing - b).max()}"
+    if dt == "bf16":
+        assert (bf16_ulp_distance(got[sel], ref[sel]) > 1).mean() < 1e-3

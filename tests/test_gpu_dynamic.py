@@ -45,12 +45,41 @@ def test_attention_mass_headline_shape_properties():
                                 hq, hkv)).astype(np.float64)
     H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, T + 1))])
     assert np.allclose(mz, (H[T] - H[:T]) / T, rtol=2e-4, atol=0)
-    # sampled keys against the oracle's definition, one key at a time: the
-    # oracle's full T x T pass is too slow here, so check a leading block
-    small = 512
-    ref = orc.attention_mass(q[:small], k[:small], hq, hkv, 128) * small / T
-    # the first 512 rows' share of the first 512 keys is a lower bound of their mass
-    assert (m[:small] >= ref * (1 - 1e-4) - 1e-9).all()
+    # every key column against the oracle's definition (plain C, fp64)
+    ref = orc.attention_mass_cols(q, k, hq, hkv, 128)
+    assert np.allclose(m, ref, rtol=1e-4, atol=1e-9), np.abs(m - ref).max()
+
+
+def test_headline_mass_chain_into_selection_and_retention():
+    """The GPU's own masses at 5120 tokens, 32 / 8 heads feed the GPU's
+    dynamic recompute set and retention (window of the last 1 - AR/T rows);
+    the oracle takes the same decisions on the same fp32 masses (floating
+    point decides integers here, so both sides decide on the GPU's values),
+    and the window masses match the oracle's definition."""
+    T, hq, hkv = 5120, 32, 8
+    cfg = CONFIGS[2]
+    announce("mass chain 5120: masses -> recompute set -> retention window -> retention")
+    q, k = _qk(cfg, T, hq, hkv, tag=64)
+    qd, kd = dev(q, "bf16"), dev(k, "bf16")
+    mass = ss.attention_mass(qd, kd, hq, hkv)
+    sigma = torch.from_numpy(np.random.default_rng(65).exponential(size=T).astype(np.float32)).cuda()
+    sel, counts = ss.dynamic_recompute(mass, sigma)
+    m_h, s_h, c = host(mass).astype(np.float32), sigma.cpu().numpy(), counts.cpu().numpy()
+    ar, ref_sel, n_hot = _oracle_dyn(m_h, s_h, int(c[0]))
+    assert c[0] == ar and c[2] == n_hot and c[1] == len(ref_sel)
+    assert np.array_equal(sel.cpu().numpy()[: c[1]], ref_sel)
+    row_begin = min(T - 1, T - int(np.floor((1.0 - ar / T) * T + 0.5)))
+    score = ss.attention_mass(qd, kd, hq, hkv, row_begin=row_begin)
+    sc_h = host(score).astype(np.float32)
+    cols = np.unique(np.concatenate([[0, T - 1], np.random.default_rng(66).choice(T, 254, replace=False)]))
+    ref_sc = orc.attention_mass_cols(q, k, hq, hkv, 128, row_begin=row_begin, cols=cols)
+    assert np.allclose(sc_h[cols], ref_sc, rtol=1e-4, atol=1e-9), np.abs(sc_h[cols] - ref_sc).max()
+    rank, kept, n_kept = ss.retention(mass, score, sel, counts, 0.8)
+    ref_rank, ref_kept, ref_keep = orc.retention(m_h, sc_h, ar, ref_sel, 0.8)
+    nk = int(n_kept.cpu().numpy()[0])
+    assert nk == ref_keep
+    assert np.array_equal(rank.cpu().numpy()[:T], ref_rank)
+    assert np.array_equal(kept.cpu().numpy()[:nk], ref_kept)
 
 
 def _dyn_inputs(T, seed, ties):

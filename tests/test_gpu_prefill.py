@@ -18,7 +18,7 @@ import paper_2509_24832_amd as ss
 import workloads
 from workloads import CONFIGS
 
-from helpers import (announce, bf16_ulp, bf16_ulp_distance, dev, dev_i32, fp32_dot_error_bound, host,
+from helpers import (announce, bf16_ulp, check_cache_rows, dev, dev_i32, fp32_dot_error_bound, host,
                      rotated_pair_bound)
 
 pytestmark = pytest.mark.gpu
@@ -41,25 +41,6 @@ def _run_gpu(cfg, x_sel, sel, w, k, v, hq, hkv, want_out=True, want_dev=True):
                                   hq, hkv, want_out=want_out, want_deviation=want_dev)
     return (None if out is None else host(out).reshape(len(sel), -1), None if sig is None else host(sig),
             host(kc), host(vc))
-
-
-def check_cache_rows(dt, got, ref, before, sel, x_sel, w, rotated):
-    """Selected rows within the derived bound of the oracle; other rows untouched."""
-    n_tok = got.shape[0]
-    got = got.reshape(n_tok, -1)
-    ref = ref.reshape(n_tok, -1)
-    before = before.reshape(n_tok, -1)
-    keep = np.ones(n_tok, bool)
-    keep[sel] = False
-    assert np.array_equal(got[keep], before[keep])
-    b = fp32_dot_error_bound(x_sel, w)
-    if rotated:
-        b = rotated_pair_bound(b, 0) + 1e-6 * np.abs(ref[sel])
-    spacing = bf16_ulp(ref[sel]) if dt == "bf16" else 2.0 ** -23 * np.abs(ref[sel])
-    err = np.abs(got[sel] - ref[sel])
-    assert np.all(err <= spacing + b), f"max excess {(err - spacing - b).max()}"
-    if dt == "bf16":
-        assert (bf16_ulp_distance(got[sel], ref[sel]) > 1).mean() < 1e-3
 
 
 def _check(cfg, got, ref, x_sel, sel, w, k0, v0):
@@ -290,3 +271,34 @@ def test_attention_plan_over_1024_row_tiles():
     rows = np.array([0, 1, 31, 32, 1023 * 32, 1024 * 32 + 5, n_sel // 2, n_sel - 33, n_sel - 1])
     ref = orc.attention_rows(host(qd)[rows], sel[rows], host(kd), host(vd), hq, hkv, d, dtype="bf16")
     assert np.max(np.abs(host(got)[rows].reshape(len(rows), -1) - ref.reshape(len(rows), -1))) <= ATOL["bf16"]
+
+
+def test_config2_first_layer_full_recompute():
+    """The benchmark's first layer in its launch configuration: all 5120 rows
+    of the 5k-token Llama-3-8B-shaped layer recomputed (hidden 4096, 32 q /
+    8 kv heads) by semshare_qkv_rope with the deviation of every row against
+    the assembled cache rows it replaces, then semshare_prefill_attention over
+    every row.  Every K/V row and every deviation is checked; output rows on a
+    sample that includes the first and the last."""
+    cfg = CONFIGS[2]
+    n_tok, hidden, hq, hkv, d = 5120, 4096, 32, 8, 128
+    x_all, w, k, v, _ = _case(cfg, n_tok, hidden, hq, hkv, d, 1, tag=9)
+    allpos = np.arange(n_tok, dtype=np.int32)
+    announce("config2 first layer: 5120 rows, hidden 4096")
+    dt = cfg.dtype
+    kc, vc = dev(k, dt), dev(v, dt)
+    ps = dev_i32(allpos)
+    q, sig = ss.qkv_rope(dev(x_all, dt), ps, dev(w.wq, dt), dev(w.wk, dt), dev(w.wv, dt), kc, vc, hq, hkv,
+                         want_deviation=True)
+    out = ss.prefill_attention(q, ps, kc, vc, hkv)
+    out_g, sig_g, kc_g, vc_g = host(out).reshape(n_tok, -1), host(sig), host(kc), host(vc)
+    _, kn, vn = orc.qkv_rows(x_all, allpos, w.wq, w.wk, w.wv, hq, hkv, d, dtype="bf16", want_q=False)
+    sig_r = orc.deviation(k.reshape(n_tok, -1), v.reshape(n_tok, -1), allpos, kn, vn)
+    np.testing.assert_allclose(sig_g, sig_r, rtol=1e-3)
+    check_cache_rows("bf16", kc_g, kn, k, allpos, x_all, w.wk, True)
+    check_cache_rows("bf16", vc_g, vn, v, allpos, x_all, w.wv, False)
+    rows = np.unique(np.concatenate([[0, 1, n_tok - 1], np.random.default_rng(9).choice(n_tok, 61, replace=False)]))
+    qr, _, _ = orc.qkv_rows(x_all[rows], allpos[rows], w.wq, w.wk, w.wv, hq, hkv, d, dtype="bf16", want_kv=False)
+    out_r = orc.attention_rows(qr, allpos[rows], kn, vn, hq, hkv, d, dtype="bf16")
+    err = np.abs(out_g[rows] - out_r).max()
+    assert err <= ATOL["bf16"], f"attention max-abs error {err}"

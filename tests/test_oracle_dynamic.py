@@ -162,3 +162,35 @@ def test_retention_rules():
     assert orc.retention(m, score, 45, [], 0.8)[2] == 45
     assert orc.retention(m, score, 45, sel, 0.8)[2] == 47  # 45 hot + the 2 cold recomputed: all kept
     assert set(np.argsort(rank)[:30].tolist()) <= set(kept.tolist())
+
+
+def test_mass_columns_in_c_closed_forms():
+    # the C statement of the same definition: q = 0 gives the harmonic form,
+    # one dominant key gives e^a / (e^a + i) row by row, masses sum to 1
+    T = 23
+    k = _rng(11).normal(size=(T, 1, 16))
+    m = orc.attention_mass_cols(np.zeros((T, 2, 16)), k, 2, 1, 16)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, T + 1))])
+    assert np.allclose(m, (H[T] - H[:T]) / T, rtol=0, atol=1e-15)
+    T, D, a = 17, 4, 3.0
+    q = np.zeros((T, 1, D)); q[:, 0, 0] = 1.0
+    k = np.zeros((T, 1, D)); k[0, 0, 0] = a * np.sqrt(D)
+    m = orc.attention_mass_cols(q, k, 1, 1, D)
+    i = np.arange(T)
+    assert abs(m[0] - np.mean(np.exp(a) / (np.exp(a) + i))) < 1e-14
+    assert all(abs(m[j] - np.sum(1.0 / (np.exp(a) + i[j:])) / T) < 1e-14 for j in range(1, T))
+    r = _rng(12)
+    q, k = r.normal(size=(30, 4, 8)), r.normal(size=(30, 2, 8))
+    assert abs(orc.attention_mass_cols(q, k, 4, 2, 8).sum() - 1.0) < 1e-12
+
+
+@pytest.mark.parametrize("T,hq,hkv,D,row_begin", [(9, 4, 2, 8, 0), (40, 4, 4, 16, 0), (33, 8, 2, 8, 20),
+                                                  (64, 4, 1, 128, 63)])
+def test_mass_columns_in_c_equal_the_matrix_form(T, hq, hkv, D, row_begin):
+    r = _rng(T + D)
+    q, k = r.normal(size=(T, hq, D)), r.normal(size=(T, hkv, D))
+    full = orc.attention_mass(q, k, hq, hkv, D, row_begin=row_begin)
+    assert np.allclose(orc.attention_mass_cols(q, k, hq, hkv, D, row_begin=row_begin), full, rtol=0, atol=1e-15)
+    cols = np.array([T - 1, 0, T // 2])
+    assert np.allclose(orc.attention_mass_cols(q, k, hq, hkv, D, row_begin=row_begin, cols=cols), full[cols],
+                       rtol=0, atol=1e-15)
