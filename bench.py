@@ -47,8 +47,9 @@ def parse():
     ap.add_argument("--encode", choices=("fused", "two-pass"), default="fused",
                     help="RoPE + LSH of the target in one kernel, or rope_embed then lsh_encode")
     ap.add_argument("--gather", choices=("except", "all"), default="except",
-                    help="layers after the first gather after the selection, skipping the recomputed rows (except), "
-                         "or every layer and row before it (all)")
+                    help="except: the first layer's deviation reads the matched reference rows directly and the "
+                         "layers after it are gathered after the selection, without the recomputed rows; all: "
+                         "every layer and row gathered before the first layer")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
     ap.add_argument("--dynamic-recompute", action="store_true",
@@ -170,14 +171,19 @@ class Path:
             m("lsh")
         self.matcher(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
         m("match")
-        if self.gather_except:  # layer 0 now; layers 1.. after the selection, without the recomputed rows
-            ss.gather_kv(self.ref_k[:1], self.ref_v[:1], self.idx, out_k=self.asm_k[:1], out_v=self.asm_v[:1])
+        wq, wk, wv = self.w[0]
+        if self.gather_except:
+            # layer 0 recomputes every row, so its gathered rows would feed the deviation only: it reads the
+            # matched reference rows directly; layers 1.. are gathered after the selection, without the
+            # recomputed rows
+            ss.qkv_rope_dev_ref(self.e_tgt, self.allpos, wq, wk, wv, self.asm_k[0], self.asm_v[0], hq, hkv,
+                                self.ref_k[0], self.ref_v[0], self.idx, q_out=self.q_full, deviation=self.sigma,
+                                workspace=self.ws)
         else:
             ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
-        m("gather")
-        wq, wk, wv = self.w[0]
-        ss.qkv_rope(self.e_tgt, self.allpos, wq, wk, wv, self.asm_k[0], self.asm_v[0], hq, hkv, q_out=self.q_full,
-                    deviation=self.sigma, want_deviation=True, workspace=self.ws)
+            m("gather")
+            ss.qkv_rope(self.e_tgt, self.allpos, wq, wk, wv, self.asm_k[0], self.asm_v[0], hq, hkv,
+                        q_out=self.q_full, deviation=self.sigma, want_deviation=True, workspace=self.ws)
         m("qkv0")
         ss.prefill_attention(self.q_full, self.allpos, self.asm_k[0], self.asm_v[0], hkv, out=self.out_full,
                              workspace=self.ws)
@@ -521,9 +527,9 @@ def main():
     attn0_flops = 4.0 * D * hq * T * (T + 1) / 2.0
     qkv_flops = 2.0 * n_sel * (hq + 2 * hkv) * D * d
     attn_ms, qkv_ms, attn0_ms = avg("attn"), avg("qkv"), avg("attn0")
-    gather_rows = T + (L - 1) * (T - n_sel) if args.gather == "except" else L * T
+    gather_rows = (L - 1) * (T - n_sel) if args.gather == "except" else L * T
     gather_bytes = 2.0 * 2 * gather_rows * hkv * D * 2  # read + write, K and V
-    gather_ms = avg("gather") + (avg("gather_rest") if "gather_rest" in stages else 0.0)
+    gather_ms = avg("gather_rest") if args.gather == "except" else avg("gather")
     match_ms = avg("match")
     pp_ms = (avg("qkv0") + attn0_ms + (L - 1) * (attn_ms + qkv_ms))
     # the dominant call: prefill_attention (attention kernel + combine of cut row tiles),

@@ -223,6 +223,33 @@ size_t semshare_qkv_rope_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_k
                                    int32_t head_dim, semshare_dtype_t dtype);
 
 /*
+ * semshare_qkv_rope for the first layer, whose deviation compares each
+ * recomputed row with the matched reference row directly (Section 4.2: the
+ * first layer is recomputed in full and its KV deviation against the
+ * rearranged reference cache picks the tokens to recompute; Appendix A.4):
+ * deviation_out[i] = ||ref_k[idx[p]] - k||_2 + ||ref_v[idx[p]] - v||_2 with
+ * p = sel_pos[i], i.e. against the row semshare_gather_kv would have placed
+ * at p (an index outside [0, n_ref) counts as the zero row that the gather
+ * writes).  When every row of the layer is recomputed, its gathered rows are
+ * read by nothing but the deviation, so this call spares that layer's gather.
+ * Cache rows sel_pos[i] are written as by semshare_qkv_rope; the others are
+ * left as they are.  Results are bit for bit those of semshare_gather_kv of
+ * this layer followed by semshare_qkv_rope with deviation.
+ *   ref_k, ref_v  [n_ref][n_kv_heads][head_dim] dtype: the reference cache of
+ *                 this layer (16-byte aligned; must not overlap k_cache or
+ *                 v_cache).   idx [n_tok] int32: the match index.
+ *   deviation_out [n_sel] float32, required.   bf16 only (fp32:
+ *   SEMSHARE_E_UNSUPPORTED).  Other arguments, workspace and limits as for
+ *   semshare_qkv_rope.
+ */
+semshare_status_t semshare_qkv_rope_dev_ref(const void* x_sel, const int32_t* sel_pos, int64_t n_sel, const void* wq,
+                                            const void* wk, const void* wv, void* k_cache, void* v_cache, int64_t n_tok,
+                                            int32_t hidden, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                            double rope_base, void* q_out, float* deviation_out, const void* ref_k,
+                                            const void* ref_v, const int32_t* idx, int64_t n_ref, void* workspace,
+                                            size_t workspace_bytes, semshare_dtype_t dtype, void* stream);
+
+/*
  * The RoPE factor table of semshare_qkv_rope for one set of selected
  * positions, made once and reused.  RoPE (Section 4.3.3: the recomputed q
  * and k are rotated by their own positions) depends on the position and the

@@ -356,12 +356,19 @@ size_t semshare_partial_prefill_workspace(int64_t n_sel, int64_t n_tok, int32_t 
 
 namespace {
 // rope_table == nullptr: semshare_qkv_rope (the table is made in the workspace)
+struct DevRef {  // the first-layer deviation source of semshare_qkv_rope_dev_ref
+    const void* k;
+    const void* v;
+    const int32_t* idx;
+    int64_t n_ref;
+};
+
 semshare_status_t qkv_rope_impl(const char* fn, const void* rope_table, size_t rope_table_bytes, const void* x_sel,
                                 const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
                                 const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base,
                                 void* q_out, float* deviation_out, void* workspace, size_t workspace_bytes,
-                                semshare_dtype_t dtype, void* stream) {
+                                semshare_dtype_t dtype, void* stream, const DevRef* ref = nullptr) {
     semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim, dtype, true);
     if (st != SEMSHARE_OK) return st;
     if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
@@ -383,6 +390,17 @@ semshare_status_t qkv_rope_impl(const char* fn, const void* rope_table, size_t r
                         semshare_rope_table_bytes(n_sel, head_dim));
         a.rope_table = rope_table;
     }
+    if (ref) {
+        if (dtype != SEMSHARE_BF16) return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 only", fn);
+        if (!deviation_out || !ref->k || !ref->v || !ref->idx)
+            return fail(SEMSHARE_E_INVAL, "%s: deviation_out, ref_k, ref_v and idx are required", fn);
+        if (ref->n_ref < 0 || ref->n_ref > (int64_t(1) << 31) - 1) return fail(SEMSHARE_E_INVAL, "%s: n_ref out of range", fn);
+        if (!aligned16(ref->k) || !aligned16(ref->v)) return fail(SEMSHARE_E_INVAL, "%s: ref_k and ref_v must be 16-byte aligned", fn);
+        a.ref_k = ref->k;
+        a.ref_v = ref->v;
+        a.ref_idx = ref->idx;
+        a.ref_n = ref->n_ref;
+    }
     hipError_t e = dtype == SEMSHARE_BF16 ? semshare::launch_qkv_bf16(a, (hipStream_t)stream)
                                           : semshare::launch_qkv_f32(a, (hipStream_t)stream);
     return from_hip(e, "qkv_rope launch");
@@ -398,6 +416,18 @@ semshare_status_t semshare_qkv_rope(const void* x_sel, const int32_t* sel_pos, i
     return qkv_rope_impl("qkv_rope", nullptr, 0, x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden,
                          n_q_heads, n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace,
                          workspace_bytes, dtype, stream);
+}
+
+semshare_status_t semshare_qkv_rope_dev_ref(const void* x_sel, const int32_t* sel_pos, int64_t n_sel, const void* wq,
+                                            const void* wk, const void* wv, void* k_cache, void* v_cache, int64_t n_tok,
+                                            int32_t hidden, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                            double rope_base, void* q_out, float* deviation_out, const void* ref_k,
+                                            const void* ref_v, const int32_t* idx, int64_t n_ref, void* workspace,
+                                            size_t workspace_bytes, semshare_dtype_t dtype, void* stream) {
+    const DevRef ref{ref_k, ref_v, idx, n_ref};
+    return qkv_rope_impl("qkv_rope_dev_ref", nullptr, 0, x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok,
+                         hidden, n_q_heads, n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace,
+                         workspace_bytes, dtype, stream, &ref);
 }
 
 size_t semshare_rope_table_bytes(int64_t n_sel, int32_t head_dim) {

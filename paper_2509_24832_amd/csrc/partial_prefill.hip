@@ -105,6 +105,10 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     g.kv[1] = static_cast<uint16_t*>(a.v_cache);
     g.rope = rope;
     g.dev_parts = dev_parts;
+    g.dev_src[0] = static_cast<const uint16_t*>(a.ref_k);
+    g.dev_src[1] = static_cast<const uint16_t*>(a.ref_v);
+    g.dev_idx = a.ref_idx;
+    g.dev_n = a.ref_n;
     launch_qkv_gemm(g, bn, s);
     if (a.deviation_out)
         hipLaunchKernelGGL(dev_final_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_parts,

@@ -18,7 +18,9 @@
 // Epilogue through an fp32 LDS tile: RoPE of q/k pairs from the per-row
 // (cos, sin) table, bf16 rounding, q to its buffer, k/v scattered to the cache
 // rows sel_pos after the squared differences against the old rows are summed
-// per tile (the deviation, reduced later in a fixed order).  Workgroups are
+// per tile (the deviation, reduced later in a fixed order).  The old rows are
+// the cache rows being replaced, or (first layer) the matched rows of the
+// reference cache read through the match index.  Workgroups are
 // mapped XCD-major: all M tiles of one weight tile run on the same XCD, so the
 // weights are fetched from HBM once per XCD.
 #include <type_traits>
@@ -271,11 +273,23 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) cs[u][e] = ok && rope ? g.rope[m * half_d + k0 + e] : make_float2(1.0f, 0.0f);
         }
+        if (dev && g.dev_idx) {  // the deviation against matched reference rows
+            const uint16_t* src = g.dev_src[seg - 1];
+            int32_t j[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            old[u] = u32x4_t{0u, 0u, 0u, 0u};
-            if (dev && p[u] >= 0 && p[u] < g.n_tok)
-                old[u] = *reinterpret_cast<const u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n);
+            for (int u = 0; u < kBatch; ++u) j[u] = p[u] >= 0 && p[u] < g.n_tok ? g.dev_idx[p[u]] : -1;
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                old[u] = u32x4_t{0u, 0u, 0u, 0u};
+                if (j[u] >= 0 && j[u] < g.dev_n) old[u] = *reinterpret_cast<const u32x4_t*>(src + (int64_t)j[u] * seg_cols + n);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                old[u] = u32x4_t{0u, 0u, 0u, 0u};
+                if (dev && p[u] >= 0 && p[u] < g.n_tok)
+                    old[u] = *reinterpret_cast<const u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n);
+            }
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {

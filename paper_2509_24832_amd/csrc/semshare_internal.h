@@ -123,6 +123,13 @@ struct QkvArgs {
     float* deviation_out;  // [n_sel] or null
     void* workspace;       // qkv_workspace_bytes()
     const void* rope_table = nullptr;  // bf16 path: [n_sel][D/2] (cos, sin) made by launch_rope_table, or null
+    // bf16 path: the deviation compares with ref_k/ref_v[ref_idx[p]] (rows of
+    // a reference cache, [ref_n][Hkv*D]) instead of the cache row p; null:
+    // with the cache row
+    const void* ref_k = nullptr;
+    const void* ref_v = nullptr;
+    const int32_t* ref_idx = nullptr;
+    int64_t ref_n = 0;
 };
 
 // Step 2: causal GQA attention of the selected rows over the cache.
@@ -168,6 +175,9 @@ struct GemmArgs {
     uint16_t* kv[2];       // k_cache, v_cache [n_tok][Hkv*D]
     const float2* rope;    // [n_sel][D/2] (cos, sin)
     float* dev_parts;      // [n_sel][2][Hkv*D/BN] squared-difference sums, or null
+    const uint16_t* dev_src[2];  // rows the deviation compares with: reference K, V [dev_n][Hkv*D], or null (the cache)
+    const int32_t* dev_idx;      // position p -> row dev_idx[p] of dev_src (outside [0, dev_n): a zero row)
+    int64_t dev_n;
 };
 int32_t qkv_gemm_bn(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim);
 hipError_t launch_qkv_gemm(const GemmArgs& g, int32_t bn, hipStream_t s);

@@ -68,6 +68,8 @@ def load() -> ctypes.CDLL:
         "semshare_dynamic_recompute": (I32, [P, P, I32, F64, F64, F64, P, P, P]),
         "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
+        "semshare_qkv_rope_dev_ref": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, P, P,
+                                            I64, P, SZ, I32, P]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_prefill_attention_workspace": (SZ, [I64, I64, I32, I32, I32, I32]),
         "semshare_bank_similarity_workspace": (SZ, [I64, I32]),
@@ -429,6 +431,48 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
     _call("semshare_qkv_rope", _ptr(x_sel), _ptr(sel_pos), n_sel, _ptr(wq) if want_q else None, _ptr(wk), _ptr(wv),
           _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, float(rope_base),
           _ptr(q_out), _ptr(deviation), _ptr(ws), 0 if ws is None else ws.numel(), _dt(x_sel), _stream())
+    return q_out, deviation
+
+
+def qkv_rope_dev_ref(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tensor], wk: torch.Tensor,
+                     wv: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int,
+                     ref_k: torch.Tensor, ref_v: torch.Tensor, idx: torch.Tensor, rope_base: float = 10000.0,
+                     q_out: Optional[torch.Tensor] = None, want_q: bool = True,
+                     deviation: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """qkv_rope (bf16) whose deviation compares each recomputed row p with the matched reference row
+    ref[idx[p]] (ref_* [n_ref, Hkv, D], one layer; idx [n_tok] int32), as gather_kv then qkv_rope would.
+    Returns (q [n_sel, Hq, D] or None, deviation [n_sel])."""
+    _dev(x_sel, "x_sel")
+    dt = x_sel.dtype
+    _dev(sel_pos, "sel_pos", torch.int32)
+    _dev(idx, "idx", torch.int32)
+    for name, t in (("wk", wk), ("wv", wv), ("k_cache", k_cache), ("v_cache", v_cache), ("ref_k", ref_k),
+                    ("ref_v", ref_v)):
+        _dev(t, name, dt)
+    n_sel, hidden = x_sel.shape
+    n_tok, head_dim = k_cache.shape[0], k_cache.shape[-1]
+    if k_cache.numel() != n_tok * n_kv_heads * head_dim or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [n_tok, n_kv_heads, head_dim]")
+    n_ref = ref_k.shape[0]
+    if ref_k.numel() != n_ref * n_kv_heads * head_dim or ref_v.shape != ref_k.shape:
+        raise ValueError("reference caches must be [n_ref, n_kv_heads, head_dim]")
+    if idx.dim() != 1 or idx.numel() < n_tok:
+        raise ValueError("idx must hold one entry per cache row")
+    if want_q:
+        _dev(wq, "wq", dt)
+        if q_out is None:
+            q_out = torch.empty((n_sel, n_q_heads, head_dim), dtype=dt, device=x_sel.device)
+        _dev(q_out, "q_out", dt)
+    else:
+        q_out = None
+    if deviation is None:
+        deviation = torch.empty(n_sel, dtype=torch.float32, device=x_sel.device)
+    _dev(deviation, "deviation", torch.float32)
+    ws = _workspace(qkv_rope_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dt), workspace, x_sel)
+    _call("semshare_qkv_rope_dev_ref", _ptr(x_sel), _ptr(sel_pos), n_sel, _ptr(wq) if want_q else None, _ptr(wk),
+          _ptr(wv), _ptr(k_cache), _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, float(rope_base),
+          _ptr(q_out), _ptr(deviation), _ptr(ref_k), _ptr(ref_v), _ptr(idx), n_ref, _ptr(ws),
+          0 if ws is None else ws.numel(), _dt(x_sel), _stream())
     return q_out, deviation
 
 

@@ -272,3 +272,18 @@ def test_bank_similarity_validation(lib):
     assert st(off=None) == b.E_INVAL and st(sim=None) == b.E_INVAL
     assert st(n_prompts=0, off=None, dsum=None, sim=None) == b.OK
 
+
+
+def test_qkv_rope_dev_ref_validation(lib):
+    L = ss.load()
+    head = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 16, 256, 8, 2, 128, 1e4, FAKE)
+    ws = (FAKE, 1 << 30)
+    assert L.semshare_qkv_rope_dev_ref(*head, None, FAKE, FAKE, FAKE, 16, *ws, 1, None) == b.E_INVAL  # no deviation
+    assert L.semshare_qkv_rope_dev_ref(*head, FAKE, None, FAKE, FAKE, 16, *ws, 1, None) == b.E_INVAL  # no ref_k
+    assert L.semshare_qkv_rope_dev_ref(*head, FAKE, FAKE, FAKE, None, 16, *ws, 1, None) == b.E_INVAL  # no idx
+    assert L.semshare_qkv_rope_dev_ref(*head, FAKE, FAKE_ODD, FAKE, FAKE, 16, *ws, 1, None) == b.E_INVAL  # alignment
+    assert L.semshare_qkv_rope_dev_ref(*head, FAKE, FAKE, FAKE, FAKE, -1, *ws, 1, None) == b.E_INVAL  # n_ref
+    assert L.semshare_qkv_rope_dev_ref(*head, FAKE, FAKE, FAKE, FAKE, 16, *ws, 0, None) == b.E_UNSUPPORTED  # fp32
+    bad = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 256, 8, 2, 128, 1e4, FAKE)
+    assert L.semshare_qkv_rope_dev_ref(*bad, FAKE, FAKE, FAKE, FAKE, 16, *ws, 1, None) == b.E_INVAL  # n_sel > n_tok
+    assert L.semshare_qkv_rope_dev_ref(*head, FAKE, FAKE, FAKE, FAKE, 16, FAKE, 0, 1, None) == b.E_INVAL  # workspace

@@ -302,3 +302,42 @@ def test_config2_first_layer_full_recompute():
     out_r = orc.attention_rows(qr, allpos[rows], kn, vn, hq, hkv, d, dtype="bf16")
     err = np.abs(out_g[rows] - out_r).max()
     assert err <= ATOL["bf16"], f"attention max-abs error {err}"
+
+
+@pytest.mark.parametrize("n_tok,n_ref,hidden,hq,hkv,d,n_sel", [(300, 280, 256, 8, 2, 128, 300),
+                                                              (300, 280, 256, 8, 2, 128, 90),
+                                                              (5120, 5120, 4096, 32, 8, 128, 5120)])
+def test_first_layer_deviation_against_reference_rows(n_tok, n_ref, hidden, hq, hkv, d, n_sel):
+    """semshare_qkv_rope_dev_ref gives bit for bit what semshare_gather_kv of
+    the layer followed by semshare_qkv_rope with deviation gives: q, the
+    recomputed cache rows, the deviation; rows not selected are untouched and
+    an index outside the reference counts as a zero row."""
+    cfg = CONFIGS[1]
+    x_all, w, _, _, _ = _case(cfg, n_tok, hidden, hq, hkv, d, 1, tag=12)
+    rk, rv = workloads.make_cache(cfg, 1, n_ref, n_kv_heads=hkv, head_dim=d, tag=13)
+    idx = np.random.default_rng(14).integers(0, n_ref, n_tok).astype(np.int32)
+    idx[3], idx[7] = -1, n_ref  # outside the reference: zero rows
+    sel = np.arange(n_tok, dtype=np.int32) if n_sel == n_tok else workloads.make_sel_pos(cfg, n_tok, n_sel, tag=15)
+    sel = np.unique(np.concatenate([sel, [3, 7]])).astype(np.int32)  # the two rows with no reference row
+    announce(f"first-layer deviation against reference rows n_tok={n_tok} n_ref={n_ref} n_sel={len(sel)}")
+    dt = "bf16"
+    RK, RV, ix, ps = dev(rk[0], dt), dev(rv[0], dt), dev_i32(idx), dev_i32(sel)
+    xs = dev(x_all[sel], dt)
+    wq, wk, wv = dev(w.wq, dt), dev(w.wk, dt), dev(w.wv, dt)
+    ka, va = ss.gather_kv(RK[None], RV[None], ix)
+    qa, sa = ss.qkv_rope(xs, ps, wq, wk, wv, ka[0], va[0], hq, hkv, want_deviation=True)
+    kb = torch.full((n_tok, hkv, d), 5.0, dtype=torch.bfloat16, device="cuda")
+    vb = torch.full_like(kb, 5.0)
+    qb, sb = ss.qkv_rope_dev_ref(xs, ps, wq, wk, wv, kb, vb, hq, hkv, RK, RV, ix)
+    assert torch.equal(qa, qb) and torch.equal(sa, sb)
+    keep = np.ones(n_tok, bool)
+    keep[sel] = False
+    for a_t, b_t in ((ka[0], kb), (va[0], vb)):
+        a_h, b_h = host(a_t), host(b_t)
+        assert np.array_equal(a_h[sel], b_h[sel])
+        assert np.all(b_h[keep] == 5.0)
+    if n_tok <= 1024:  # and the deviation against the oracle's gathered rows
+        g_k = np.where((idx >= 0)[:, None] & (idx < n_ref)[:, None], rk[0].reshape(n_ref, -1)[np.clip(idx, 0, n_ref - 1)], 0)
+        g_v = np.where((idx >= 0)[:, None] & (idx < n_ref)[:, None], rv[0].reshape(n_ref, -1)[np.clip(idx, 0, n_ref - 1)], 0)
+        _, kn, vn = orc.qkv_rows(x_all[sel], sel, w.wq, w.wk, w.wv, hq, hkv, d, dtype="bf16", want_q=False)
+        np.testing.assert_allclose(host(sb), orc.deviation(g_k, g_v, sel, kn, vn), rtol=1e-3)
