@@ -303,6 +303,28 @@ size_t semshare_prefill_attention_workspace(int64_t n_sel, int64_t n_tok, int32_
                                             semshare_dtype_t dtype);
 
 /*
+ * semshare_prefill_attention for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same kernels and results, bit for bit, with no workspace
+ * argument.  The work plan and the partial results of cut row tiles live in a
+ * static device array of the library, 40 MiB per GPU, held from the
+ * library's first use on that GPU until the process ends; this call
+ * allocates nothing.  Sizes whose workspace
+ * (semshare_prefill_attention_workspace) exceeds 40 MiB return
+ * SEMSHARE_E_UNSUPPORTED (with 8 kv heads and head_dim 128 the need is about
+ * 34 MiB whatever n_tok, so every size the other call takes fits).  The
+ * array is shared by every call on the same GPU and keeps the last call's
+ * contents (nothing in it needs to start at zero): calls that overlap on one
+ * GPU, from several streams or threads, race and must be serialised by the
+ * caller.  Arguments, limits and errors otherwise as
+ * semshare_prefill_attention.
+ */
+semshare_status_t semshare_prefill_attention_noalloc(const void* q, const int32_t* sel_pos, int64_t n_sel,
+                                                     const void* k_cache, const void* v_cache, int64_t n_tok,
+                                                     int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                     float sm_scale, void* out, semshare_dtype_t dtype, void* stream);
+
+/*
  * The work plan of semshare_prefill_attention for one set of selected
  * positions, made once and reused.  The selection is made once per prompt
  * (Section 4.2: the same high-deviation tokens are recomputed in every layer

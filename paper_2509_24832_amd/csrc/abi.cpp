@@ -508,6 +508,36 @@ semshare_status_t semshare_prefill_attention(const void* q, const int32_t* sel_p
                                   dtype, stream);
 }
 
+semshare_status_t semshare_prefill_attention_noalloc(const void* q, const int32_t* sel_pos, int64_t n_sel,
+                                                     const void* k_cache, const void* v_cache, int64_t n_tok,
+                                                     int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                     float sm_scale, void* out, semshare_dtype_t dtype, void* stream) {
+    const char* fn = "prefill_attention_noalloc";
+    semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, 0, n_q_heads, n_kv_heads, head_dim, dtype, false);
+    if (st != SEMSHARE_OK) return st;
+    // the argument checks of semshare_prefill_attention come first, so that a
+    // bad call is rejected before the device is touched
+    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", fn);
+    if (n_sel == 0) return ok();
+    if (!q || !sel_pos || !k_cache || !v_cache || !out) return fail(SEMSHARE_E_INVAL, "%s: null buffer", fn);
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+        return fail(SEMSHARE_E_INVAL, "%s: buffers must be 16-byte aligned", fn);
+    const size_t need = semshare::plan_attention(n_sel, n_tok, n_q_heads, n_kv_heads, head_dim, dtype).total;
+    if (need > semshare::kAttnScratchBytes)
+        return fail(SEMSHARE_E_UNSUPPORTED,
+                    "%s: these sizes need %zu bytes of scratch, more than the %zu bytes of the library's static "
+                    "scratch; use semshare_prefill_attention with a workspace",
+                    fn, need, semshare::kAttnScratchBytes);
+    if (need == 0)  // the fp32 path uses no scratch
+        return prefill_attention_impl(fn, PLAN_IN_WORKSPACE, 0, q, sel_pos, n_sel, k_cache, v_cache, n_tok, n_q_heads,
+                                      n_kv_heads, head_dim, sm_scale, out, nullptr, 0, dtype, stream);
+    void* ws = nullptr;
+    const hipError_t e = semshare::attention_scratch(&ws);
+    if (e != hipSuccess) return from_hip(e, "prefill_attention_noalloc: scratch address");
+    return prefill_attention_impl(fn, PLAN_IN_WORKSPACE, 0, q, sel_pos, n_sel, k_cache, v_cache, n_tok, n_q_heads,
+                                  n_kv_heads, head_dim, sm_scale, out, ws, semshare::kAttnScratchBytes, dtype, stream);
+}
+
 size_t semshare_attention_plan_bytes(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
                                      int32_t head_dim, semshare_dtype_t dtype) {
     if (!dtype_ok(dtype) || n_sel < 0 || n_tok < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0 ||

@@ -46,7 +46,9 @@
 // halve that traffic; each adds one bf16 rounding (relative 2^-9) before the
 // output's own.
 #include <algorithm>
+#include <atomic>
 #include <climits>
+#include <mutex>
 
 #include "semshare_internal.h"
 
@@ -966,6 +968,39 @@ hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream
     if (!make_plan) t.plan = static_cast<int32_t*>(const_cast<void*>(a.plan));
     if (a.head_dim == 128) return launch<128>(t, make_plan, s);
     return launch<64>(t, make_plan, s);
+}
+
+// ---- the allocation-free attention (semshare_prefill_attention_noalloc)
+// Its plan and partial results live in this file-scope device array, one
+// copy per GPU, kept until the process ends.  In host code `scratch` names a
+// host-side stand-in, never the device memory: every use goes through the
+// address hipGetSymbolAddress returns for the current device.
+namespace {
+__device__ __align__(256) unsigned char scratch[kAttnScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+}  // namespace
+
+hipError_t attention_scratch(void** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (!p) return hipErrorInvalidSymbol;
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *ptr = p;
+    return hipSuccess;
 }
 
 hipError_t launch_attention_plan_bf16(const AttnCall& a, const AttnPlan& p, void* plan, hipStream_t s) {

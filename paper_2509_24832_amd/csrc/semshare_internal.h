@@ -194,4 +194,10 @@ hipError_t launch_attention_bf16(const AttnCall& a, const AttnPlan& p, hipStream
 hipError_t launch_attention_plan_bf16(const AttnCall& a, const AttnPlan& p, void* plan, hipStream_t s);
 hipError_t launch_attention_f32(const AttnCall& a, const AttnPlan& p, hipStream_t s);
 
+// Size of the static device array that holds the plan and partial results of
+// semshare_prefill_attention_noalloc (plan_attention().total must fit), and
+// its address on the current device (looked up once per device).
+constexpr size_t kAttnScratchBytes = size_t(40) << 20;
+hipError_t attention_scratch(void** ptr);
+
 }  // namespace semshare

@@ -68,6 +68,7 @@ def load() -> ctypes.CDLL:
         "semshare_dynamic_recompute": (I32, [P, P, I32, F64, F64, F64, P, P, P]),
         "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
         "semshare_qkv_rope_workspace": (SZ, [I64, I32, I32, I32, I32]),
+        "semshare_prefill_attention_noalloc": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, I32, P]),
         "semshare_qkv_rope_dev_ref": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, P, P,
                                             I64, P, SZ, I32, P]),
         "semshare_prefill_attention": (I32, [P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
@@ -568,6 +569,28 @@ def prefill_attention(q: torch.Tensor, sel_pos: torch.Tensor, k_cache: torch.Ten
         _call("semshare_prefill_attention_planned", _ptr(plan), plan.numel(), _ptr(q), _ptr(sel_pos), n_sel,
               _ptr(k_cache), _ptr(v_cache), n_tok, n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out),
               _ptr(ws), 0 if ws is None else ws.numel(), _dt(q), _stream())
+    return out
+
+
+def prefill_attention_noalloc(q: torch.Tensor, sel_pos: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                              n_kv_heads: int, sm_scale: float = 0.0,
+                              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """prefill_attention with no workspace: the library's static device scratch holds the plan and the
+    partial results (calls on one GPU must not overlap)."""
+    _dev(q, "q")
+    dt = q.dtype
+    _dev(sel_pos, "sel_pos", torch.int32)
+    _dev(k_cache, "k_cache", dt)
+    _dev(v_cache, "v_cache", dt)
+    n_sel, n_q_heads, head_dim = q.shape
+    n_tok = k_cache.shape[0]
+    if k_cache.numel() != n_tok * n_kv_heads * head_dim or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [n_tok, n_kv_heads, head_dim]")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out", dt)
+    _call("semshare_prefill_attention_noalloc", _ptr(q), _ptr(sel_pos), n_sel, _ptr(k_cache), _ptr(v_cache), n_tok,
+          n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out), _dt(q), _stream())
     return out
 
 

@@ -287,3 +287,22 @@ def test_qkv_rope_dev_ref_validation(lib):
     bad = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 256, 8, 2, 128, 1e4, FAKE)
     assert L.semshare_qkv_rope_dev_ref(*bad, FAKE, FAKE, FAKE, FAKE, 16, *ws, 1, None) == b.E_INVAL  # n_sel > n_tok
     assert L.semshare_qkv_rope_dev_ref(*head, FAKE, FAKE, FAKE, FAKE, 16, FAKE, 0, 1, None) == b.E_INVAL  # workspace
+
+
+def test_prefill_attention_noalloc_validation(lib):
+    L = ss.load()
+    args = (FAKE, FAKE, 8, FAKE, FAKE, 16, 8, 2, 128)
+    assert L.semshare_prefill_attention_noalloc(*args, 0.0, None, 1, None) == b.E_INVAL  # no output
+    assert L.semshare_prefill_attention_noalloc(*args, -1.0, FAKE, 1, None) == b.E_INVAL  # scale
+    assert L.semshare_prefill_attention_noalloc(FAKE_ODD, FAKE, 8, FAKE, FAKE, 16, 8, 2, 128, 0.0, FAKE, 1,
+                                                None) == b.E_INVAL  # alignment
+    assert L.semshare_prefill_attention_noalloc(FAKE, FAKE, 8, FAKE, FAKE, 16, 8, 2, 96, 0.0, FAKE, 1,
+                                                None) == b.E_UNSUPPORTED  # head_dim
+    assert L.semshare_prefill_attention_noalloc(None, None, 0, None, None, 16, 8, 2, 128, 0.0, None, 1, None) == b.OK
+    # 512 kv heads of head_dim 128 need 64 MiB of partial results: beyond the 40 MiB static scratch
+    assert L.semshare_prefill_attention_noalloc(FAKE, FAKE, 64, FAKE, FAKE, 64, 512, 512, 128, 0.0, FAKE, 1,
+                                                None) == b.E_UNSUPPORTED
+    assert "scratch" in ss.last_error()
+    # the headline shapes fit: the workspace the other call needs stays below 40 MiB
+    for n_sel, n_tok in [(1280, 5120), (5120, 5120), (3277, 32768), (32768, 32768)]:
+        assert L.semshare_prefill_attention_workspace(n_sel, n_tok, 32, 8, 128, 1) <= 40 << 20
