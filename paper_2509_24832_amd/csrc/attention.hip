@@ -4,11 +4,14 @@
 // For a selected row at position p and query head h:
 //   out = softmax_{j <= p}(q_h . K[j][h/G] * scale) V[j][h/G]
 //
-// Work decomposition.  A 256-thread workgroup owns one kv head g and 256
+// Work decomposition.  A 512-thread workgroup owns one kv head g and 256
 // query columns = (256/G selected rows) x (the G query heads of g); it runs
-// alone on its CU (one wave per SIMD).  Each wave owns two 32-column blocks,
-// so every K or V fragment it reads from LDS feeds two MFMAs (64 flop per LDS
-// byte; with one block per wave the matrix cores would wait on LDS).
+// alone on its CU with two waves per SIMD, each wave owning one 32-column
+// block.  The two waves of a SIMD share its matrix core, so the softmax
+// arithmetic of one runs while the other's MFMAs execute (with one wave per
+// SIMD and two blocks per wave the key loop took ~62 cycles per MFMA, with
+// two waves ~51 per MFMA and SIMD; 11% fewer cycles per workgroup at 5120
+// tokens, partly given back by a lower clock under the higher MFMA load).
 // S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_32x32x16_bf16: every lane then
 // holds one query column.
 //
@@ -58,6 +61,8 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int KT = 64;       // keys per LDS tile (two sub-tiles)
 constexpr int NCOL = 256;    // query columns per workgroup
+constexpr int kNW = 8;       // waves per workgroup (two per SIMD)
+constexpr int kNB = NCOL / 32 / kNW;  // 32-column blocks per wave
 constexpr int kStages = 4;   // K/V ring depth
 constexpr float kSumLimit = 65536.0f;  // 2^16
 constexpr int kCUs = 256;        // compute units of the chip
@@ -104,7 +109,7 @@ struct ACfg {
     static constexpr int kStage = 2 * kTileBytes;      // K then V
     static constexpr int kLds = kStages * kStage;
     static constexpr int kRowsPerLoad = 64 / kNch;     // rows one 1-KB direct load covers
-    static constexpr int kLoadsPerWave = KT / kRowsPerLoad / 4;  // per tensor
+    static constexpr int kLoadsPerWave = KT / kRowsPerLoad / kNW;  // per tensor
     static constexpr int kLoads = 2 * kLoadsPerWave;   // per wave per tile (K + V)
     static constexpr int kMd = D / 32;                 // 32-row blocks of O^T
     static constexpr int kKs = D / 16;                 // k-steps of S^T
@@ -178,11 +183,11 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     asm volatile("" ::"s"(lgR), "s"(Hq), "s"(G), "s"(n_sel), "s"(posp), "s"(qbase));
     // this lane's two query columns: column c of the tile is row c % R of
     // it, query head g*G + c / R
-    int64_t row[2];
-    int32_t p_l[2];
+    int64_t row[kNB];
+    int32_t p_l[kNB];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int c = 64 * wave + 32 * nb + l32;
+    for (int nb = 0; nb < kNB; ++nb) {
+        const int c = 32 * (kNB * wave + nb) + l32;
         row[nb] = ((int64_t)tile << lgR) + (c & ((1 << lgR) - 1));
         p_l[nb] = row[nb] < n_sel ? posp[row[nb]] : -1;  // checked below, after the Q loads are out
     }
@@ -190,10 +195,10 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     // are issued here, together with the positions; they move to the
     // accumulation registers (zeroed for columns without a position) once
     // the first K/V tile is on its way as well.
-    u32x4_t qv[2][C::kKs];
+    u32x4_t qv[kNB][C::kKs];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int c = 64 * wave + 32 * nb + l32;
+    for (int nb = 0; nb < kNB; ++nb) {
+        const int c = 32 * (kNB * wave + nb) + l32;
         const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(
             qbase + ((row[nb] < n_sel ? row[nb] : 0) * Hq + g * G + (c >> lgR)) * (int64_t)D + half * (D / 2));
 #pragma unroll
@@ -201,9 +206,9 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < kNB; ++nb)
         if (p_l[nb] < 0 || p_l[nb] >= a.n_tok) p_l[nb] = -1;
-    bf16x8_t qf[2][C::kKs];
+    bf16x8_t qf[kNB][C::kKs];
 
     // ---- direct-load sources.  Load i of this wave (per tensor) fills rows
     // [rpl*(wave*lpw + i), +rpl) of the tile; lane -> (row, physical chunk pc),
@@ -277,19 +282,24 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             (lds_s16x4_t*)(uintptr_t)((vb0 ^ (uint32_t)(md << 6)) + (uint32_t)row_off * C::kRowBytes));
     };
 
-    f32x16_t oacc[2][C::kMd];
+    f32x16_t oacc[kNB][C::kMd];
     // O is zeroed after the first sub-tile's probabilities (zero_o): before
     // it the accumulation registers hold Q and two score tiles only
     auto zero_o = [&]() {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
             for (int i = 0; i < C::kMd; ++i) {
                 oacc[nb][i] = f32x16_t{};
                 asm volatile("" : "+a"(oacc[nb][i]));
             }
     };
-    float m_run[2] = {-1.0e30f, -1.0e30f}, l_run[2] = {0.0f, 0.0f};
+    float m_run[kNB], l_run[kNB];
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+        m_run[nb] = -1.0e30f;
+        l_run[nb] = 0.0f;
+    }
     const float cl2 = a.cl2;
 
     // Sub-tile u is half u%2 of the 64-key tile u/2 in ring stage (u/2) % kStages.
@@ -317,30 +327,31 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             }
     };
     // S^T for both column blocks (one K fragment feeds both)
-    auto s_mfma = [&](const bf16x8_t (&kf)[C::kKs], f32x16_t (&sacc)[2]) {
-        sacc[0] = sacc[1] = f32x16_t{};
+    auto s_mfma = [&](const bf16x8_t (&kf)[C::kKs], f32x16_t (&sacc)[kNB]) {
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) sacc[nb] = f32x16_t{};
 #pragma unroll
         for (int s = 0; s < C::kKs; ++s)
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
+            for (int nb = 0; nb < kNB; ++nb)
                 sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[nb][s], sacc[nb], 0, 0, 0);
     };
     // O^T += V^T P^T
-    auto pv_mfma = [&](const bf16x8_t (&vf)[2][C::kMd], const bf16x8_t (&pb)[2][2]) {
+    auto pv_mfma = [&](const bf16x8_t (&vf)[2][C::kMd], const bf16x8_t (&pb)[kNB][2]) {
 #pragma unroll
         for (int sp = 0; sp < 2; ++sp)
 #pragma unroll
             for (int md = 0; md < C::kMd; ++md)
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
+                for (int nb = 0; nb < kNB; ++nb)
                     oacc[nb][md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[sp][md], pb[nb][sp], oacc[nb][md], 0, 0, 0);
     };
     // mask keys past a column's position or past the chunk (boundary sub-tiles only)
-    auto mask = [&](int u, f32x16_t (&sacc)[2]) {
+    auto mask = [&](int u, f32x16_t (&sacc)[kNB]) {
         const int32_t k0 = kbeg + 32 * u;
         if (k0 + 31 > pmin || k0 + 32 > kend) {
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < kNB; ++nb) {
                 // key k0 + 4*half + o is kept iff o <= lim
                 const int32_t lim = min(p_l[nb], kend - 1) - k0 - 4 * half;
 #pragma unroll
@@ -356,9 +367,9 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     // probabilities as bf16 MFMA operands (k index 8h+e of step sp is key
     // 16sp + 8(e/4) + 4h + e%4 of the sub-tile, the keys whose S^T values this
     // lane holds) and the lane's sums of them
-    auto exp_pack = [&](const f32x16_t (&sacc)[2], bf16x8_t (&pb)[2][2], float (&ts)[2]) {
+    auto exp_pack = [&](const f32x16_t (&sacc)[kNB], bf16x8_t (&pb)[kNB][2], float (&ts)[kNB]) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < kNB; ++nb) {
             const float mc = m_run[nb] * cl2;
             ts[nb] = 0.0f;
 #pragma unroll
@@ -374,10 +385,13 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     };
     // accept the sub-tile's probabilities, or (rare) move the reference to
     // the sub-tile's maximum, rescale O and l, and form them again
-    auto settle = [&](const f32x16_t (&sacc)[2], bf16x8_t (&pb)[2][2], float (&ts)[2], bool o_live) {
-        if (__any(!(ts[0] <= kSumLimit) || !(ts[1] <= kSumLimit))) {
+    auto settle = [&](const f32x16_t (&sacc)[kNB], bf16x8_t (&pb)[kNB][2], float (&ts)[kNB], bool o_live) {
+        bool over = false;
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < kNB; ++nb) over = over || !(ts[nb] <= kSumLimit);
+        if (__any(over)) {
+#pragma unroll
+            for (int nb = 0; nb < kNB; ++nb) {
                 float mx = sacc[nb][0];
 #pragma unroll
                 for (int v = 1; v < 16; ++v) mx = fmaxf(mx, sacc[nb][v]);
@@ -398,8 +412,8 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             }
             exp_pack(sacc, pb, ts);
         }
-        l_run[0] += ts[0];
-        l_run[1] += ts[1];
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) l_run[nb] += ts[nb];
     };
 
     const int n_sub = (kend - kbeg + 31) / 32;
@@ -409,7 +423,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     // the direct loads) also cover tile 0, needed next anyway; tiles 1 and 2
     // are issued after them so that those waits do not cover them too.
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
         for (int s = 0; s < C::kKs; ++s) {
             const u32x4_t w = p_l[nb] >= 0 ? qv[nb][s] : u32x4_t{0u, 0u, 0u, 0u};
@@ -422,9 +436,9 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     else wait_vmcnt<0>();
     ring_barrier();
 
-    f32x16_t sA[2], sB[2];       // scores of even / odd sub-tiles
-    bf16x8_t pA[2][2], pB[2][2];  // probabilities of even / odd sub-tiles
-    float ts[2];
+    f32x16_t sA[kNB], sB[kNB];       // scores of even / odd sub-tiles
+    bf16x8_t pA[kNB][2], pB[kNB][2];  // probabilities of even / odd sub-tiles
+    float ts[kNB];
     {
         bf16x8_t kf[C::kKs];
         read_k(0, kf);
@@ -434,14 +448,14 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     // Q kept in accumulation registers from here on (MFMA reads its B operand
     // from there), leaving the vector registers to K/V fragments and softmax
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
         for (int s = 0; s < C::kKs; ++s) asm volatile("" : "+a"(qf[nb][s]));
     // Sub-tile u with a successor: S(u+1) and PV(u-1) on the matrix cores
     // while the probabilities of u are formed.  An odd u first opens tile
     // (u+1)/2 (its loads done, the stage of tile (u+1)/2 - 2 free again).
-    auto body = [&](int u, f32x16_t (&cur)[2], f32x16_t (&nxt)[2], bf16x8_t (&pc)[2][2],
-                    const bf16x8_t (&pp)[2][2], bool has_prev, bool opens) {
+    auto body = [&](int u, f32x16_t (&cur)[kNB], f32x16_t (&nxt)[kNB], bf16x8_t (&pc)[kNB][2],
+                    const bf16x8_t (&pp)[kNB][2], bool has_prev, bool opens) {
         if (opens) {
             const int T = (u + 1) >> 1;
             if (T + 1 < n_kt) wait_vmcnt<C::kLoads>();
@@ -457,17 +471,23 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             s_mfma(kf, nxt);
             exp_pack(cur, pc, ts);
         } else {
-            // Steady state as a software pipeline of 4*kKs slots.  Slot k
-            // issues one MFMA, fenced off on its own: k%4 = 0, 1 are S^T
-            // k-step k/4 for column blocks 0, 1; k%4 = 2, 3 are PV step k/4.
-            // A fenced group of VALU work follows it: the scaled scores of
-            // this slot's values, the exponentials of the previous slot's, a
-            // bf16 pair conversion and a row-sum update further behind, and
-            // one LDS request for step k/4 + 2.  The strict alternation keeps
-            // the matrix pipe fed while the softmax arithmetic runs in its
-            // shadow, and no operation waits on its immediate predecessor.
-            constexpr int kSlots = 4 * C::kKs;
-            constexpr int kV = 32 / kSlots;  // probabilities formed per slot (1 or 2)
+            // Steady state as a software pipeline of 2*kNB*kKs slots.  Slot k
+            // issues one MFMA, fenced off on its own: within the 2*kNB slots
+            // of k-step j, the first kNB are S^T step j of the wave's column
+            // blocks, the other kNB PV step j.  A fenced group of VALU work
+            // follows it: the scaled scores of this slot's values, the
+            // exponentials of the previous slot's, a bf16 pair conversion and
+            // a row-sum update further behind, and the LDS requests for step
+            // j + 2.  The strict alternation keeps the matrix pipe fed while
+            // the softmax arithmetic runs in its shadow, and no operation
+            // waits on its immediate predecessor.
+            constexpr int kPer = 2 * kNB;              // slots per k-step
+            constexpr int kSlots = kPer * C::kKs;
+            constexpr int kVals = 16 * kNB;            // probabilities per lane per sub-tile
+            constexpr int kV = kVals / kSlots;         // formed per slot (1 or 2)
+            constexpr int kPairs = kVals / 2;
+            constexpr int kRdV0 = kNB == 1 ? 0 : 1;    // slots of the step that request V
+            constexpr int kRdV1 = kNB == 1 ? 1 : 2;
             auto cvt_slot = [](int q) { return (2 * q + 1) / kV + 2; };
             const uint32_t kb0 = stage_of(u + 1) + k_ro0;
             const uint32_t vb0 = stage_of(u - 1) + C::kTileBytes + v_ro0;
@@ -477,13 +497,18 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             auto rv = [&](int j, int hi) {
                 return __builtin_bit_cast(u32x2_t, v_half(vb0, j % C::kMd, 16 * (j / C::kMd) + 8 * hi));
             };
-            const float mc[2] = {m_run[0] * cl2, m_run[1] * cl2};
-            float fv[32], ev[32];
-            uint32_t pw[16];
+            float mc[kNB];
+#pragma unroll
+            for (int nb = 0; nb < kNB; ++nb) mc[nb] = m_run[nb] * cl2;
+            float fv[kVals], ev[kVals];
+            uint32_t pw[kPairs];
             bf16x8_t kf[C::kKs];
             u32x2_t vl[C::kKs], vh[C::kKs];
-            ts[0] = ts[1] = 0.0f;
-            nxt[0] = nxt[1] = f32x16_t{};
+#pragma unroll
+            for (int nb = 0; nb < kNB; ++nb) {
+                ts[nb] = 0.0f;
+                nxt[nb] = f32x16_t{};
+            }
 #pragma unroll
             for (int j = 0; j < 2 && j < C::kKs; ++j) {
                 kf[j] = rk(j);
@@ -492,19 +517,19 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             }
 #pragma unroll
             for (int k = 0; k < kSlots; ++k) {
-                const int j = k >> 2, kind = k & 3;
-                if (kind < 2) {
+                const int j = k / kPer, kind = k % kPer;
+                if (kind < kNB) {
                     nxt[kind] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[j], qf[kind][j], nxt[kind], 0, 0, 0);
                 } else {
                     const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4_t{vl[j][0], vl[j][1], vh[j][0], vh[j][1]});
-                    f32x16_t& o = oacc[kind - 2][j % C::kMd];
-                    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pp[kind - 2][j / C::kMd], o, 0, 0, 0);
+                    f32x16_t& o = oacc[kind - kNB][j % C::kMd];
+                    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pp[kind - kNB][j / C::kMd], o, 0, 0, 0);
                 }
                 __builtin_amdgcn_sched_barrier(0);
                 if (j + 2 < C::kKs) {
                     if (kind == 0) kf[j + 2] = rk(j + 2);
-                    if (kind == 1) vl[j + 2] = rv(j + 2, 0);
-                    if (kind == 2) vh[j + 2] = rv(j + 2, 1);
+                    if (kind == kRdV0) vl[j + 2] = rv(j + 2, 0);
+                    if (kind == kRdV1) vh[j + 2] = rv(j + 2, 1);
                 }
 #pragma unroll
                 for (int v = 0; v < kV; ++v) {
@@ -513,7 +538,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
                     if (k > 0) ev[f - kV] = __builtin_amdgcn_exp2f(fv[f - kV]);
                 }
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
+                for (int q = 0; q < kPairs; ++q) {
                     if (cvt_slot(q) == k)
                         pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
                     if (cvt_slot(q) + 1 == k) ts[q >> 3] += ev[2 * q] + ev[2 * q + 1];
@@ -522,17 +547,17 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             }
             // drain: the last slot's exponentials, conversions and sums
 #pragma unroll
-            for (int f = (kSlots - 1) * kV; f < 32; ++f) ev[f] = __builtin_amdgcn_exp2f(fv[f]);
+            for (int f = (kSlots - 1) * kV; f < kVals; ++f) ev[f] = __builtin_amdgcn_exp2f(fv[f]);
 #pragma unroll
-            for (int q = 0; q < 16; ++q)
+            for (int q = 0; q < kPairs; ++q)
                 if (cvt_slot(q) >= kSlots)
                     pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
 #pragma unroll
-            for (int q = 0; q < 16; ++q)
+            for (int q = 0; q < kPairs; ++q)
                 if (cvt_slot(q) + 1 >= kSlots) ts[q >> 3] += ev[2 * q] + ev[2 * q + 1];
             // word q = (nb, sp, w) with q = 8 nb + 4 sp + w
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
+            for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
                 for (int sp = 0; sp < 2; ++sp)
                     pc[nb][sp] = __builtin_bit_cast(bf16x8_t, u32x4_t{pw[8 * nb + 4 * sp], pw[8 * nb + 4 * sp + 1],
@@ -542,7 +567,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         mask(u + 1, nxt);
     };
     // The last sub-tile u: PV(u-1) while its probabilities are formed, then PV(u).
-    auto last = [&](int u, f32x16_t (&cur)[2], bf16x8_t (&pc)[2][2], const bf16x8_t (&pp)[2][2],
+    auto last = [&](int u, f32x16_t (&cur)[kNB], bf16x8_t (&pc)[kNB][2], const bf16x8_t (&pp)[kNB][2],
                     bool has_prev) {
         bf16x8_t vf[2][C::kMd];
         if (has_prev) {
@@ -570,7 +595,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             ++u;
         } else {  // u = n_sub - 1: its scores and the previous probabilities move to where the other path has them
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < kNB; ++nb) {
                 sA[nb] = sB[nb];
 #pragma unroll
                 for (int sp = 0; sp < 2; ++sp) pB[nb][sp] = pA[nb][sp];
@@ -582,13 +607,13 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     }
 
     // ---- results: oacc[nb][i][4r + e] = O[col][d = 32i + 8r + 4half + e]
-    float l_tot[2];
+    float l_tot[kNB];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) l_tot[nb] = l_run[nb] + __shfl_xor(l_run[nb], 32);
+    for (int nb = 0; nb < kNB; ++nb) l_tot[nb] = l_run[nb] + __shfl_xor(l_run[nb], 32);
     // the columns' rows and heads, recomputed rather than held through the loop
     int ln = (int)threadIdx.x & 63;
     asm volatile("" : "+v"(ln));
-    auto col_of = [&](int nb) { return 64 * wave + 32 * nb + (ln & 31); };
+    auto col_of = [&](int nb) { return 32 * (kNB * wave + nb) + (ln & 31); };
     auto store_out = [&](int nb, const f32x16_t (&o)[C::kMd], float inv) {
         const int c = col_of(nb);
         uint16_t* op =
@@ -605,7 +630,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     };
     if (slot < 0) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < kNB; ++nb)
             if (p_l[nb] >= 0) store_out(nb, oacc[nb], 1.0f / l_tot[nb]);
         return;
     }
@@ -613,8 +638,8 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     // piece of a cut row tile: publish its (m, l) and O / l in register order
     const int64_t sl = (int64_t)g * a.max_slots + slot;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        u32x2_t* po = a.part_o + ((sl * 4 + wave) * 2 + nb) * (C::kMd * 4 * 64) + lane;
+    for (int nb = 0; nb < kNB; ++nb) {
+        u32x2_t* po = a.part_o + (sl * 8 + kNB * wave + nb) * (C::kMd * 4 * 64) + lane;
         const float inv = l_tot[nb] > 0.0f ? 1.0f / l_tot[nb] : 0.0f;  // l = 0: no key of this piece
 #pragma unroll
         for (int i = 0; i < C::kMd; ++i)
@@ -641,7 +666,7 @@ __device__ __forceinline__ bool plan_fits(const AttnArgs& a, const int32_t* hdr)
 // Workgroup b serves kv head b % Hkv (with 8 kv heads each XCD serves one, so
 // its K/V stay in that XCD's L2) and walks range b / Hkv of the plan.
 template <int D>
-__global__ __launch_bounds__(256, 1) void attention_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * kNW, 1) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[ACfg<D>::kLds];
     const int b = blockIdx.x;
     const int g = b % a.Hkv;
@@ -901,7 +926,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(AttnArgs a) {
 template <int D>
 hipError_t launch(const AttnArgs& args, bool make_plan, hipStream_t s) {
     if (make_plan) hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, args);
-    hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(args.P * args.Hkv)), dim3(256), 0, s, args);
+    hipLaunchKernelGGL(attention_kernel<D>, dim3((unsigned)(args.P * args.Hkv)), dim3(64 * kNW), 0, s, args);
     hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)std::min(args.P * args.Hkv * 8, 2 * kCUs)), dim3(256), 0, s,
                        args);
     return hipGetLastError();
