@@ -267,11 +267,14 @@ semshare_status_t semshare_rope_table(const int32_t* sel_pos, int64_t n_sel, int
 
 /*
  * semshare_qkv_rope (bf16) with the RoPE factors from semshare_rope_table
- * (same sel_pos values, n_sel, n_tok and head_dim; rope_base is the table's).
- * The table stays owned by the caller and is only read.  Same results as
- * semshare_qkv_rope with that rope_base, bit for bit; a table of other
- * positions gives wrong results.  The workspace is the one
- * semshare_qkv_rope_workspace() sizes.  dtype FP32: SEMSHARE_E_UNSUPPORTED.
+ * (n_sel and head_dim as the table's; rope_base is the table's).  The table
+ * stays owned by the caller and is only read.  With a table of the same
+ * sel_pos values: the results of semshare_qkv_rope with that rope_base, bit
+ * for bit.  The rows the call writes are sel_pos; the rotation is the
+ * table's, so a table of the tokens' positions with sel_pos holding their
+ * rows in a compacted cache (semshare_retention_layer) recomputes the tokens
+ * of a layer whose cache holds the kept tokens only.  The workspace is the
+ * one semshare_qkv_rope_workspace() sizes.  dtype FP32: SEMSHARE_E_UNSUPPORTED.
  */
 semshare_status_t semshare_qkv_rope_tabled(const void* rope_table, size_t rope_table_bytes, const void* x_sel,
                                            const int32_t* sel_pos, int64_t n_sel, const void* wq, const void* wk,
@@ -371,6 +374,24 @@ semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, i
                                             int32_t* sel_pos, void* stream);
 
 /*
+ * The recompute set of a later layer, drawn from the previous layer's
+ * (Section 4.3.3: starting from the second layer, the tokens of a layer are
+ * chosen among those of the previous layer, Recomp[i] = T prod alpha_recomp[j]
+ * of Appendix A.5; by Insight 1 of Section 3 the ones with the largest KV
+ * deviation): of the n_cand candidates cand_pos (the previous layer's
+ * recomputed positions, strictly ascending) with deviations sigma (that
+ * layer's deviation_out, aligned with cand_pos), the n_sel with the largest
+ * deviation (ties: the lower position first), their positions written in
+ * ascending order.  The same one-workgroup radix selection as
+ * semshare_select_recompute.
+ *   sigma  [n_cand] float32 (non-negative, finite).   cand_pos [n_cand] int32.
+ *   sel_pos [n_sel] int32 (output; may not alias cand_pos).
+ *   n_cand <= 2^20;  0 <= n_sel <= n_cand.
+ */
+semshare_status_t semshare_select_recompute_nested(const float* sigma, const int32_t* cand_pos, int64_t n_cand,
+                                                   int64_t n_sel, int32_t* sel_pos, void* stream);
+
+/*
  * Average attention score of every token at a fully computed layer (Section
  * 3, Insight 2: the attention of each head averaged over the heads, then
  * over the query rows): mass[j] = sum_h sum_{i >= max(j, row_begin)}
@@ -413,6 +434,37 @@ semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, in
 semshare_status_t semshare_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
                                      const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos,
                                      int32_t* n_kept, void* stream);
+
+/*
+ * Retention on a later layer (Section 4.3.4: later layers keep fewer tokens;
+ * Appendix A.6: Retain[i] = T prod alpha_retain[j]) and the compaction plan of
+ * its cache.  Kept are the tokens whose first-layer rank (semshare_retention)
+ * is below n_retain, plus this layer's recomputed tokens sel_pos (never
+ * evicted: recomputing a token that is then dropped would waste the work), so
+ * the kept sets of layers with falling n_retain are nested apart from the
+ * recomputed tokens.  Written in ascending position order:
+ *   kept_pos[0 .. *n_kept)  the kept positions;
+ *   src_idx[j] = idx[kept_pos[j]]  the reference row each compacted cache row
+ *                copies (semshare_gather_kv with idx = src_idx and
+ *                n_tgt = *n_kept builds the compacted cache), when idx (the
+ *                match index, [n_tok]) is given;
+ *   sel_rows[i]  the row of sel_pos[i] in the compacted cache (-1 for a
+ *                position outside [0, n_tok)).  A layer's recomputed tokens
+ *                attend over its compacted cache when semshare_qkv_rope_tabled
+ *                (RoPE table of their positions sel_pos) and
+ *                semshare_prefill_attention take sel_rows as their positions
+ *                and *n_kept as n_tok: every kept token before a recomputed
+ *                one sits at a lower row, every later one at a higher row.
+ *   rank   [n_tok] int32 (a permutation of 0 .. n_tok-1; entries outside
+ *          [0, n_tok) count as not ranked).   sel_pos [n_sel] int32 strictly
+ *          ascending.   kept_pos, src_idx [n_tok] int32, sel_rows [n_sel]
+ *          int32, n_kept [1] int32 (outputs, device; src_idx and idx are
+ *          both NULL or both set).   n_tok <= 2^20.  0 <= n_retain.
+ */
+semshare_status_t semshare_retention_layer(const int32_t* rank, int32_t n_tok, int32_t n_retain,
+                                           const int32_t* sel_pos, int32_t n_sel, const int32_t* idx,
+                                           int32_t* kept_pos, int32_t* src_idx, int32_t* sel_rows, int32_t* n_kept,
+                                           void* stream);
 
 /*
  * Dynamic recompute set (Section 4.3.3 with the Attention Recovery equation

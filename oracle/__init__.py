@@ -58,7 +58,7 @@ def _load() -> ctypes.CDLL:
         "orc_gather_rows": (None, [P, P, I64, I64, P, I32, I64]),
         "orc_qkv_rows": (None, [P, P, I64, P, P, P, I32, I32, I32, I32, F64, P, P, P, INT]),
         "orc_deviation": (None, [P, P, P, I64, P, P, I32, P]),
-        "orc_attention_rows": (None, [P, P, I64, P, I64, P, P, I32, I32, I32, F64, P, INT]),
+        "orc_attention_rows": (None, [P, P, I64, P, I64, P, P, I32, I32, I32, F64, P, INT, P]),
         "orc_partial_prefill": (None, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, F64,
                                        P, P, INT]),
         "orc_select_recompute": (None, [P, I64, I64, P]),
@@ -183,9 +183,11 @@ def deviation(k_cache, v_cache, sel_pos, k_new, v_new) -> np.ndarray:
 
 
 def attention_rows(q, sel_pos, k_cache, v_cache, n_q_heads: int, n_kv_heads: int, head_dim: int,
-                   scale: float = 0.0, dtype: str = "f64", rows=None) -> np.ndarray:
+                   scale: float = 0.0, dtype: str = "f64", rows=None, keep=None) -> np.ndarray:
     """Causal attention of selected rows over a cache [n_tok, Hkv*D].
-    Returns [n_sel, Hq*D]; with ``rows`` only those rows are computed (others NaN)."""
+    Returns [n_sel, Hq*D]; with ``rows`` only those rows are computed (others NaN).
+    With ``keep`` (bool per cache position) only kept positions are attended
+    (the cache after retention, Section 4.3.4)."""
     q = _f64(q)
     pos = np.ascontiguousarray(sel_pos, dtype=np.int32)
     kc = _f64(k_cache).reshape(-1, n_kv_heads * head_dim)
@@ -194,9 +196,14 @@ def attention_rows(q, sel_pos, k_cache, v_cache, n_q_heads: int, n_kv_heads: int
         scale = 1.0 / np.sqrt(head_dim)
     out = np.full((pos.size, n_q_heads * head_dim), np.nan)
     r = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    kp = None
+    if keep is not None:
+        kp = np.ascontiguousarray(keep, dtype=np.uint8)
+        if kp.size != kc.shape[0]:
+            raise ValueError("keep needs one entry per cache position")
     _load().orc_attention_rows(_ptr(q), _ptr(pos), pos.size, _ptr(r), 0 if r is None else r.size,
                                _ptr(kc), _ptr(vc), n_q_heads, n_kv_heads, head_dim, float(scale),
-                               _ptr(out), _DT[dtype])
+                               _ptr(out), _DT[dtype], _ptr(kp))
     return out
 
 
@@ -227,6 +234,34 @@ def select_recompute(sigma, n_sel: int) -> np.ndarray:
     pos = np.empty(n_sel, dtype=np.int32)
     _load().orc_select_recompute(_ptr(s), s.size, n_sel, _ptr(pos))
     return pos
+
+
+def select_recompute_nested(sigma, cand_pos, n_sel: int) -> np.ndarray:
+    """A later layer's recompute set drawn from the previous layer's (Section
+    4.3.3, Appendix A.5): of the candidates cand_pos (ascending positions) with
+    deviations sigma, the n_sel of largest deviation, lower position first on
+    ties; their positions ascending."""
+    cand = np.ascontiguousarray(cand_pos, dtype=np.int64)
+    if cand.size != np.size(sigma):
+        raise ValueError("one deviation per candidate")
+    return cand[select_recompute(sigma, n_sel)].astype(np.int32)
+
+
+def retention_layer(rank, n_retain: int, sel_pos, idx=None):
+    """Retention on a later layer (Section 4.3.4, Appendix A.6): the positions
+    with first-layer rank below n_retain plus the recomputed sel_pos (never
+    evicted), ascending; the reference rows they copy (idx[kept]); the rows of
+    sel_pos in the compacted cache.  Returns (kept, src_idx or None, sel_rows)."""
+    rank = np.asarray(rank, dtype=np.int64)
+    keep = (rank >= 0) & (rank < n_retain)
+    sel = np.asarray(sel_pos, dtype=np.int64)
+    keep[sel[(sel >= 0) & (sel < rank.size)]] = True
+    kept = np.flatnonzero(keep)
+    row_of = np.full(rank.size, -1, dtype=np.int64)
+    row_of[kept] = np.arange(kept.size)
+    rows = np.array([row_of[p] if 0 <= p < rank.size else -1 for p in sel], dtype=np.int64)
+    src = None if idx is None else np.asarray(idx, dtype=np.int64)[kept]
+    return kept, src, rows
 
 
 def bank_similarity(tgt_codes, ref_codes, offsets, dmin: float = 0.0, dmax: float = 30.0):

@@ -264,11 +264,13 @@ void orc_deviation(const double* k_cache, const double* v_cache, const int32_t* 
  * h = G*g .. G*g+G-1 share kv head g).  O is rounded to the storage dtype.
  * Rows listed in `rows` (indices into the selected set) are computed; rows
  * == NULL means all n_sel rows.  out is [n_sel][Hq*D] (only listed rows are
- * written). */
+ * written).  With `keep` (one byte per cache position), only the positions
+ * j <= p with keep[j] != 0 are attended: the cache after retention evicted
+ * the others (Section 4.3.4); keep == NULL keeps every position. */
 void orc_attention_rows(const double* q, const int32_t* sel_pos, int64_t n_sel,
                         const int64_t* rows, int64_t n_rows, const double* k_cache,
                         const double* v_cache, int32_t n_q_heads, int32_t n_kv_heads,
-                        int32_t head_dim, double scale, double* out, int dt) {
+                        int32_t head_dim, double scale, double* out, int dt, const uint8_t* keep) {
     const int32_t G = n_q_heads / n_kv_heads;
     const int32_t nq = n_q_heads * head_dim, nkv = n_kv_heads * head_dim;
     const int64_t count = rows ? n_rows : n_sel;
@@ -283,6 +285,7 @@ void orc_attention_rows(const double* q, const int32_t* sel_pos, int64_t n_sel,
             const double* qh = q + s * (int64_t)nq + (int64_t)h * head_dim;
             double mx = -INFINITY;
             for (int64_t j = 0; j <= p; ++j) {
+                if (keep && !keep[j]) continue;
                 const double* kj = k_cache + j * (int64_t)nkv + (int64_t)g * head_dim;
                 double dot = 0.0;
                 for (int32_t i = 0; i < head_dim; ++i) dot += qh[i] * kj[i];
@@ -290,7 +293,11 @@ void orc_attention_rows(const double* q, const int32_t* sel_pos, int64_t n_sel,
                 if (sc[j] > mx) mx = sc[j];
             }
             double den = 0.0;
-            for (int64_t j = 0; j <= p; ++j) { sc[j] = exp(sc[j] - mx); den += sc[j]; }
+            for (int64_t j = 0; j <= p; ++j) {
+                if (keep && !keep[j]) { sc[j] = 0.0; continue; }  /* evicted: weight 0 */
+                sc[j] = exp(sc[j] - mx);
+                den += sc[j];
+            }
             /* every output element sums its products in ascending key order */
             double* o = out + s * (int64_t)nq + (int64_t)h * head_dim;
             for (int32_t i = 0; i < head_dim; ++i) acc[i] = 0.0;
@@ -384,7 +391,7 @@ void orc_partial_prefill(const double* x_sel, const int32_t* sel_pos, int64_t n_
     }
     if (out)
         orc_attention_rows(q, sel_pos, n_sel, NULL, 0, k_cache, v_cache, n_q_heads, n_kv_heads,
-                           head_dim, scale, out, dt);
+                           head_dim, scale, out, dt, NULL);
     free(q);
     free(k);
     free(v);

@@ -8,5 +8,5 @@ from .semshare import (  # noqa: F401
     last_error, load, lsh_encode, match, match_mfma,
     partial_prefill, partial_prefill_workspace_bytes, prefill_attention, prefill_attention_noalloc,
     prefill_attention_workspace_bytes,
-    qkv_rope, qkv_rope_dev_ref, qkv_rope_workspace_bytes, retention, rope_embed, rope_lsh_encode, rope_table, rope_table_bytes, select_recompute, version,
+    qkv_rope, qkv_rope_dev_ref, qkv_rope_workspace_bytes, retention, retention_layer, rope_embed, rope_lsh_encode, rope_table, rope_table_bytes, select_recompute, select_recompute_nested, version,
 )

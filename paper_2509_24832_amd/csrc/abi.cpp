@@ -155,6 +155,23 @@ semshare_status_t semshare_retention(const float* mass, const float* score, int3
                     "retention launch");
 }
 
+semshare_status_t semshare_retention_layer(const int32_t* rank, int32_t n_tok, int32_t n_retain,
+                                           const int32_t* sel_pos, int32_t n_sel, const int32_t* idx,
+                                           int32_t* kept_pos, int32_t* src_idx, int32_t* sel_rows, int32_t* n_kept,
+                                           void* stream) {
+    const char* fn = "retention_layer";
+    if (n_tok < 0 || n_sel < 0 || n_retain < 0) return fail(SEMSHARE_E_INVAL, "%s: negative size", fn);
+    if (n_tok > semshare::kMaxRetainTok)
+        return fail(SEMSHARE_E_UNSUPPORTED, "%s: n_tok must be <= %d", fn, semshare::kMaxRetainTok);
+    if (n_sel > n_tok) return fail(SEMSHARE_E_INVAL, "%s: n_sel > n_tok", fn);
+    if (!n_kept || (n_tok > 0 && (!rank || !kept_pos)) || (n_sel > 0 && (!sel_pos || !sel_rows)) ||
+        ((idx == nullptr) != (src_idx == nullptr)))
+        return fail(SEMSHARE_E_INVAL, "%s: null buffer (idx and src_idx go together)", fn);
+    return from_hip(semshare::launch_retention_layer(rank, n_tok, n_retain, sel_pos, n_sel, idx, kept_pos, src_idx,
+                                                     sel_rows, n_kept, (hipStream_t)stream),
+                    "retention_layer launch");
+}
+
 semshare_status_t semshare_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres,
                                              double w_hot, double w_cold, int32_t* sel_pos, int32_t* counts,
                                              void* stream) {
@@ -619,6 +636,17 @@ semshare_status_t semshare_select_recompute(const float* sigma, int64_t n_tok, i
     if (!sigma || !sel_pos) return fail(SEMSHARE_E_INVAL, "select_recompute: null buffer");
     return from_hip(semshare::launch_select_recompute(sigma, n_tok, n_sel, sel_pos, (hipStream_t)stream),
                     "select_recompute launch");
+}
+
+semshare_status_t semshare_select_recompute_nested(const float* sigma, const int32_t* cand_pos, int64_t n_cand,
+                                                   int64_t n_sel, int32_t* sel_pos, void* stream) {
+    if (n_cand < 0 || n_sel < 0 || n_sel > n_cand)
+        return fail(SEMSHARE_E_INVAL, "select_recompute_nested: need 0 <= n_sel <= n_cand");
+    if (n_cand > (int64_t(1) << 20)) return fail(SEMSHARE_E_UNSUPPORTED, "select_recompute_nested: n_cand must be <= 2^20");
+    if (n_sel == 0) return ok();
+    if (!sigma || !cand_pos || !sel_pos) return fail(SEMSHARE_E_INVAL, "select_recompute_nested: null buffer");
+    return from_hip(semshare::launch_select_recompute(sigma, n_cand, n_sel, sel_pos, (hipStream_t)stream, cand_pos),
+                    "select_recompute_nested launch");
 }
 
 size_t semshare_bank_similarity_workspace(int64_t n_tgt, int32_t n_prompts) {

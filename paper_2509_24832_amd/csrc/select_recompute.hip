@@ -8,7 +8,10 @@
 // finds its digit by a block-wide scan of the 256 counts.  A final pass
 // walks the positions in order and keeps every value > T plus the first
 // (n_sel - count(> T)) values == T, compacting with block-wide prefix sums,
-// which yields the ascending output directly.
+// which yields the ascending output directly.  With a candidate map the
+// values belong to candidates map[0 .. n) (ascending positions, e.g. the
+// tokens the previous layer recomputed) and the selected candidates'
+// positions are written instead of their indices.
 #include "semshare_internal.h"
 
 namespace semshare {
@@ -48,7 +51,8 @@ __device__ __forceinline__ void block_scan2(uint32_t a, uint32_t b, uint32_t& ea
 }
 
 __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ sigma, int32_t n_tok,
-                                                    int32_t n_sel, int32_t* __restrict__ out) {
+                                                    int32_t n_sel, const int32_t* __restrict__ map,
+                                                    int32_t* __restrict__ out) {
     __shared__ uint32_t hist[256];
     __shared__ uint32_t s_digit, s_need;
     __shared__ uint32_t sw[kWaves][2];
@@ -98,7 +102,7 @@ __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ si
         const uint32_t take = gt || (eq && eq_taken + e_eq < need);
         uint32_t e_take, e_d2, t_take, t_d2;
         block_scan2(take, 0u, e_take, e_d2, t_take, t_d2, sw);
-        if (take) out[base + e_take] = i;
+        if (take) out[base + e_take] = map ? map[i] : i;
         base += t_take;
         eq_taken += t_eq;
     }
@@ -107,8 +111,8 @@ __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ si
 }  // namespace
 
 hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
-                                   int32_t* sel_pos, hipStream_t s) {
-    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kT), 0, s, sigma, (int32_t)n_tok, (int32_t)n_sel,
+                                   int32_t* sel_pos, hipStream_t s, const int32_t* map) {
+    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kT), 0, s, sigma, (int32_t)n_tok, (int32_t)n_sel, map,
                        sel_pos);
     return hipGetLastError();
 }

@@ -75,6 +75,11 @@ hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* c
 
 // token count limit of the dynamic recompute selection (one workgroup, keys in LDS)
 constexpr int kMaxDynTok = 8192;
+// token count limit of the per-layer retention (one workgroup, one bit per position in LDS)
+constexpr int kMaxRetainTok = 1 << 20;
+hipError_t launch_retention_layer(const int32_t* rank, int32_t n_tok, int32_t n_retain, const int32_t* sel_pos,
+                                  int32_t n_sel, const int32_t* idx, int32_t* kept_pos, int32_t* src_idx,
+                                  int32_t* sel_rows, int32_t* n_kept, hipStream_t s);
 
 size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads);
 hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int64_t row_begin, int32_t n_q_heads,
@@ -97,7 +102,7 @@ hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_
                               const int32_t* except_pos = nullptr, int64_t n_except = 0);
 
 hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
-                                   int32_t* sel_pos, hipStream_t s);
+                                   int32_t* sel_pos, hipStream_t s, const int32_t* map = nullptr);
 
 size_t bank_similarity_workspace(int64_t n_tgt, int32_t n_prompts);
 hipError_t launch_bank_similarity(const uint64_t* tgt, int64_t n_tgt, const uint64_t* ref, int64_t n_ref,

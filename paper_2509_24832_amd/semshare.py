@@ -62,6 +62,8 @@ def load() -> ctypes.CDLL:
                                            P, P, P, SZ, I32, P]),
         "semshare_partial_prefill_workspace": (SZ, [I64, I64, I32, I32, I32, I32, I32]),
         "semshare_select_recompute": (I32, [P, I64, I64, P, P]),
+        "semshare_select_recompute_nested": (I32, [P, P, I64, I64, P, P]),
+        "semshare_retention_layer": (I32, [P, I32, I32, P, I32, P, P, P, P, P, P]),
         "semshare_attention_mass_workspace": (SZ, [I64, I32]),
         "semshare_attention_mass": (I32, [P, P, I64, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_retention": (I32, [P, P, I32, P, P, F64, P, P, P, P]),
@@ -592,6 +594,44 @@ def prefill_attention_noalloc(q: torch.Tensor, sel_pos: torch.Tensor, k_cache: t
     _call("semshare_prefill_attention_noalloc", _ptr(q), _ptr(sel_pos), n_sel, _ptr(k_cache), _ptr(v_cache), n_tok,
           n_q_heads, n_kv_heads, head_dim, float(sm_scale), _ptr(out), _dt(q), _stream())
     return out
+
+
+def select_recompute_nested(sigma: torch.Tensor, cand_pos: torch.Tensor, n_sel: int,
+                            out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The n_sel candidates (positions cand_pos, deviations sigma) of largest deviation (ties: lower
+    position), their positions ascending: a later layer's recompute set drawn from the previous one's."""
+    _dev(sigma, "sigma", torch.float32)
+    _dev(cand_pos, "cand_pos", torch.int32)
+    if cand_pos.numel() != sigma.numel():
+        raise ValueError("sigma and cand_pos must have one entry per candidate")
+    if out is None:
+        out = torch.empty(n_sel, dtype=torch.int32, device=sigma.device)
+    _dev(out, "out", torch.int32)
+    _call("semshare_select_recompute_nested", _ptr(sigma), _ptr(cand_pos), sigma.numel(), int(n_sel), _ptr(out),
+          _stream())
+    return out
+
+
+def retention_layer(rank: torch.Tensor, n_retain: int, sel_pos: torch.Tensor, idx: Optional[torch.Tensor] = None):
+    """Kept positions of a later layer (rank < n_retain, plus the recomputed sel_pos), ascending; the
+    reference row each compacted row copies (with idx); the recomputed tokens' rows in the compacted cache.
+    Returns (kept_pos [n_tok] (first n_kept valid), src_idx [n_tok] or None, sel_rows [n_sel], n_kept [1]),
+    all on the device."""
+    _dev(rank, "rank", torch.int32)
+    _dev(sel_pos, "sel_pos", torch.int32)
+    n_tok, n_sel = rank.numel(), sel_pos.numel()
+    kept = torch.empty(max(n_tok, 1), dtype=torch.int32, device=rank.device)
+    src = None
+    if idx is not None:
+        _dev(idx, "idx", torch.int32)
+        if idx.numel() < n_tok:
+            raise ValueError("idx needs one entry per position")
+        src = torch.empty(max(n_tok, 1), dtype=torch.int32, device=rank.device)
+    rows = torch.empty(max(n_sel, 1), dtype=torch.int32, device=rank.device)
+    n_kept = torch.empty(1, dtype=torch.int32, device=rank.device)
+    _call("semshare_retention_layer", _ptr(rank), n_tok, int(n_retain), _ptr(sel_pos), n_sel, _ptr(idx), _ptr(kept),
+          _ptr(src), _ptr(rows), _ptr(n_kept), _stream())
+    return kept, src, rows[:n_sel], n_kept
 
 
 def select_recompute(sigma: torch.Tensor, n_sel: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
