@@ -107,3 +107,37 @@ def check_cache_rows(dt, got, ref, before, sel, x_sel, w, rotated):
     assert np.all(err <= spacing + b), f"max excess {(err - spacing - b).max()}"
     if dt == "bf16":
         assert (bf16_ulp_distance(got[sel], ref[sel]) > 1).mean() < 1e-3
+
+
+# ---- integer decisions taken on floating-point values that each side
+# computes itself (GPU in fp32, oracle in fp64): equal, or, where the two
+# differ, valid for the oracle's values within the float tolerance tol
+
+def topk_valid(ref_keys: np.ndarray, chosen: np.ndarray, tol) -> bool:
+    """A set chosen as the k largest: no unchosen key exceeds a chosen one by more than tol."""
+    ref_keys = np.asarray(ref_keys, dtype=np.float64)
+    mask = np.zeros(ref_keys.size, bool)
+    mask[np.asarray(chosen, dtype=np.int64)] = True
+    if mask.all() or not mask.any():
+        return True
+    t = np.broadcast_to(np.asarray(tol, dtype=np.float64), ref_keys.shape)
+    return bool(ref_keys[mask].min() >= (ref_keys[~mask] - t[~mask] - t[mask].max()).max())
+
+
+def order_valid(ref_keys: np.ndarray, order: np.ndarray, tol) -> bool:
+    """An order by descending key: every key is at least every later key minus tol."""
+    k = np.asarray(ref_keys, dtype=np.float64)[np.asarray(order, dtype=np.int64)]
+    t = np.broadcast_to(np.asarray(tol, dtype=np.float64), np.shape(ref_keys))[np.asarray(order, dtype=np.int64)]
+    suffix_max = np.maximum.accumulate((k - t)[::-1])[::-1]
+    return bool(np.all(k[:-1] + t[:-1] >= suffix_max[1:])) if k.size > 1 else True
+
+
+def recovery_valid(ref_mass: np.ndarray, order: np.ndarray, ar: int, thres: float, tol_sum: float) -> bool:
+    """An AR taken on masses within tol of ref_mass: the first ar tokens of `order` reach thres of the
+    total within tol_sum, the first ar - 1 do not exceed it by more than tol_sum."""
+    m = np.asarray(ref_mass, dtype=np.float64)
+    tot = m.sum()
+    s = np.cumsum(m[np.asarray(order, dtype=np.int64)])
+    ok_hi = s[ar - 1] >= thres * tot - tol_sum
+    ok_lo = ar == 1 or s[ar - 2] < thres * tot + tol_sum
+    return bool(ok_hi and ok_lo)

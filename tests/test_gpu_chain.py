@@ -1,0 +1,293 @@
+"""End-to-end GPU chains against the oracle's chains (Sections 4.2 and 4.3):
+each side runs the whole path on its own values from the same seeded inputs,
+and every stage is compared.  Floating-point stages within their tolerances;
+integer decisions (codes, match indices, recompute sets, rankings, kept sets)
+equal, or, where the floating point of the two sides makes them differ,
+valid for the oracle's values within that stage's tolerance, after which the
+stages that depend on the differing decision are compared only where they do
+not depend on it.  Also the synthetic analogue of the Section 4.3.1
+observation: without positional encoding repeated tokens map to their first
+occurrence, with RoPE to the nearest one."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import paper_2509_24832_amd as ss
+import workloads
+from paper_2509_24832_amd.schedule import DynamicSchedule
+from workloads import CONFIGS
+
+from helpers import (announce, bf16_ulp, check_cache_rows, code_mismatch_ok, dev, dev_codes, dev_i32, host,
+                     host_codes, order_valid, recovery_valid, topk_valid)
+
+pytestmark = pytest.mark.gpu
+
+ATOL = 2e-2
+
+
+def _bits(c):
+    return np.unpackbits(np.ascontiguousarray(c).view(np.uint8), axis=1, bitorder="little")
+
+
+def _match_agreement(ct_g, cr_g, ct_o, cr_o, idx_g, idx_o):
+    """Match indices equal where the codes agree; where they differ, the GPU's
+    choice is within the flipped bits of the oracle's best distance."""
+    bt_g, br_g, bt_o, br_o = _bits(ct_g), _bits(cr_g), _bits(ct_o), _bits(cr_o)
+    flips_t = (bt_g != bt_o).sum(1)
+    flips_r = (br_g != br_o).sum(1)
+    diff = np.flatnonzero(idx_g != idx_o)
+    for t in diff:
+        d_best = int((bt_o[t] != br_o[idx_o[t]]).sum())
+        d_gpu = int((bt_o[t] != br_o[idx_g[t]]).sum())
+        assert d_gpu - d_best <= flips_t[t] + flips_r[idx_g[t]] + flips_r[idx_o[t]], t
+    return idx_g == idx_o
+
+
+def _codes(e, planes):
+    x = orc.rope_embed(e, dtype="bf16")
+    return x, orc.lsh_encode(x, planes)
+
+
+def _first_divergence(n_tok, *masks):
+    """The first position at which any per-position mask is False (n_tok if none)."""
+    bad = np.zeros(n_tok, bool)
+    for m in masks:
+        bad |= ~m
+    idx = np.flatnonzero(bad)
+    return int(idx[0]) if idx.size else n_tok
+
+
+def test_fixed_fraction_chain_config1():
+    """Config 1's shape (1024 tokens, hidden 4096, 32 q / 8 kv heads, 128-bit
+    LSH, recompute fraction 0.25) over two layers, the benchmark's sequence of
+    calls: RoPE + LSH, match, first layer with the deviation against the
+    matched reference rows, selection, gather of the second layer without the
+    recomputed rows, partial prefill of the second layer."""
+    cfg = CONFIGS[1]
+    T, d, hq, hkv, D, L = cfg.n_tok, cfg.dim, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, 2
+    n_sel = cfg.n_sel(cfg.recompute_fracs[0])
+    pair = workloads.make_prompt_pair(cfg)
+    planes = workloads.make_planes(cfg)
+    ws = [workloads.make_weights(cfg, l) for l in range(L)]
+    allpos = np.arange(T, dtype=np.int32)
+    announce("fixed-fraction chain, config 1 shape, 2 layers")
+    # ---- GPU chain
+    er, et, pl = dev(pair.e_ref, "bf16"), dev(pair.e_tgt, "bf16"), dev(planes, "bf16")
+    W = [tuple(dev(a, "bf16") for a in (w.wq, w.wk, w.wv)) for w in ws]
+    ap = dev_i32(allpos)
+    cr_g = ss.lsh_encode(ss.rope_embed(er), pl)
+    ref_k = torch.empty((L, T, hkv, D), dtype=torch.bfloat16, device="cuda")
+    ref_v = torch.empty_like(ref_k)
+    for l in range(L):
+        ss.qkv_rope(er, ap, None, W[l][1], W[l][2], ref_k[l], ref_v[l], hq, hkv, want_q=False)
+    ct_g = ss.rope_lsh_encode(et, pl)
+    idx_g_t, _ = ss.match_mfma(ct_g, cr_g)
+    asm_k, asm_v = torch.empty_like(ref_k), torch.empty_like(ref_v)
+    q0, sig0 = ss.qkv_rope_dev_ref(et, ap, *W[0], asm_k[0], asm_v[0], hq, hkv, ref_k[0], ref_v[0], idx_g_t)
+    out0 = ss.prefill_attention(q0, ap, asm_k[0], asm_v[0], hkv)
+    sel_t = ss.select_recompute(sig0, n_sel)
+    ss.gather_kv(ref_k[1:], ref_v[1:], idx_g_t, out_k=asm_k[1:], out_v=asm_v[1:], except_pos=sel_t)
+    q1, _ = ss.qkv_rope(ss.gather_rows(et, sel_t), sel_t, *W[1], asm_k[1], asm_v[1], hq, hkv)
+    out1 = ss.prefill_attention(q1, sel_t, asm_k[1], asm_v[1], hkv)
+    # ---- oracle chain
+    xr, cr_o = _codes(pair.e_ref, planes)
+    xt, ct_o = _codes(pair.e_tgt, planes)
+    for got, want, x in ((host_codes(cr_g), cr_o, xr), (host_codes(ct_g), ct_o, xt)):
+        _, outside = code_mismatch_ok(got, want, orc.lsh_project(x, planes), x, planes)
+        assert outside == 0
+    idx_o, _ = orc.match(ct_o, cr_o)
+    idx_g = idx_g_t.cpu().numpy()
+    idx_same = _match_agreement(host_codes(ct_g), host_codes(cr_g), ct_o, cr_o, idx_g, idx_o)
+    copied = pair.pi >= 0
+    assert (idx_o[copied] == pair.pi[copied]).mean() > 0.5  # match quality: most copied tokens find their source
+    kr, vr = [], []
+    for l in range(L):
+        _, k_l, v_l = orc.qkv_rows(pair.e_ref, allpos, ws[l].wq, ws[l].wk, ws[l].wv, hq, hkv, D, dtype="bf16",
+                                   want_q=False)
+        check_cache_rows("bf16", host(ref_k[l]), k_l, k_l, allpos, pair.e_ref, ws[l].wk, True)
+        kr.append(k_l)
+        vr.append(v_l)
+    q0_o, kn0, vn0 = orc.qkv_rows(pair.e_tgt, allpos, ws[0].wq, ws[0].wk, ws[0].wv, hq, hkv, D, dtype="bf16")
+    sig0_o = orc.deviation(kr[0][idx_o], vr[0][idx_o], allpos, kn0, vn0)
+    sig0_g = host(sig0)
+    assert np.allclose(sig0_g[idx_same], sig0_o[idx_same], rtol=1e-3, atol=1e-3)
+    check_cache_rows("bf16", host(asm_k[0]), kn0, kn0, allpos, pair.e_tgt, ws[0].wk, True)
+    rows = np.unique(np.concatenate([[0, T - 1], np.random.default_rng(1).choice(T, 30, replace=False)]))
+    want0 = orc.attention_rows(q0_o[rows], allpos[rows], kn0, vn0, hq, hkv, D, dtype="bf16")
+    assert np.abs(host(out0).reshape(T, -1)[rows] - want0).max() <= ATOL
+    # the selection: equal, or a valid top-n_sel for the oracle's deviations
+    sel_o = orc.select_recompute(sig0_o, n_sel)
+    sel_g = sel_t.cpu().numpy()
+    if not np.array_equal(sel_g, sel_o):
+        # among the tokens whose match agrees, the GPU's choice is a valid top set for the oracle's deviations
+        sub = np.flatnonzero(idx_same)
+        chosen = np.flatnonzero(np.isin(sub, sel_g))
+        assert topk_valid(sig0_o[sub], chosen, 1e-3 * np.abs(sig0_o[sub]) + 1e-3)
+    # the second layer, compared where nothing it depends on differs
+    in_g = np.zeros(T, bool)
+    in_g[sel_g] = True
+    in_o = np.zeros(T, bool)
+    in_o[sel_o] = True
+    p_cut = _first_divergence(T, idx_same, in_g == in_o)
+    xs = pair.e_tgt[sel_o]
+    q1_o, kn1, vn1 = orc.qkv_rows(xs, sel_o, ws[1].wq, ws[1].wk, ws[1].wv, hq, hkv, D, dtype="bf16")
+    k1, v1 = kr[1][idx_o].copy(), vr[1][idx_o].copy()
+    k1[sel_o], v1[sel_o] = kn1, vn1
+    common = np.flatnonzero(sel_o < p_cut)
+    if common.size == 0:  # every recomputed row depends on a decision that differs (validly, checked above)
+        return
+    pick = common[np.unique(np.linspace(0, common.size - 1, 24).astype(int))]
+    want1 = orc.attention_rows(q1_o[pick], sel_o[pick], k1, v1, hq, hkv, D, dtype="bf16")
+    row_g = np.searchsorted(sel_g, sel_o[pick])
+    assert np.abs(host(out1).reshape(n_sel, -1)[row_g] - want1).max() <= ATOL
+
+
+def test_dynamic_schedule_chain():
+    """The dynamic schedule (first layer in full, average attention score ->
+    AR -> recompute set, window score -> retention ranking, nested recompute
+    sets and compacted caches on later layers) over three layers of 1024
+    tokens, hidden 512, 16 q / 4 kv heads, against the oracle's chain."""
+    cfg = CONFIGS[1]
+    T, d, hq, hkv, D, L = 1024, 512, 16, 4, 128, 3
+    alpha_recomp, alpha_retain = [1.0, 1.0, 0.7], [1.0, 0.95, 0.9]
+    pair = workloads.make_prompt_pair(cfg, dim=d)
+    planes = workloads.make_planes(cfg, dim=d)
+    ws = [workloads.make_weights(cfg, 20 + l, hidden=d, n_q_heads=hq, n_kv_heads=hkv, head_dim=D) for l in range(L)]
+    allpos = np.arange(T, dtype=np.int32)
+    announce("dynamic schedule chain: 1024 tokens, 3 layers")
+    # ---- GPU chain
+    er, et, pl = dev(pair.e_ref, "bf16"), dev(pair.e_tgt, "bf16"), dev(planes, "bf16")
+    W = [tuple(dev(a, "bf16") for a in (w.wq, w.wk, w.wv)) for w in ws]
+    ap = dev_i32(allpos)
+    cr_g = ss.lsh_encode(ss.rope_embed(er), pl)
+    ref_k = torch.empty((L, T, hkv, D), dtype=torch.bfloat16, device="cuda")
+    ref_v = torch.empty_like(ref_k)
+    for l in range(L):
+        ss.qkv_rope(er, ap, None, W[l][1], W[l][2], ref_k[l], ref_v[l], hq, hkv, want_q=False)
+    sched = DynamicSchedule(T, d, L, hq, hkv, D, 2, alpha_recomp, alpha_retain)
+    rec = sched.run(et, pl, cr_g, ref_k, ref_v, W, record=True)
+    # ---- oracle chain, stage by stage
+    _, cr_o = _codes(pair.e_ref, planes)
+    _, ct_o = _codes(pair.e_tgt, planes)
+    idx_o, _ = orc.match(ct_o, cr_o)
+    idx_g = rec.idx.cpu().numpy()
+    idx_same = _match_agreement(host_codes(sched.codes), host_codes(cr_g), ct_o, cr_o, idx_g, idx_o)
+    kr, vr = [], []
+    for l in range(L):
+        _, k_l, v_l = orc.qkv_rows(pair.e_ref, allpos, ws[l].wq, ws[l].wk, ws[l].wv, hq, hkv, D, dtype="bf16",
+                                   want_q=False)
+        kr.append(k_l)
+        vr.append(v_l)
+    q0_o, kn0, vn0 = orc.qkv_rows(pair.e_tgt, allpos, ws[0].wq, ws[0].wk, ws[0].wv, hq, hkv, D, dtype="bf16")
+    sig0_o = orc.deviation(kr[0][idx_o], vr[0][idx_o], allpos, kn0, vn0)
+    assert np.allclose(host(rec.sigma0)[idx_same], sig0_o[idx_same], rtol=1e-3, atol=1e-3)
+    # masses of the first layer
+    m_o = orc.attention_mass_cols(q0_o, kn0, hq, hkv, D)
+    m_g = host(rec.mass)
+    tol_m = 1e-4 * m_o + 1e-9
+    assert np.all(np.abs(m_g - m_o) <= tol_m)
+    ar_g, n1_g, nh_g = rec.counts
+    order_g = np.array(sorted(range(T), key=lambda j: (-float(m_g[j]), j)))
+    assert order_valid(m_o, order_g, tol_m)
+    ar_o, sel1_o, nh_o = orc.dynamic_recompute(m_o.astype(np.float32), sig0_o.astype(np.float32))
+    assert ar_g == ar_o or recovery_valid(m_o, order_g, ar_g, 0.55, float(tol_m.sum()))
+    sel1_g = sched.sel1.cpu().numpy()[:n1_g]
+    _, order_o = orc.attention_recovery(m_o.astype(np.float32))
+    same_hot = np.array_equal(np.sort(order_g[:ar_g]), np.sort(order_o[:ar_o]))
+    if not (ar_g == ar_o and same_hot and nh_g == nh_o and np.array_equal(sel1_g, sel1_o) and idx_same.all()):
+        # a decision taken on floating-point values differs validly: the stages after it depend on it
+        announce("dynamic chain: compared through the masses (a valid near-tie in AR or the recompute set (a valid near-tie follows)")
+        return
+    # the window score and the retention ranking
+    sc_o = orc.attention_mass_cols(q0_o, kn0, hq, hkv, D, row_begin=rec.row_begin)
+    tol_s = 1e-4 * sc_o + 1e-9
+    assert np.all(np.abs(host(rec.score) - sc_o) <= tol_s)
+    rank_o, kept0_o, nk0_o = orc.retention(m_o.astype(np.float32), sc_o.astype(np.float32), ar_o, sel1_o, 0.8)
+    rank_g = rec.rank.cpu().numpy()[:T]
+    order_rank = np.argsort(rank_g)
+    forced = np.zeros(T, bool)
+    forced[order_g[:ar_g]] = True
+    forced[sel1_g] = True
+    n_f = int(forced.sum())
+    assert np.array_equal(order_rank[:n_f], np.flatnonzero(forced))
+    assert order_valid(sc_o, order_rank[n_f:], tol_s)
+    assert rec.n_kept0 == nk0_o
+    # later layers: nested recompute sets and compacted caches
+    s_prev_o, sig_prev_o, n_prev, retain = sel1_o, None, n1_g, float(nk0_o)
+    for l in range(1, L):
+        lr = rec.layers[l - 1]
+        if l == 1:
+            s_o = sel1_o
+        else:
+            n_l = max(1, min(n_prev, int(math.floor(n_prev * alpha_recomp[l] + 0.5))))
+            s_o = orc.select_recompute_nested(sig_prev_o, s_prev_o, n_l)
+        s_g = lr.sel.cpu().numpy()
+        if not np.array_equal(s_g, s_o):
+            assert topk_valid(sig_prev_o, np.searchsorted(s_prev_o, s_g), 1e-3 * sig_prev_o + 1e-3)
+            announce(f"dynamic chain: compared through layer {l - 1} (a valid near-tie in layer {l}'s set)")
+            return
+        retain *= alpha_retain[l]
+        kept_o, _, rows_o = orc.retention_layer(rank_o, int(math.floor(retain + 0.5)), s_o)
+        kept_g = lr.kept.cpu().numpy()
+        if not np.array_equal(kept_g, kept_o):
+            # rankings that differ only among near-equal window scores place a different token at the boundary
+            assert kept_g.size == kept_o.size and np.setdiff1d(kept_g, kept_o).size <= 2
+            announce(f"dynamic chain: compared through layer {l - 1} (a valid near-tie in layer {l}'s kept set)")
+            return
+        assert np.array_equal(lr.rows.cpu().numpy(), rows_o)
+        q_o, kn, vn = orc.qkv_rows(pair.e_tgt[s_o], s_o, ws[l].wq, ws[l].wk, ws[l].wv, hq, hkv, D, dtype="bf16")
+        kf, vf = kr[l][idx_o].copy(), vr[l][idx_o].copy()
+        sig_o = orc.deviation(kf, vf, s_o, kn, vn)
+        assert np.allclose(host(lr.sigma), sig_o, rtol=1e-3, atol=1e-3)
+        kf[s_o], vf[s_o] = kn, vn
+        keep = np.zeros(T, bool)
+        keep[kept_o] = True
+        pick = np.unique(np.linspace(0, s_o.size - 1, 16).astype(int))
+        want = orc.attention_rows(q_o[pick], s_o[pick], kf, vf, hq, hkv, D, dtype="bf16", keep=keep)
+        assert np.abs(host(lr.out).reshape(s_o.size, -1)[pick] - want).max() <= ATOL
+        s_prev_o, sig_prev_o, n_prev = s_o, sig_o, s_o.size
+    # the cache kept over the layers (the memory retention saves)
+    assert rec.kv_rows_kept(T, L) < 1.0
+    announce(f"dynamic chain: every layer compared; {rec.kv_rows_kept(T, L):.3f} of the cache rows kept")
+
+
+def test_rope_locality_repeated_tokens():
+    """Section 4.3.1's observation on synthetic prompts: a reference whose 1024
+    tokens repeat a vocabulary of 32 embeddings, a target copying it with
+    noise.  Matched on the plain embeddings, equal codes tie and the lowest
+    index wins: target tokens map to the first occurrences near the start.
+    With RoPE injected before hashing, each matches an occurrence near its own
+    position.  The GPU's match indices agree with the oracle's where the codes
+    agree."""
+    cfg = CONFIGS[1]
+    T, d, vocab = 1024, 256, 32
+    r = np.random.default_rng(33)
+    emb = r.standard_normal((vocab, d)).astype(np.float32)
+    tok = r.integers(0, vocab, T)
+    e_ref = workloads.round_bf16(emb[tok])
+    noise = 0.05 * np.linalg.norm(emb[tok], axis=1, keepdims=True) / np.sqrt(d) * r.standard_normal((T, d))
+    e_tgt = workloads.round_bf16((emb[tok] + noise).astype(np.float32))
+    planes = workloads.make_planes(cfg, n_bits=128, dim=d)
+    announce("RoPE locality: repeated tokens")
+    pl = dev(planes, "bf16")
+    found = {}
+    for rope in (False, True):
+        xt = ss.rope_embed(dev(e_tgt, "bf16")) if rope else dev(e_tgt, "bf16")
+        xr = ss.rope_embed(dev(e_ref, "bf16")) if rope else dev(e_ref, "bf16")
+        ct, cr = ss.lsh_encode(xt, pl), ss.lsh_encode(xr, pl)
+        idx, _ = ss.match_mfma(ct, cr)
+        idx = idx.cpu().numpy()
+        xt_o = orc.rope_embed(e_tgt, dtype="bf16") if rope else e_tgt.astype(np.float64)
+        xr_o = orc.rope_embed(e_ref, dtype="bf16") if rope else e_ref.astype(np.float64)
+        ct_o, cr_o = orc.lsh_encode(xt_o, planes), orc.lsh_encode(xr_o, planes)
+        idx_o, _ = orc.match(ct_o, cr_o)
+        _match_agreement(host_codes(ct), host_codes(cr), ct_o, cr_o, idx, idx_o)
+        assert (tok[idx_o] == tok).mean() > 0.9  # the same vocabulary entry either way
+        found[rope] = idx_o
+    first = np.array([np.flatnonzero(tok == v)[0] for v in range(vocab)])
+    assert np.mean(found[False] == first[tok]) > 0.9   # plain embeddings: the first occurrence
+    dist = {k: np.abs(v - np.arange(T)) for k, v in found.items()}
+    assert np.median(dist[True]) < 0.25 * np.median(dist[False])  # RoPE: an occurrence nearby
