@@ -429,7 +429,8 @@ semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, in
  * Compacting the cache is semshare_gather_kv with idx = kept_pos.
  *   mass, score  [n_tok] float32;  sel_pos, counts: the outputs of
  *   semshare_dynamic_recompute (device).   rank, kept_pos [n_tok] int32,
- *   n_kept [1] int32 (outputs, device).   n_tok <= 8192.
+ *   n_kept [1] int32 (outputs, device).   n_tok <= 65536 (beyond 8192 the
+ *   ranking is counted by many workgroups, same results).
  */
 semshare_status_t semshare_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
                                      const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos,
@@ -479,7 +480,9 @@ semshare_status_t semshare_retention_layer(const int32_t* rank, int32_t n_tok, i
  *   mass, sigma  [n_tok] float32 (sigma >= 0, as deviation_out gives)
  *   sel_pos      [n_tok] int32 (output; the first counts[1] are written)
  *   counts       [3] int32 (output, device): AR, number selected, of them hot
- *   n_tok <= 8192 (one workgroup), else SEMSHARE_E_UNSUPPORTED.
+ *   n_tok <= 65536, else SEMSHARE_E_UNSUPPORTED (up to 8192 one workgroup
+ *   sorts the keys; beyond, ranks are counted by many workgroups, with the
+ *   same keys and the same results).
  *   thres, w_hot, w_cold in [0, 1].
  */
 semshare_status_t semshare_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres,

@@ -144,9 +144,9 @@ semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, in
 semshare_status_t semshare_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
                                      const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos,
                                      int32_t* n_kept, void* stream) {
-    if (n_tok < 0 || n_tok > semshare::kMaxDynTok)
+    if (n_tok < 0 || n_tok > semshare::kMaxDynTokLarge)
         return fail(n_tok < 0 ? SEMSHARE_E_INVAL : SEMSHARE_E_UNSUPPORTED, "retention: n_tok must be in [0, %d]",
-                    semshare::kMaxDynTok);
+                    semshare::kMaxDynTokLarge);
     if (!(min_keep >= 0.0 && min_keep <= 1.0)) return fail(SEMSHARE_E_INVAL, "retention: min_keep must lie in [0, 1]");
     if (!counts || !n_kept || (n_tok > 0 && (!mass || !score || !sel_pos || !rank || !kept_pos)))
         return fail(SEMSHARE_E_INVAL, "retention: null buffer");
@@ -175,9 +175,9 @@ semshare_status_t semshare_retention_layer(const int32_t* rank, int32_t n_tok, i
 semshare_status_t semshare_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres,
                                              double w_hot, double w_cold, int32_t* sel_pos, int32_t* counts,
                                              void* stream) {
-    if (n_tok < 0 || n_tok > semshare::kMaxDynTok)
+    if (n_tok < 0 || n_tok > semshare::kMaxDynTokLarge)
         return fail(n_tok < 0 ? SEMSHARE_E_INVAL : SEMSHARE_E_UNSUPPORTED, "dynamic_recompute: n_tok must be in [0, %d]",
-                    semshare::kMaxDynTok);
+                    semshare::kMaxDynTokLarge);
     if (!(thres >= 0.0 && thres <= 1.0) || !(w_hot >= 0.0 && w_hot <= 1.0) || !(w_cold >= 0.0 && w_cold <= 1.0))
         return fail(SEMSHARE_E_INVAL, "dynamic_recompute: thres, w_hot and w_cold must lie in [0, 1]");
     if (!counts || (n_tok > 0 && (!mass || !sigma || !sel_pos)))

@@ -456,6 +456,8 @@ __global__ __launch_bounds__(kSelThreads) void retention_kernel(const float* __r
 hipError_t launch_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
                             const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos, int32_t* n_kept,
                             hipStream_t s) {
+    if (n_tok > kMaxDynTok)
+        return launch_retention_large(mass, score, n_tok, sel_pos, counts, min_keep, rank, kept_pos, n_kept, s);
     hipLaunchKernelGGL(retention_kernel, dim3(1), dim3(kSelThreads), 0, s, mass, score, n_tok, sel_pos, counts,
                        min_keep, rank, kept_pos, n_kept);
     return hipGetLastError();
@@ -484,6 +486,8 @@ hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, in
 
 hipError_t launch_dynamic_recompute(const float* mass, const float* sigma, int32_t n_tok, double thres, double w_hot,
                                     double w_cold, int32_t* sel_pos, int32_t* counts, hipStream_t s) {
+    if (n_tok > kMaxDynTok)
+        return launch_dynamic_recompute_large(mass, sigma, n_tok, thres, w_hot, w_cold, sel_pos, counts, s);
     hipLaunchKernelGGL(dyn_select_kernel, dim3(1), dim3(kSelThreads), 0, s, mass, sigma, n_tok, thres, w_hot, w_cold,
                        sel_pos, counts);
     return hipGetLastError();

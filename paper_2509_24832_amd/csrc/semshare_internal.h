@@ -73,8 +73,17 @@ hipError_t launch_lsh_encode(const void* x, const void* planes, uint64_t* codes,
 hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* codes, int64_t n_tok, int32_t dim,
                                   int32_t n_bits, int64_t pos0, double base, hipStream_t s);
 
-// token count limit of the dynamic recompute selection (one workgroup, keys in LDS)
+// token count limit of the dynamic recompute selection and first-layer
+// retention sorted in one workgroup (keys in LDS); up to kMaxDynTokLarge they
+// rank by counting (rank_select.hip)
 constexpr int kMaxDynTok = 8192;
+constexpr int kMaxDynTokLarge = 65536;
+hipError_t launch_dynamic_recompute_large(const float* mass, const float* sigma, int32_t n, double thres,
+                                          double w_hot, double w_cold, int32_t* sel_pos, int32_t* counts,
+                                          hipStream_t s);
+hipError_t launch_retention_large(const float* mass, const float* score, int32_t n, const int32_t* sel_pos,
+                                  const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos,
+                                  int32_t* n_kept, hipStream_t s);
 // token count limit of the per-layer retention (one workgroup, one bit per position in LDS)
 constexpr int kMaxRetainTok = 1 << 20;
 hipError_t launch_retention_layer(const int32_t* rank, int32_t n_tok, int32_t n_retain, const int32_t* sel_pos,

@@ -100,7 +100,8 @@ def test_attention_mass_and_dynamic_validation(lib):
     assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, None, FAKE, ws, 1, None) == b.E_INVAL  # null mass
     assert _st(e, None, None, 0, 0, 32, 8, 128, 0.0, None, None, 0, 1, None) == b.OK
     d = "semshare_dynamic_recompute"
-    assert _st(d, FAKE, FAKE, 8193, 0.55, 0.5, 0.1, FAKE, FAKE, None) == b.E_UNSUPPORTED
+    assert _st(d, FAKE, FAKE, 65537, 0.55, 0.5, 0.1, FAKE, FAKE, None) == b.E_UNSUPPORTED
+    assert _st("semshare_retention", FAKE, FAKE, 65537, FAKE, FAKE, 0.8, FAKE, FAKE, FAKE, None) == b.E_UNSUPPORTED
     assert _st(d, FAKE, FAKE, -1, 0.55, 0.5, 0.1, FAKE, FAKE, None) == b.E_INVAL
     assert _st(d, FAKE, FAKE, 10, 1.5, 0.5, 0.1, FAKE, FAKE, None) == b.E_INVAL
     assert _st(d, FAKE, FAKE, 10, 0.55, float("nan"), 0.1, FAKE, FAKE, None) == b.E_INVAL

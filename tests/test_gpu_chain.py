@@ -199,7 +199,7 @@ def test_dynamic_schedule_chain():
     same_hot = np.array_equal(np.sort(order_g[:ar_g]), np.sort(order_o[:ar_o]))
     if not (ar_g == ar_o and same_hot and nh_g == nh_o and np.array_equal(sel1_g, sel1_o) and idx_same.all()):
         # a decision taken on floating-point values differs validly: the stages after it depend on it
-        announce("dynamic chain: compared through the masses (a valid near-tie in AR or the recompute set (a valid near-tie follows)")
+        announce("dynamic chain: compared through the masses (a valid near-tie in AR or the recompute set follows)")
         return
     # the window score and the retention ranking
     sc_o = orc.attention_mass_cols(q0_o, kn0, hq, hkv, D, row_begin=rec.row_begin)

@@ -142,7 +142,8 @@ def _oracle_dyn(m, s, ar_gpu, **kw):
 
 
 @pytest.mark.parametrize("T,seed,ties", [(1, 0, False), (7, 1, False), (100, 2, True), (1000, 3, False),
-                                         (5120, 4, False), (5120, 5, True), (8192, 6, False)])
+                                         (5120, 4, False), (5120, 5, True), (8192, 6, False), (8193, 7, False),
+                                         (32768, 8, False), (32768, 9, True), (65536, 10, False)])
 def test_dynamic_recompute_matches_oracle(T, seed, ties):
     announce(f"dynamic recompute T={T} ties={ties}")
     m, s = _dyn_inputs(T, seed, ties)
@@ -191,7 +192,9 @@ def test_window_mass_matches_oracle(T, row_begin):
 
 
 @pytest.mark.parametrize("T,seed,ties,min_keep", [(1, 0, False, 0.8), (50, 1, True, 0.8), (1000, 2, False, 0.8),
-                                                  (5120, 3, False, 0.8), (5120, 4, True, 0.5), (8192, 5, False, 1.0)])
+                                                  (5120, 3, False, 0.8), (5120, 4, True, 0.5), (8192, 5, False, 1.0),
+                                                  (8193, 6, False, 0.8), (32768, 7, True, 0.8),
+                                                  (65536, 8, False, 0.8)])
 def test_retention_matches_oracle(T, seed, ties, min_keep):
     announce(f"retention T={T} ties={ties} min_keep={min_keep}")
     m, s = _dyn_inputs(T, seed, ties)
