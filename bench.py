@@ -76,8 +76,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "59404c5679c56e4f02c3ee28f4124f25ea63005f56862afd0c84ed45830ddba9",
-                "bytes_per_call": 94964455}
+ATTN_TRAFFIC = {"source_sha256": "411ab50bbf55f049646863a85b8e5a556db5f1450d31181c6eb560714be8a11b",
+                "bytes_per_call": 95690828}
 
 
 def source_sha256(rel):
@@ -162,22 +162,24 @@ class Path:
                    ss.prefill_attention_workspace_bytes(n, self.T, self.hq, self.hkv, self.D, bf))
         self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
 
-    def step(self, mark=None):
-        """One pass of the hot path.  mark(name) records a boundary event when given."""
+    # ---- the stages of one step, in order; the per-layer ones take the layer
+    def s_encode(self):
         ss = self.ss
-        m = mark or (lambda name: None)
-        hq, hkv = self.hq, self.hkv
-        m("start")
         if self.fused_encode:
             ss.rope_lsh_encode(self.e_tgt, self.planes, out=self.codes_t)
-            m("rope_lsh")
         else:
             ss.rope_embed(self.e_tgt, out=self.e_rot)
-            m("rope")
             ss.lsh_encode(self.e_rot, self.planes, out=self.codes_t)
-            m("lsh")
+
+    def s_match(self):
         self.matcher(self.codes_t, self.codes_ref, idx=self.idx, dist=self.dist)
-        m("match")
+
+    def s_gather(self):
+        if not self.gather_except:
+            self.ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
+
+    def s_qkv0(self):
+        ss, hq, hkv = self.ss, self.hq, self.hkv
         wq, wk, wv = self.w[0]
         if self.gather_except:
             # layer 0 recomputes every row, so its gathered rows would feed the deviation only: it reads the
@@ -187,67 +189,106 @@ class Path:
                                 self.ref_k[0], self.ref_v[0], self.idx, q_out=self.q_full, deviation=self.sigma,
                                 workspace=self.ws)
         else:
-            ss.gather_kv(self.ref_k, self.ref_v, self.idx, out_k=self.asm_k, out_v=self.asm_v)
-            m("gather")
             ss.qkv_rope(self.e_tgt, self.allpos, wq, wk, wv, self.asm_k[0], self.asm_v[0], hq, hkv,
                         q_out=self.q_full, deviation=self.sigma, want_deviation=True, workspace=self.ws)
-        m("qkv0")
-        ss.prefill_attention(self.q_full, self.allpos, self.asm_k[0], self.asm_v[0], hkv, out=self.out_full,
-                             workspace=self.ws)
-        m("attn0")
+
+    def s_attn0(self):
+        self.ss.prefill_attention(self.q_full, self.allpos, self.asm_k[0], self.asm_v[0], self.hkv, out=self.out_full,
+                                  workspace=self.ws)
+
+    def s_select(self):
+        ss = self.ss
         ss.select_recompute(self.sigma, self.n_sel, out=self.sel)
-        ss.attention_plan(self.sel, self.T, hq, hkv, self.D, out=self.plan)
+        ss.attention_plan(self.sel, self.T, self.hq, self.hkv, self.D, out=self.plan)
         ss.rope_table(self.sel, self.T, self.D, out=self.rope_sel)
-        m("select")
+
+    def s_gather_rest(self):
         if self.gather_except:
-            ss.gather_kv(self.ref_k[1:], self.ref_v[1:], self.idx, out_k=self.asm_k[1:], out_v=self.asm_v[1:],
-                         except_pos=self.sel)
-            m("gather_rest")
-        ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
-        m("xsel")
+            self.ss.gather_kv(self.ref_k[1:], self.ref_v[1:], self.idx, out_k=self.asm_k[1:], out_v=self.asm_v[1:],
+                              except_pos=self.sel)
+
+    def s_xsel(self):
+        self.ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
+
+    def s_qkv(self, l):
+        wq, wk, wv = self.w[l]
+        self.ss.qkv_rope(self.x_sel, self.sel, wq, wk, wv, self.asm_k[l], self.asm_v[l], self.hq, self.hkv,
+                         q_out=self.q_sel, workspace=self.ws, rope_table=self.rope_sel)
+
+    def s_attn(self, l):
+        self.ss.prefill_attention(self.q_sel, self.sel, self.asm_k[l], self.asm_v[l], self.hkv, out=self.out_sel,
+                                  workspace=self.ws, plan=self.plan)
+
+    def step(self):
+        """One pass of the hot path."""
+        self.s_encode()
+        self.s_match()
+        self.s_gather()
+        self.s_qkv0()
+        self.s_attn0()
+        self.s_select()
+        self.s_gather_rest()
+        self.s_xsel()
         for l in range(1, self.L):
-            wq, wk, wv = self.w[l]
-            ss.qkv_rope(self.x_sel, self.sel, wq, wk, wv, self.asm_k[l], self.asm_v[l], hq, hkv, q_out=self.q_sel,
-                        workspace=self.ws, rope_table=self.rope_sel)
-            m("qkv")
-            ss.prefill_attention(self.q_sel, self.sel, self.asm_k[l], self.asm_v[l], hkv, out=self.out_sel,
-                                 workspace=self.ws, plan=self.plan)
-            m("attn")
+            self.s_qkv(l)
+            self.s_attn(l)
 
 
-def time_steps(torch, path, steps, warmup, instrument):
-    """Times `steps` steps after `warmup` untimed ones.  With instrument, a
-    HIP event pair brackets every call (on the stream the kernels run on) and
-    per-stage durations are returned as well."""
+def time_steps(torch, path, steps, warmup):
+    """Times `steps` steps after `warmup` untimed ones: one HIP event pair on
+    the launch stream around the whole run."""
     for _ in range(warmup):
         path.step()
-    torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    marks = []
-
-    def mark(name):
-        ev = torch.cuda.Event(enable_timing=True)
-        ev.record(stream)
-        marks.append((name, ev))
-
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record(stream)
     for _ in range(steps):
-        path.step(mark if instrument else None)
+        path.step()
     t1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    total_ms = t0.elapsed_time(t1)
-    stages = {}
-    if instrument:
-        for (_, a), (name, b) in zip(marks[:-1], marks[1:]):
-            if name == "start":
-                continue
-            stages.setdefault(name, []).append(a.elapsed_time(b))
-    return total_ms / steps, wall / steps * 1e3, stages
+    return t0.elapsed_time(t1) / steps, wall / steps * 1e3
+
+
+def stage_times(torch, path, reps):
+    """Per-call duration of every stage of a step.  A stage is timed as a run
+    of its own calls with the inputs of a real step (one full step first),
+    between one HIP event pair on the launch stream: `reps` calls of a
+    once-per-step stage, `reps` passes over layers 1..L-1 of a per-layer one.
+    No event sits between the calls of a run, so the figure is the kernels'
+    time plus the launch gaps of back-to-back calls."""
+    path.step()
+    stream = torch.cuda.current_stream()
+    once = [("rope_lsh", path.s_encode), ("match", path.s_match)]
+    once += [("gather_rest", path.s_gather_rest)] if path.gather_except else [("gather", path.s_gather)]
+    once += [("qkv0", path.s_qkv0), ("attn0", path.s_attn0), ("select", path.s_select), ("xsel", path.s_xsel)]
+    out = {}
+    for name, fn in once:
+        fn()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(reps):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        out[name] = t0.elapsed_time(t1) / reps
+    for name, fn in (("qkv", path.s_qkv), ("attn", path.s_attn)):
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(reps):
+            for l in range(1, path.L):
+                fn(l)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        out[name] = t0.elapsed_time(t1) / (reps * (path.L - 1))
+    path.step()  # leave every buffer as a plain step leaves it
+    torch.cuda.synchronize()
+    return out
 
 
 def attention_flops(sel_pos, hq, D):
@@ -566,16 +607,15 @@ def main():
         del src, dst, flush
     # headline: plain timed region
     path.set_frac(args.frac)
-    ms, wall_ms, _ = time_steps(torch, path, args.steps, args.warmup, instrument=False)
-    # per-call durations: the same steps with an event pair around every call
-    ms_i, _, stages = time_steps(torch, path, args.steps, 1, instrument=True)
+    ms, wall_ms = time_steps(torch, path, args.steps, args.warmup)
+    # per-call durations: each stage timed as a run of its own calls after the timed region
+    stages = stage_times(torch, path, max(2, args.steps // 4))
     sel_h = path.sel.cpu().numpy()
     T, L, hq, hkv, D, d = path.T, path.L, path.hq, path.hkv, path.D, path.d
     n_sel = path.n_sel
 
     def avg(name):
-        v = stages.get(name, [])
-        return sum(v) / len(v) if v else float("nan")
+        return stages.get(name, float("nan"))
 
     attn_flops = attention_flops(sel_h, hq, D)
     attn0_flops = 4.0 * D * hq * T * (T + 1) / 2.0
@@ -617,8 +657,9 @@ def main():
                    "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode, "gather": args.gather},
         "partial_prefill_tokens_per_s": T / (pp_ms * 1e-3),
         "match_token_pairs_per_s": T * T / (match_ms * 1e-3),
-        "stage_ms": {k: round(sum(v) / len(v), 4) for k, v in stages.items()},
-        "instrumented_ms_per_step": ms_i,
+        "stage_ms": {k: round(v, 4) for k, v in stages.items()},
+        "stage_sum_ms_per_step": sum(v for k, v in stages.items() if k not in ("qkv", "attn")) +
+                                 (L - 1) * (stages["qkv"] + stages["attn"]),
         "wall_ms_per_step": wall_ms,
         "gather": {"GB/s": gather_bytes / (gather_ms * 1e-3) / 1e9, "frac_of_hbm": gather_bytes / (gather_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS},
         "attention_TFLOPs": {"partial_layer": attn_flops / (attn_ms * 1e-3) / 1e12,
@@ -633,7 +674,7 @@ def main():
         sweep = {}
         for f in [float(x) for x in args.sweep.split(",") if x]:
             path.set_frac(f)
-            m_f, _, _ = time_steps(torch, path, max(3, args.steps // 2), 2, instrument=False)
+            m_f, _ = time_steps(torch, path, max(3, args.steps // 2), 2)
             sweep[f"{f:.2f}"] = {"ms_per_step": m_f, "tokens_per_s": T / (m_f * 1e-3), "n_recompute": path.n_sel,
                                  "recomputed_tokens_per_s": (T + (L - 1) * path.n_sel) / (m_f * 1e-3)}
         res["recompute_sweep"] = sweep
