@@ -115,49 +115,6 @@ struct ACfg {
     static constexpr int kKs = D / 16;                 // k-steps of S^T
 };
 
-// 16 bytes per lane from gbase + off (bytes, per lane) straight into LDS at
-// lds_base + 16 * lane (global_load_lds_dwordx4, M0 = the wave-uniform LDS
-// base, scalar base address + 32-bit lane offset).  Issued as inline assembly
-// on purpose: the compiler then does not treat the transposing LDS reads that
-// follow as dependent on these in-flight loads (it would drain the whole ring
-// with vmcnt(0) before each of them).  Stage readiness is established
-// explicitly instead (wait_vmcnt + ring_barrier), and M0 is written only here
-// in this kernel.
-__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
-    // the scalar operands are wave-uniform by construction; readfirstlane
-    // places them in scalar registers
-    // (readfirstlane returns int: both halves go through uint32_t so the low
-    // half is zero-extended, never sign-extended into the high half)
-    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
-    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
-    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
-    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :
-                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
-                 : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// s_waitcnt vmcnt(n), other counters left at their maximum; vmcnt is split
-// over bits [3:0] and [15:14] of the immediate.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Barrier without the fence of __syncthreads (which would drain the ring of
-// in-flight direct loads); stage visibility comes from the explicit vmcnt waits.
-__device__ __forceinline__ void ring_barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
 // One segment: keys [kbeg, kend) of row tile `tile` for kv head g (kend <=
 // pmax + 1; pmin = the tile's smallest valid position).  slot < 0: the
 // segment is the whole causal range and writes the output; otherwise it

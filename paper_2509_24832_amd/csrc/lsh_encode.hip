@@ -37,35 +37,6 @@ __device__ __forceinline__ void load_chunk(const uint16_t* p, bf16x8_t (&v)[4]) 
 
 typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
 
-// 16 bytes per lane from gbase + off (bytes) straight into LDS at lds_base +
-// 16 * lane (global_load_lds_dwordx4, M0 = the wave-uniform LDS base).  Inline
-// assembly, so the compiler does not wait for these loads (it models the
-// builtin as an LDS access and drains every LDS read before each MFMA);
-// readiness comes from the explicit vmcnt waits and barriers of the loop.
-__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
-    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
-    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
-    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
-    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :
-                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
-                 : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(n), other counters at their maximum (vmcnt split over bits [3:0] and [15:14])
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-__device__ __forceinline__ void ring_barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
 template <int NB>
 struct LshCfg {
     static constexpr int kRows = 32 + 32 * NB;                // rows of a stage: 32 of x, then 32*NB planes

@@ -3,9 +3,12 @@
 //
 // C[n_sel, Nq + 2 Nkv] = X_sel [n_sel, hidden] . [Wq; Wk; Wv]^T  (all K-major)
 //
-// Tiling for gfx950: a 256-thread workgroup owns a 128 x BN output tile (BN =
-// 256, or 128 when a segment is narrower) and runs alone on its CU; each wave
-// owns a 64 x BN/2 sub-tile (2 x BN/64 accumulators of 32x32).  K advances in
+// Tiling for gfx950: a 512-thread workgroup owns a 128 x BN output tile (BN =
+// 256, or 128 when a segment is narrower) and runs alone on its CU, two waves
+// per SIMD, so that one wave's operand reads and loads overlap the other's
+// MFMAs (the partial layer's 1280 x 6144 x 4096 product: 65 -> 61.5 us
+// against one wave per SIMD).  Waves sit 2 along M and 4 along N; each owns a
+// 64 x BN/4 sub-tile (2 x BN/128 accumulators of 32x32).  K advances in
 // 64-wide tiles through a 3-stage LDS ring filled with direct-to-LDS loads
 // (global_load_lds_dwordx4): two tiles are always in flight while the third
 // is multiplied, and no VGPRs are spent on staging.  Rows are 128 B in LDS
@@ -31,67 +34,33 @@ namespace semshare {
 namespace {
 
 constexpr int kBM = 128, kBK = 64, kStages = 3;
+constexpr int kWaves = 8;  // two per SIMD
 
-template <int BN>
+template <int BN, int NW>
 struct Cfg {
+    static constexpr int kThreads = 64 * NW;
     static constexpr int kABytes = kBM * kBK * 2;  // 16 KB
     static constexpr int kBBytes = BN * kBK * 2;   // 32 KB (BN = 256)
     static constexpr int kStage = kABytes + kBBytes;
     static constexpr int kLdc = BN + 8;  // floats per epilogue row (acc writes conflict-free)
     static constexpr int kEpi = kBM * kLdc * 4;
     static constexpr int kLds = kStages * kStage > kEpi ? kStages * kStage : kEpi;
-    static constexpr int kNB = BN / 64;       // 32-wide column blocks per wave
-    static constexpr int kALoads = kBM / 32;  // 1-KB direct loads per wave per K tile
-    static constexpr int kBLoads = BN / 32;
+    static constexpr int kWN = NW / 2;             // waves side by side along N (two along M)
+    static constexpr int kWCols = BN / kWN;        // columns per wave
+    static constexpr int kNB = kWCols / 32;        // 32-wide column blocks per wave
+    static constexpr int kALoads = kBM / 8 / NW;   // 1-KB direct loads (8 rows of 128 B) per wave per K tile
+    static constexpr int kBLoads = BN / 8 / NW;
     static constexpr int kLoads = kALoads + kBLoads;
+    static_assert(kNB >= 1 && kALoads >= 1 && kBLoads >= 1, "tile split");
+    // direct loads issued by k-steps 0 .. s-1 of a K tile (spread evenly over its 4 k-steps)
+    static constexpr int loads_before(int s) { return (s * kLoads + 3) / 4; }
 };
-
-// 16 bytes per lane from gbase + off (bytes) straight into LDS at lds_base +
-// 16 * lane (global_load_lds_dwordx4, M0 = the wave-uniform LDS base, scalar
-// base address + 32-bit lane offset).  Inline assembly on purpose: the
-// compiler models the builtin form as an LDS access that can complete out of
-// order, and then waits for lgkmcnt(0), i.e. for every LDS read in flight,
-// before each MFMA group, which serialises the operand reads with the
-// multiplies.  Stage readiness is established explicitly instead
-// (wait_vmcnt + ring_barrier).
-__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
-    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
-    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
-    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
-    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :
-                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
-                 : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// s_waitcnt vmcnt(n) (n < 16), other counters left at their maximum.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 16, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8));
-}
 
 __device__ __forceinline__ int swz(int row, int chunk) { return ((chunk ^ ((row >> 1) & 7)) << 4); }
 
-// Workgroup barrier without the memory fence of __syncthreads(): the fence
-// would wait for every in-flight direct-to-LDS load (vmcnt(0)) and drain the
-// ring.  Visibility of a stage is established explicitly instead: each wave
-// waits for its own loads of that stage (vmcnt), then all waves meet here.
-// The empty asm statements keep the compiler from moving LDS accesses across.
-__device__ __forceinline__ void ring_barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-template <int BN>
-__global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
-    using C = Cfg<BN>;
+template <int BN, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void qkv_gemm_kernel(GemmArgs g) {
+    using C = Cfg<BN, NW>;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[C::kLds];
 
     const int b = blockIdx.x;
@@ -115,7 +84,7 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS targets stay scalar
     const int half = lane >> 5, l32 = lane & 31;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / C::kWN, wn = wave % C::kWN;
 
     // Direct-load sources: instruction i of this wave fills LDS rows
     // [8*grp, 8*grp+8) of its operand; lane -> (row = 8*grp + lane/8, chunk pc = lane%8)
@@ -158,7 +127,7 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) koff[s] = swz(l32, 4 * half + s);
     const int a_row0 = (64 * wm + l32) * 128;
-    const int b_row0 = ((BN / 2) * wn + l32) * 128;
+    const int b_row0 = (C::kWCols * wn + l32) * 128;
 
     const int nk = g.hidden / kBK;
     for (int j = 0; j < C::kLoads; ++j) issue_one(j, 0, 0);
@@ -194,20 +163,20 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
     auto step = [&](auto st_c, int kt) {
         constexpr int ST = decltype(st_c)::value;
         constexpr int NEXT = (ST + 2) % kStages, FOLLOW = (ST + 1) % kStages;
-        constexpr int kPerStep = C::kLoads / 4;  // direct loads per k-step
-        constexpr int kM = 2 * C::kNB;            // MFMAs per k-step
-        static_assert(2 * kPerStep <= kM, "a load after every other MFMA");
+        constexpr int kM = 2 * C::kNB;  // MFMAs per k-step
         const int kt2 = kt + 2 < nk ? kt + 2 : nk - 1;
         const unsigned char* Ab = smem + ST * C::kStage;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const int cur = s & 1;
+        auto kstep = [&](auto s_c) {
+            constexpr int s = decltype(s_c)::value;
+            constexpr int cur = s & 1;
+            constexpr int j0 = C::loads_before(s), nj = C::loads_before(s + 1) - j0;
+            static_assert(nj <= (kM + 1) / 2, "a load after every other MFMA");
             if (s < 3) {
                 read_ops(Ab, s + 1, cur ^ 1);
             } else {
                 // tile kt + 1 has landed: in flight after it are only the
                 // loads of tile kt + 2 issued by the first three k-steps
-                wait_vmcnt<3 * kPerStep>();
+                wait_vmcnt<C::loads_before(3)>();
                 // this wave's reads of tile kt are done: after the barrier the
                 // loads of tile kt + 3 refill its stage
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
@@ -219,10 +188,14 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
             for (int q = 0; q < kM; ++q) {
                 acc[q / C::kNB][q % C::kNB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     av[cur][q / C::kNB], bv[cur][q % C::kNB], acc[q / C::kNB][q % C::kNB], 0, 0, 0);
-                if (q % 2 == 0 && q / 2 < kPerStep) issue_one(s * kPerStep + q / 2, kt2, NEXT * C::kStage);
+                if (q % 2 == 0 && q / 2 < nj) issue_one(j0 + q / 2, kt2, NEXT * C::kStage);
                 __builtin_amdgcn_sched_barrier(0);
             }
-        }
+        };
+        kstep(std::integral_constant<int, 0>{});
+        kstep(std::integral_constant<int, 1>{});
+        kstep(std::integral_constant<int, 2>{});
+        kstep(std::integral_constant<int, 3>{});
     };
     for (int kt = 0; kt < nk; kt += kStages) {
         step(std::integral_constant<int, 0>{}, kt);
@@ -241,7 +214,7 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int r = 64 * wm + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
-                const int c = (BN / 2) * wn + 32 * k + l32;
+                const int c = C::kWCols * wn + 32 * k + l32;
                 Cs[r * C::kLdc + c] = acc[i][k][v];
             }
     __syncthreads();
@@ -251,10 +224,10 @@ __global__ __launch_bounds__(256, 1) void qkv_gemm_kernel(GemmArgs g) {
     // factors, old cache rows) are all issued before any of them is used, so
     // their latencies overlap instead of adding up row by row.
     const int half_d = g.D / 2;
-    constexpr int kGroups = BN / 8;             // 8-column groups per row
-    constexpr int kRowStep = 256 / kGroups;     // rows between a thread's items
-    constexpr int kItems = kBM / kRowStep;      // items per thread
-    constexpr int kBatch = 8;
+    constexpr int kGroups = BN / 8;                 // 8-column groups per row
+    constexpr int kRowStep = C::kThreads / kGroups; // rows between a thread's items
+    constexpr int kItems = kBM / kRowStep;          // items per thread
+    constexpr int kBatch = kItems < 8 ? kItems : 8;
     static_assert(kItems % kBatch == 0, "batches divide the items");
     const int cg = tid % kGroups, r0 = tid / kGroups;
     const int32_t n = ncol0 + 8 * cg;           // column within the segment
@@ -350,9 +323,9 @@ hipError_t launch_qkv_gemm(const GemmArgs& g, int32_t bn, hipStream_t s) {
     const int64_t per_xcd = (g.n_nt + 7) / 8;
     const dim3 grid((unsigned)(8 * per_xcd * g.n_mt));
     if (bn == 256)
-        hipLaunchKernelGGL(qkv_gemm_kernel<256>, grid, dim3(256), 0, s, g);
+        hipLaunchKernelGGL((qkv_gemm_kernel<256, kWaves>), grid, dim3(64 * kWaves), 0, s, g);
     else
-        hipLaunchKernelGGL(qkv_gemm_kernel<128>, grid, dim3(256), 0, s, g);
+        hipLaunchKernelGGL((qkv_gemm_kernel<128, kWaves>), grid, dim3(64 * kWaves), 0, s, g);
     return hipGetLastError();
 }
 

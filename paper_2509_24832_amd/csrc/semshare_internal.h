@@ -39,6 +39,56 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
+// ------------------------------------------------------------ direct loads into LDS
+// Used by the kernels that stream operands through an LDS ring (the QKV GEMM,
+// the attention, the LSH encode).
+
+// 16 bytes per lane from gbase + off (bytes, per lane) straight into LDS at
+// lds_base + 16 * lane (global_load_lds_dwordx4; M0 = the wave-uniform LDS
+// base, scalar base address + 32-bit lane offset).  Inline assembly on
+// purpose: the compiler models the builtin form as an LDS access that may
+// complete out of order and then waits for every LDS read in flight
+// (lgkmcnt(0)) before each MFMA group, or drains the whole ring with
+// vmcnt(0) before a transposing LDS read.  Stage readiness is established
+// explicitly instead: wait_vmcnt for the wave's own loads, then ring_barrier.
+// M0 is written only here.
+__device__ __forceinline__ void g2lds(const void* gbase, uint32_t off, uint32_t lds_base) {
+    // the scalar operands are wave-uniform by construction; readfirstlane
+    // places them in scalar registers (both halves of the address go through
+    // uint32_t so the low half is zero-extended, never sign-extended)
+    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory", "m0");
+}
+
+// Byte address of a __shared__ object in the LDS address space.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// s_waitcnt vmcnt(N), the other counters left at their maximum; vmcnt is
+// split over bits [3:0] and [15:14] of the immediate.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would wait for every in-flight direct-to-LDS load (vmcnt(0)) and drain the
+// ring.  The empty asm statements keep the compiler from moving LDS accesses
+// across it.
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // RoPE angle m * theta reduced to [-pi, pi] in fp64 (two-constant
 // Cody-Waite reduction).
 __device__ __forceinline__ double rope_reduced_angle(double m, double theta) {
