@@ -36,8 +36,11 @@ COMMON_FLAGS = [
 
 # Per-source extra flags.  attention.hip: scores and probabilities are finite
 # or -inf by construction (masked keys), so NaN-preserving max is not needed;
-# without this every fmaxf operand is first quieted with an extra v_max.
-EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans"], "hamming_match_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# without this every fmaxf operand is first quieted with an extra v_max.  The
+# VGPR form of MFMA keeps accumulators where the vector ALU can read them
+# (attention scores, the matcher's distances) without copies out of AGPRs.
+EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+               "hamming_match_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def sources() -> List[str]:

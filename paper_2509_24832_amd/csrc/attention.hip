@@ -13,7 +13,12 @@
 // two waves ~51 per MFMA and SIMD; 11% fewer cycles per workgroup at 5120
 // tokens, partly given back by a lower clock under the higher MFMA load).
 // S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_32x32x16_bf16: every lane then
-// holds one query column.
+// holds one query column.  Every MFMA operand and accumulator (Q, the two
+// score tiles, O) lives in the architectural vector registers (the file is
+// built with the VGPR form of MFMA; 204 registers, two waves per SIMD): with
+// scores accumulated in AGPRs, each score had to be copied out
+// (v_accvgpr_read) before the softmax could use it, and each masked score
+// copied back, 16 to 48 extra vector instructions per 32-key sub-tile.
 //
 // Data movement.  K and V tiles of 64 keys travel by direct-to-LDS loads
 // (global_load_lds_dwordx4) into a 4-stage ring, in their natural [key][d]
@@ -31,8 +36,10 @@
 // nothing can overflow; otherwise (the first sub-tile, where m is still
 // unset, and large upward jumps later) the sub-tile's true maximum becomes
 // the new m, O and l are rescaled and the probabilities formed again.  The
-// normaliser l sums the fp32 p (the PV product consumes them rounded to bf16;
-// a v_dot2c sum of the rounded pairs is a serial chain that cost ~20% here).
+// normaliser l sums the probabilities as the PV product consumes them,
+// rounded to bf16, one v_dot2c_f32_bf16 per packed pair against (1, 1): half
+// the instructions of two fp32 adds per pair, and the output is then an
+// exactly normalised average of V's rows under the rounded weights.
 //
 // Work division (stream-K over keys).  The unit of work is one 64-key tile
 // of one row tile's causal range: a row tile whose largest valid position is
@@ -75,6 +82,12 @@ constexpr int kPlanHdr = 12;
 constexpr int32_t kSegCost = 6;
 
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
+
+// acc + the two bf16 values of a packed pair (one v_dot2c_f32_bf16 against (1, 1))
+__device__ __forceinline__ float sum_pair(uint32_t pair, float acc) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pair), __builtin_bit_cast(bf16x2_t, 0x3F803F80u),
+                                           acc, false);
+}
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
@@ -149,9 +162,9 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         p_l[nb] = row[nb] < n_sel ? posp[row[nb]] : -1;  // checked below, after the Q loads are out
     }
     // Q^T operands: lane half h holds d in [h*D/2, h*D/2 + D/2).  All loads
-    // are issued here, together with the positions; they move to the
-    // accumulation registers (zeroed for columns without a position) once
-    // the first K/V tile is on its way as well.
+    // are issued here, together with the positions; they become MFMA
+    // operands (zeroed for columns without a position) once the first K/V
+    // tile is on its way as well.
     u32x4_t qv[kNB][C::kKs];
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
@@ -183,22 +196,33 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         uint32_t off_k[C::kLoadsPerWave], off_v[C::kLoadsPerWave];
         uint32_t lds;
     };
+    // per-lane byte offsets of this wave's rows for a tile that lies below
+    // the last key (the common case), formed once per segment
+    uint32_t off_k0[C::kLoadsPerWave], off_v0[C::kLoadsPerWave];
+    auto row_offsets = [&](int32_t lim, uint32_t (&ok)[C::kLoadsPerWave], uint32_t (&ov)[C::kLoadsPerWave]) {
+        const int pc = lane % C::kNch;
+#pragma unroll
+        for (int i = 0; i < C::kLoadsPerWave; ++i) {
+            const int rw = C::kRowsPerLoad * (wave * C::kLoadsPerWave + i) + lane / C::kNch;
+            const uint32_t r = (uint32_t)min(rw, lim);
+            ok[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (rw & (C::kNch - 1)))) * 2u;
+            ov[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (2 * (rw & (C::kNch / 2 - 1))))) * 2u;
+        }
+    };
+    row_offsets(KT - 1, off_k0, off_v0);
     auto prep_tile = [&](int t, TileLoads& d) {
         const int32_t key0 = kbeg + t * KT;
         d.kg = kbase + (int64_t)key0 * row_stride;
         d.vg = vbase + (int64_t)key0 * row_stride;
         const int32_t lim = last_key - key0;
-        // recomputed from an opaque lane id at every tile (a few VALU
-        // operations) instead of being held through the key loop
-        int ln = (int)threadIdx.x & 63;
-        asm volatile("" : "+v"(ln));
-        const int pc = ln % C::kNch;
+        if (lim >= KT - 1) {
 #pragma unroll
-        for (int i = 0; i < C::kLoadsPerWave; ++i) {
-            const int rw = C::kRowsPerLoad * (wave * C::kLoadsPerWave + i) + ln / C::kNch;
-            const uint32_t r = (uint32_t)min(rw, lim);
-            d.off_k[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (rw & (C::kNch - 1)))) * 2u;
-            d.off_v[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (2 * (rw & (C::kNch / 2 - 1))))) * 2u;
+            for (int i = 0; i < C::kLoadsPerWave; ++i) {
+                d.off_k[i] = off_k0[i];
+                d.off_v[i] = off_v0[i];
+            }
+        } else {
+            row_offsets(lim, d.off_k, d.off_v);  // rows past the last key read the last key
         }
         d.lds = __builtin_amdgcn_readfirstlane(smem_base + (t % kStages) * C::kStage +
                                                wave * C::kLoadsPerWave * 1024);
@@ -241,14 +265,14 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
 
     f32x16_t oacc[kNB][C::kMd];
     // O is zeroed after the first sub-tile's probabilities (zero_o): before
-    // it the accumulation registers hold Q and two score tiles only
+    // it the registers hold Q and two score tiles only
     auto zero_o = [&]() {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
             for (int i = 0; i < C::kMd; ++i) {
                 oacc[nb][i] = f32x16_t{};
-                asm volatile("" : "+a"(oacc[nb][i]));
+                asm volatile("" : "+v"(oacc[nb][i]));
             }
     };
     float m_run[kNB], l_run[kNB];
@@ -314,10 +338,10 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
                     if (8 * (v >> 2) + (v & 3) > lim) sacc[nb][v] = -INFINITY;
-                // applied here, back in the accumulation registers: left to
-                // the compiler the selects sink to the next sub-tile's reads
-                // and hold 32 lane masks in scalar registers meanwhile
-                asm volatile("" : "+a"(sacc[nb]));
+                // applied here: left to the compiler the selects sink to the
+                // next sub-tile's reads and hold 32 lane masks in scalar
+                // registers meanwhile
+                asm volatile("" : "+v"(sacc[nb]));
             }
         }
     };
@@ -335,8 +359,9 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
 #pragma unroll
                 for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[nb][8 * sp + e], cl2, -mc));
                 pb[nb][sp] = __builtin_convertvector(pv, bf16x8_t);
+                const u32x4_t w = __builtin_bit_cast(u32x4_t, pb[nb][sp]);
 #pragma unroll
-                for (int e = 0; e < 8; e += 2) ts[nb] += pv[e] + pv[e + 1];
+                for (int e = 0; e < 4; ++e) ts[nb] = sum_pair(w[e], ts[nb]);
             }
         }
     };
@@ -402,12 +427,11 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
         s_mfma(kf, sA);  // Q still in vector registers here
         mask(0, sA);
     }
-    // Q kept in accumulation registers from here on (MFMA reads its B operand
-    // from there), leaving the vector registers to K/V fragments and softmax
+    // Q stays in the registers it was loaded into for the whole segment
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
-        for (int s = 0; s < C::kKs; ++s) asm volatile("" : "+a"(qf[nb][s]));
+        for (int s = 0; s < C::kKs; ++s) asm volatile("" : "+v"(qf[nb][s]));
     // Sub-tile u with a successor: S(u+1) and PV(u-1) on the matrix cores
     // while the probabilities of u are formed.  An odd u first opens tile
     // (u+1)/2 (its loads done, the stage of tile (u+1)/2 - 2 free again).
@@ -498,7 +522,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
                 for (int q = 0; q < kPairs; ++q) {
                     if (cvt_slot(q) == k)
                         pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
-                    if (cvt_slot(q) + 1 == k) ts[q >> 3] += ev[2 * q] + ev[2 * q + 1];
+                    if (cvt_slot(q) + 1 == k) ts[q >> 3] = sum_pair(pw[q], ts[q >> 3]);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -511,7 +535,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
                     pw[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{ev[2 * q], ev[2 * q + 1]}, bf16x2_t));
 #pragma unroll
             for (int q = 0; q < kPairs; ++q)
-                if (cvt_slot(q) + 1 >= kSlots) ts[q >> 3] += ev[2 * q] + ev[2 * q + 1];
+                if (cvt_slot(q) + 1 >= kSlots) ts[q >> 3] = sum_pair(pw[q], ts[q >> 3]);
             // word q = (nb, sp, w) with q = 8 nb + 4 sp + w
 #pragma unroll
             for (int nb = 0; nb < kNB; ++nb)
