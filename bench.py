@@ -76,8 +76,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "411ab50bbf55f049646863a85b8e5a556db5f1450d31181c6eb560714be8a11b",
-                "bytes_per_call": 95690828}
+ATTN_TRAFFIC = {"source_sha256": "48ba106da7ee37b2143538bfcdf5f61765758f927e94117ab34ca2512136e1a4",
+                "bytes_per_call": 93986446}
 
 
 def source_sha256(rel):
