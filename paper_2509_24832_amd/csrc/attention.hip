@@ -22,9 +22,12 @@
 //
 // Data movement.  K and V tiles of 64 keys travel by direct-to-LDS loads
 // (global_load_lds_dwordx4) into a 4-stage ring, in their natural [key][d]
-// layout with the 16-byte chunk index XOR-swizzled per row (K by row mod D/8,
-// V by 2*(row mod D/16)), so the MFMA operand reads below are free of bank
-// conflicts.  V^T operands come from ds_read_b64_tr_b16, which transposes
+// layout with the 16-byte chunk index XOR-swizzled per row (K by row mod D/8;
+// V so that the 32 lanes a transposing read serves per pass cover all 64
+// banks, ACfg::vswz), so the MFMA operand reads below are free of bank
+// conflicts (the SQ_LDS_BANK_CONFLICT counter reads 0; a V swizzle that was
+// conflict-free only per 16 lanes cost 1.3 conflict cycles per LDS
+// instruction).  V^T operands come from ds_read_b64_tr_b16, which transposes
 // 4 keys x 4 dims per 16-lane group on the way out of LDS.
 //
 // Softmax.  Keys run in sub-tiles of 32.  The probabilities of sub-tile u are
@@ -126,6 +129,12 @@ struct ACfg {
     static constexpr int kLoads = 2 * kLoadsPerWave;   // per wave per tile (K + V)
     static constexpr int kMd = D / 32;                 // 32-row blocks of O^T
     static constexpr int kKs = D / 16;                 // k-steps of S^T
+    // V swizzle: chunk c of key row r is stored at chunk c ^ vswz(r).  A
+    // transposing read serves 32 lanes per pass: the 4 rows x 4 chunks of one
+    // 32-dim block that they read must fill all 64 banks (D = 128: 256-byte
+    // rows, so the 4 rows take 4 different 4-chunk blocks; D = 64: 128-byte
+    // rows, two per bank sweep, so rows r and r + 2 take different blocks)
+    static __host__ __device__ constexpr int vswz(int r) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
 };
 
 // One segment: keys [kbeg, kend) of row tile `tile` for kv head g (kend <=
@@ -206,7 +215,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
             const int rw = C::kRowsPerLoad * (wave * C::kLoadsPerWave + i) + lane / C::kNch;
             const uint32_t r = (uint32_t)min(rw, lim);
             ok[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (rw & (C::kNch - 1)))) * 2u;
-            ov[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ (2 * (rw & (C::kNch / 2 - 1))))) * 2u;
+            ov[i] = (r * (uint32_t)row_stride + 8u * (uint32_t)(pc ^ C::vswz(rw))) * 2u;
         }
     };
     row_offsets(KT - 1, off_k0, off_v0);
@@ -253,7 +262,7 @@ __device__ __forceinline__ void segment(const AttnArgs& a, unsigned char* smem, 
     const int gq = lane >> 4, m16 = lane & 15;
     const int v_r = 4 * half + (m16 >> 2);  // row within an 8-row group (the swizzle depends on it only)
     const uint32_t v_ro0 = v_r * C::kRowBytes +
-                           (((2 * (gq & 1) + ((m16 & 3) >> 1)) ^ (2 * (v_r & (C::kNch / 2 - 1)))) << 4) + (m16 & 1) * 8;
+                           (((2 * (gq & 1) + ((m16 & 3) >> 1)) ^ C::vswz(v_r)) << 4) + (m16 & 1) * 8;
     // Stage and sub-tile bases are multiples of 1 KB, above every bit these
     // XORs touch: (base + off0) ^ x == base + (off0 ^ x).
     typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
