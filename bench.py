@@ -480,7 +480,8 @@ def dynamic_recompute_line(torch, np, ss, cfg, args):
     t_win = t_ret = t_cmp = 0.0
     for it in range(args.warmup + args.steps):
         ev[0].record()
-        ss.attention_mass(q, k, hq, hkv, mass=score, workspace=ws, row_begin=row_begin)
+        # the window pass takes the row normalisers the full pass left in ws
+        ss.attention_mass(q, k, hq, hkv, mass=score, workspace=ws, row_begin=row_begin, reuse_normalisers=True)
         ev[1].record()
         rank, kept, n_kept = ss.retention(mass, score, sel, counts, 0.8)
         ev[2].record()
@@ -504,6 +505,7 @@ def dynamic_recompute_line(torch, np, ss, cfg, args):
            "attention_mass_us": round(us_mass, 2), "dynamic_select_us": round(us_sel, 2),
            "AR": c[0], "n_recompute": c[1], "n_hot_recompute": c[2],
            "retention": {"window_rows": T - row_begin, "window_mass_us": round(t_win / n * 1e3, 2),
+                         "window_reuses_row_normalisers": True,
                          "rank_us": round(t_ret / n * 1e3, 2), "n_kept": nk,
                          "compaction_us": round(t_cmp / n * 1e3, 2),
                          "compaction_GB_per_s": 2 * 2 * L * nk * hkv * D * 2 / (t_cmp / n * 1e-3) / 1e9},

@@ -414,6 +414,21 @@ semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, in
                                           semshare_dtype_t dtype, void* stream);
 
 /*
+ * The same average over the rows >= row_begin (the retention window of
+ * Section 4.3.4), reusing the per-row softmax normalisers that a previous
+ * semshare_attention_mass call left in `workspace`: a row's normaliser sums
+ * over all its keys whatever row_begin is, so the window pass only sums the
+ * columns (about 40% less work at 5120 tokens).  Precondition (not checked on
+ * the device): workspace is the buffer of a semshare_attention_mass call with
+ * the same q, k_cache, n_tok, heads, head_dim and sm_scale, on the same
+ * stream, not written since.  Arguments and errors as semshare_attention_mass.
+ */
+semshare_status_t semshare_attention_mass_window(const void* q, const void* k_cache, int64_t n_tok, int64_t row_begin,
+                                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                 float sm_scale, float* mass, void* workspace, size_t workspace_bytes,
+                                                 semshare_dtype_t dtype, void* stream);
+
+/*
  * Token retention on the first layer (Section 4.3.4; Appendix A.6 gives the
  * per-layer counts Retain[i] = T prod alpha[j]): hot tokens (the counts[0]
  * first by mass, as semshare_dynamic_recompute orders them) and the

@@ -112,33 +112,52 @@ size_t semshare_attention_mass_workspace(int64_t n_tok, int32_t n_q_heads) {
     return semshare::attention_mass_workspace(n_tok, n_q_heads);
 }
 
+// semshare_attention_mass (reuse = false) and semshare_attention_mass_window
+// (reuse = true: the row normalisers are taken from the workspace)
+static semshare_status_t attention_mass_impl(const char* name, bool reuse, const void* q, const void* k_cache,
+                                             int64_t n_tok, int64_t row_begin, int32_t n_q_heads, int32_t n_kv_heads,
+                                             int32_t head_dim, float sm_scale, float* mass, void* workspace,
+                                             size_t workspace_bytes, semshare_dtype_t dtype, void* stream) {
+    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "%s: unknown dtype %d", name, dtype);
+    if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "%s: n_tok < 0", name);
+    if (row_begin < 0 || (n_tok > 0 && row_begin >= n_tok))
+        return fail(SEMSHARE_E_INVAL, "%s: row_begin must lie in [0, n_tok)", name);
+    if (n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads)
+        return fail(SEMSHARE_E_INVAL, "%s: n_q_heads must be a positive multiple of n_kv_heads", name);
+    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale))
+        return fail(SEMSHARE_E_INVAL, "%s: sm_scale must be finite and >= 0", name);
+    if (dtype != SEMSHARE_BF16 || head_dim != 128)
+        return fail(SEMSHARE_E_UNSUPPORTED, "%s: built for bf16 with head_dim 128", name);
+    if (n_tok > (int64_t(1) << 24) || (int64_t)n_q_heads * n_tok > (int64_t(1) << 31))
+        return fail(SEMSHARE_E_UNSUPPORTED, "%s: too many tokens", name);
+    if (n_tok == 0) return ok();
+    if (!q || !k_cache || !mass || !workspace) return fail(SEMSHARE_E_INVAL, "%s: null buffer", name);
+    if (!aligned16(q) || !aligned16(k_cache) || reinterpret_cast<uintptr_t>(workspace) % 4 ||
+        reinterpret_cast<uintptr_t>(mass) % 4)
+        return fail(SEMSHARE_E_INVAL, "%s: q and k_cache must be 16-byte aligned, mass and workspace 4-byte", name);
+    if (workspace_bytes < semshare::attention_mass_workspace(n_tok, n_q_heads))
+        return fail(SEMSHARE_E_INVAL, "%s: workspace too small (%zu < %zu)", name, workspace_bytes,
+                    semshare::attention_mass_workspace(n_tok, n_q_heads));
+    const float scale = sm_scale == 0.0f ? 1.0f / sqrtf((float)head_dim) : sm_scale;
+    return from_hip(semshare::launch_attention_mass(q, k_cache, n_tok, row_begin, n_q_heads, n_kv_heads, scale, mass,
+                                                    workspace, (hipStream_t)stream, reuse),
+                    name);
+}
+
 semshare_status_t semshare_attention_mass(const void* q, const void* k_cache, int64_t n_tok, int64_t row_begin,
                                           int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float sm_scale,
                                           float* mass, void* workspace, size_t workspace_bytes,
                                           semshare_dtype_t dtype, void* stream) {
-    if (!dtype_ok(dtype)) return fail(SEMSHARE_E_INVAL, "attention_mass: unknown dtype %d", dtype);
-    if (n_tok < 0) return fail(SEMSHARE_E_INVAL, "attention_mass: n_tok < 0");
-    if (row_begin < 0 || (n_tok > 0 && row_begin >= n_tok))
-        return fail(SEMSHARE_E_INVAL, "attention_mass: row_begin must lie in [0, n_tok)");
-    if (n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads)
-        return fail(SEMSHARE_E_INVAL, "attention_mass: n_q_heads must be a positive multiple of n_kv_heads");
-    if (!(sm_scale >= 0.0f) || !std::isfinite(sm_scale)) return fail(SEMSHARE_E_INVAL, "attention_mass: sm_scale must be finite and >= 0");
-    if (dtype != SEMSHARE_BF16 || head_dim != 128)
-        return fail(SEMSHARE_E_UNSUPPORTED, "attention_mass: built for bf16 with head_dim 128");
-    if (n_tok > (int64_t(1) << 24) || (int64_t)n_q_heads * n_tok > (int64_t(1) << 31))
-        return fail(SEMSHARE_E_UNSUPPORTED, "attention_mass: too many tokens");
-    if (n_tok == 0) return ok();
-    if (!q || !k_cache || !mass || !workspace) return fail(SEMSHARE_E_INVAL, "attention_mass: null buffer");
-    if (!aligned16(q) || !aligned16(k_cache) || reinterpret_cast<uintptr_t>(workspace) % 4 ||
-        reinterpret_cast<uintptr_t>(mass) % 4)
-        return fail(SEMSHARE_E_INVAL, "attention_mass: q and k_cache must be 16-byte aligned, mass and workspace 4-byte");
-    if (workspace_bytes < semshare::attention_mass_workspace(n_tok, n_q_heads))
-        return fail(SEMSHARE_E_INVAL, "attention_mass: workspace too small (%zu < %zu)", workspace_bytes,
-                    semshare::attention_mass_workspace(n_tok, n_q_heads));
-    const float scale = sm_scale == 0.0f ? 1.0f / sqrtf((float)head_dim) : sm_scale;
-    return from_hip(semshare::launch_attention_mass(q, k_cache, n_tok, row_begin, n_q_heads, n_kv_heads, scale, mass,
-                                                    workspace, (hipStream_t)stream),
-                    "attention_mass launch");
+    return attention_mass_impl("attention_mass", false, q, k_cache, n_tok, row_begin, n_q_heads, n_kv_heads, head_dim,
+                               sm_scale, mass, workspace, workspace_bytes, dtype, stream);
+}
+
+semshare_status_t semshare_attention_mass_window(const void* q, const void* k_cache, int64_t n_tok, int64_t row_begin,
+                                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                 float sm_scale, float* mass, void* workspace, size_t workspace_bytes,
+                                                 semshare_dtype_t dtype, void* stream) {
+    return attention_mass_impl("attention_mass_window", true, q, k_cache, n_tok, row_begin, n_q_heads, n_kv_heads,
+                               head_dim, sm_scale, mass, workspace, workspace_bytes, dtype, stream);
 }
 
 semshare_status_t semshare_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,

@@ -468,7 +468,8 @@ size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads) {
 }
 
 hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int64_t row_begin, int32_t n_q_heads,
-                                 int32_t n_kv_heads, float sm_scale, float* mass, void* workspace, hipStream_t s) {
+                                 int32_t n_kv_heads, float sm_scale, float* mass, void* workspace, hipStream_t s,
+                                 bool reuse_normalisers) {
     float* lse2 = static_cast<float*>(workspace);
     float* part = lse2 + (int64_t)n_q_heads * n_tok;
     const float sl2e = sm_scale * 1.4426950408889634f;
@@ -476,7 +477,10 @@ hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, in
     const dim3 grid((unsigned)((nb + kNB - 1) / kNB), (unsigned)n_q_heads);
     const auto* qp = static_cast<const uint16_t*>(q);
     const auto* kp = static_cast<const uint16_t*>(k);
-    hipLaunchKernelGGL(mass_lse_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2);
+    // the row normalisers do not depend on row_begin: a window pass after a
+    // pass over the same q and K finds them in the workspace
+    if (!reuse_normalisers)
+        hipLaunchKernelGGL(mass_lse_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2);
     hipLaunchKernelGGL(mass_col_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, row_begin, n_q_heads, n_kv_heads, sl2e,
                        lse2, part);
     hipLaunchKernelGGL(mass_final_kernel, dim3((unsigned)((n_tok + 255) / 256)), dim3(256), 0, s, part, n_tok,

@@ -142,7 +142,8 @@ hipError_t launch_retention_layer(const int32_t* rank, int32_t n_tok, int32_t n_
 
 size_t attention_mass_workspace(int64_t n_tok, int32_t n_q_heads);
 hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, int64_t row_begin, int32_t n_q_heads,
-                                 int32_t n_kv_heads, float sm_scale, float* mass, void* workspace, hipStream_t s);
+                                 int32_t n_kv_heads, float sm_scale, float* mass, void* workspace, hipStream_t s,
+                                 bool reuse_normalisers = false);
 hipError_t launch_retention(const float* mass, const float* score, int32_t n_tok, const int32_t* sel_pos,
                             const int32_t* counts, double min_keep, int32_t* rank, int32_t* kept_pos, int32_t* n_kept,
                             hipStream_t s);

@@ -133,7 +133,7 @@ class DynamicSchedule:
         ar, n1 = counts[0], counts[1]
         row_begin = min(T - 1, T - int(math.floor((1.0 - ar / T) * T + 0.5)))
         ss.attention_mass(self.q0, self.asm_k[0], hq, hkv, mass=self.score, workspace=self.mass_ws,
-                          row_begin=row_begin)
+                          row_begin=row_begin, reuse_normalisers=True)
         rank, kept0, n_kept0_t = ss.retention(self.mass, self.score, self.sel1, self.counts, self.min_keep)
         n_kept0 = self._n(n_kept0_t)
         ss.gather_kv(self.asm_k[0][None], self.asm_v[0][None], kept0[:n_kept0], out_k=self.kc0[None, :n_kept0],

@@ -66,6 +66,7 @@ def load() -> ctypes.CDLL:
         "semshare_retention_layer": (I32, [P, I32, I32, P, I32, P, P, P, P, P, P]),
         "semshare_attention_mass_workspace": (SZ, [I64, I32]),
         "semshare_attention_mass": (I32, [P, P, I64, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
+        "semshare_attention_mass_window": (I32, [P, P, I64, I64, I32, I32, I32, F32, P, P, SZ, I32, P]),
         "semshare_retention": (I32, [P, P, I32, P, P, F64, P, P, P, P]),
         "semshare_dynamic_recompute": (I32, [P, P, I32, F64, F64, F64, P, P, P]),
         "semshare_qkv_rope": (I32, [P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, F64, P, P, P, SZ, I32, P]),
@@ -187,9 +188,12 @@ def rope_lsh_encode(x: torch.Tensor, planes: torch.Tensor, out: Optional[torch.T
 
 def attention_mass(q: torch.Tensor, k_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int, sm_scale: float = 0.0,
                    mass: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
-                   row_begin: int = 0) -> torch.Tensor:
+                   row_begin: int = 0, reuse_normalisers: bool = False) -> torch.Tensor:
     """Average attention score per token over the query rows >= row_begin: q [T, Hq, D], k_cache [T, Hkv, D]
-    -> mass [T] float32."""
+    -> mass [T] float32.  reuse_normalisers: semshare_attention_mass_window, which takes the row normalisers
+    from `workspace` as a previous call over the same q and k_cache left them (workspace required)."""
+    if reuse_normalisers and workspace is None:
+        raise ValueError("reuse_normalisers needs the workspace of a previous attention_mass call")
     _dev(q, "q")
     _dev(k_cache, "k_cache", q.dtype)
     T = q.shape[0]
@@ -200,7 +204,8 @@ def attention_mass(q: torch.Tensor, k_cache: torch.Tensor, n_q_heads: int, n_kv_
     need = int(load().semshare_attention_mass_workspace(T, n_q_heads))
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
-    _call("semshare_attention_mass", _ptr(q), _ptr(k_cache), T, int(row_begin), n_q_heads, n_kv_heads, d,
+    _call("semshare_attention_mass_window" if reuse_normalisers else "semshare_attention_mass", _ptr(q),
+          _ptr(k_cache), T, int(row_begin), n_q_heads, n_kv_heads, d,
           float(sm_scale), _ptr(mass),
           _ptr(workspace), workspace.numel() * workspace.element_size(), _dt(q), _stream())
     return mass

@@ -99,6 +99,12 @@ def test_attention_mass_and_dynamic_validation(lib):
     assert _st(e, FAKE_ODD, FAKE, 100, 0, 32, 8, 128, 0.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # alignment
     assert _st(e, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, None, FAKE, ws, 1, None) == b.E_INVAL  # null mass
     assert _st(e, None, None, 0, 0, 32, 8, 128, 0.0, None, None, 0, 1, None) == b.OK
+    w = "semshare_attention_mass_window"  # same checks
+    assert _st(w, FAKE, FAKE, 100, 100, 32, 8, 128, 0.0, FAKE, FAKE, ws, 1, None) == b.E_INVAL  # row_begin
+    assert _st(w, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, FAKE, None, ws, 1, None) == b.E_INVAL  # null workspace
+    assert _st(w, FAKE, FAKE, 100, 0, 32, 8, 128, 0.0, FAKE, FAKE, ws - 4, 1, None) == b.E_INVAL  # workspace
+    assert _st(w, FAKE, FAKE, 100, 0, 32, 8, 64, 0.0, FAKE, FAKE, ws, 1, None) == b.E_UNSUPPORTED  # head_dim
+    assert _st(w, None, None, 0, 0, 32, 8, 128, 0.0, None, None, 0, 1, None) == b.OK
     d = "semshare_dynamic_recompute"
     assert _st(d, FAKE, FAKE, 65537, 0.55, 0.5, 0.1, FAKE, FAKE, None) == b.E_UNSUPPORTED
     assert _st("semshare_retention", FAKE, FAKE, 65537, FAKE, FAKE, 0.8, FAKE, FAKE, FAKE, None) == b.E_UNSUPPORTED

@@ -191,6 +191,25 @@ def test_window_mass_matches_oracle(T, row_begin):
     assert np.allclose(m, ref, rtol=1e-4, atol=1e-8), np.abs(m - ref).max()
 
 
+@pytest.mark.parametrize("T,hq,hkv,row_begin", [(300, 8, 2, 137), (5120, 32, 8, 4003), (1000, 32, 8, 999)])
+def test_window_mass_reusing_normalisers(T, hq, hkv, row_begin):
+    """The window pass that takes the row normalisers from the full pass's
+    workspace equals the one that computes them (bit for bit: the same
+    normaliser kernel wrote them) and the oracle's window average."""
+    cfg = CONFIGS[1]
+    announce(f"window mass reusing normalisers T={T} row_begin={row_begin}")
+    q, k = _qk(cfg, T, hq, hkv, tag=90 + T)
+    qd, kd = dev(q, "bf16"), dev(k, "bf16")
+    ws = torch.empty(int(ss.semshare.load().semshare_attention_mass_workspace(T, hq)), dtype=torch.uint8,
+                     device="cuda")
+    ss.attention_mass(qd, kd, hq, hkv, workspace=ws)  # the full pass leaves the normalisers in ws
+    reused = host(ss.attention_mass(qd, kd, hq, hkv, workspace=ws, row_begin=row_begin, reuse_normalisers=True))
+    fresh = host(ss.attention_mass(qd, kd, hq, hkv, row_begin=row_begin))
+    assert np.array_equal(reused, fresh)
+    ref = orc.attention_mass_cols(q, k, hq, hkv, 128, row_begin=row_begin)
+    assert np.allclose(reused, ref, rtol=1e-4, atol=1e-9), np.abs(reused - ref).max()
+
+
 @pytest.mark.parametrize("T,seed,ties,min_keep", [(1, 0, False, 0.8), (50, 1, True, 0.8), (1000, 2, False, 0.8),
                                                   (5120, 3, False, 0.8), (5120, 4, True, 0.5), (8192, 5, False, 1.0),
                                                   (8193, 6, False, 0.8), (32768, 7, True, 0.8),
