@@ -222,7 +222,11 @@ __global__ __launch_bounds__(64 * NW, 1) void qkv_gemm_kernel(GemmArgs g) {
     // Each thread owns one 8-column group (cg) of rows r0, r0 + kRowStep, ...
     // Rows go in batches of kBatch whose global reads (position, RoPE
     // factors, old cache rows) are all issued before any of them is used, so
-    // their latencies overlap instead of adding up row by row.
+    // their latencies overlap instead of adding up row by row.  One pass per
+    // segment, specialised at compile time (q: RoPE and store; k: RoPE,
+    // deviation and scatter; v: deviation and scatter): with the segment a
+    // run-time value every optional load became a branch of its own.  Loads
+    // read the last row for rows past n_sel (in bounds, never stored).
     const int half_d = g.D / 2;
     constexpr int kGroups = BN / 8;                 // 8-column groups per row
     constexpr int kRowStep = C::kThreads / kGroups; // rows between a thread's items
@@ -231,85 +235,107 @@ __global__ __launch_bounds__(64 * NW, 1) void qkv_gemm_kernel(GemmArgs g) {
     static_assert(kItems % kBatch == 0, "batches divide the items");
     const int cg = tid % kGroups, r0 = tid / kGroups;
     const int32_t n = ncol0 + 8 * cg;           // column within the segment
-    const int32_t k0 = (n % g.D) >> 1;          // first RoPE pair of the group
-    const bool rope = seg < 2, kv = seg > 0, dev = kv && g.dev_parts;
+    const int32_t k0 = (n % g.D) >> 1;          // first RoPE pair of the group (a multiple of 4)
+    auto epilogue = [&](auto seg_c) {
+        constexpr int SEG = decltype(seg_c)::value;
+        constexpr bool kRope = SEG < 2, kKV = SEG > 0;
+        const bool dev = kKV && g.dev_parts != nullptr;
 #pragma unroll 1
-    for (int b0 = 0; b0 < kItems; b0 += kBatch) {
-        int32_t p[kBatch];
-        float2 cs[kBatch][4];
-        u32x4_t old[kBatch];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int64_t m = m0 + r0 + (b0 + u) * kRowStep;
-            const bool ok = m < g.n_sel;
-            p[u] = ok && kv ? g.pos[m] : -1;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) cs[u][e] = ok && rope ? g.rope[m * half_d + k0 + e] : make_float2(1.0f, 0.0f);
-        }
-        if (dev && g.dev_idx) {  // the deviation against matched reference rows
-            const uint16_t* src = g.dev_src[seg - 1];
-            int32_t j[kBatch];
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u) j[u] = p[u] >= 0 && p[u] < g.n_tok ? g.dev_idx[p[u]] : -1;
+        for (int b0 = 0; b0 < kItems; b0 += kBatch) {
+            int64_t mc[kBatch];
+            int32_t p[kBatch];
+            f32x4_t cs[kBatch][2];  // (cos, sin) of the group's 4 pairs
+            u32x4_t old[kBatch];
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) {
-                old[u] = u32x4_t{0u, 0u, 0u, 0u};
-                if (j[u] >= 0 && j[u] < g.dev_n) old[u] = *reinterpret_cast<const u32x4_t*>(src + (int64_t)j[u] * seg_cols + n);
+                const int64_t m = m0 + r0 + (b0 + u) * kRowStep;
+                mc[u] = m < g.n_sel ? m : g.n_sel - 1;
             }
-        } else {
+            if constexpr (kRope) {
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                old[u] = u32x4_t{0u, 0u, 0u, 0u};
-                if (dev && p[u] >= 0 && p[u] < g.n_tok)
-                    old[u] = *reinterpret_cast<const u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int r = r0 + (b0 + u) * kRowStep;
-            const int64_t m = m0 + r;
-            float v8[8];
-            {
-                const f32x4_t c0 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg);
-                const f32x4_t c1 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg + 4);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) { v8[e] = c0[e]; v8[4 + e] = c1[e]; }
-            }
-            if (rope) {  // RoPE on q and k: pairs (2k, 2k+1) within the head
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float2 t = cs[u][e];
-                    const float x0 = v8[2 * e], x1 = v8[2 * e + 1];
-                    v8[2 * e] = t.x * x0 - t.y * x1;
-                    v8[2 * e + 1] = t.y * x0 + t.x * x1;
+                for (int u = 0; u < kBatch; ++u) {
+                    const f32x4_t* rp = reinterpret_cast<const f32x4_t*>(g.rope + mc[u] * half_d + k0);
+                    cs[u][0] = rp[0];
+                    cs[u][1] = rp[1];
                 }
             }
-            const u32x4_t packed = u32x4_t{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
-                                           pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
-            float dsum = 0.0f;
-            if (m < g.n_sel) {
-                if (seg == 0) {
-                    *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
-                } else if (p[u] >= 0 && p[u] < g.n_tok) {
-                    if (dev) {
+            if constexpr (kKV) {
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const float d0 = bf16_lo(old[u][e]) - bf16_lo(packed[e]);
-                            const float d1 = bf16_hi(old[u][e]) - bf16_hi(packed[e]);
-                            dsum += d0 * d0 + d1 * d1;
-                        }
+                for (int u = 0; u < kBatch; ++u) {
+                    const int32_t pp = g.pos[mc[u]];
+                    p[u] = m0 + r0 + (b0 + u) * kRowStep < g.n_sel && pp >= 0 && pp < g.n_tok ? pp : -1;
+                }
+                if (dev && g.dev_idx) {  // the deviation against matched reference rows
+                    const uint16_t* src = g.dev_src[SEG - 1];
+                    int32_t j[kBatch];
+#pragma unroll
+                    for (int u = 0; u < kBatch; ++u) j[u] = p[u] >= 0 ? g.dev_idx[p[u]] : -1;
+#pragma unroll
+                    for (int u = 0; u < kBatch; ++u) {
+                        old[u] = u32x4_t{0u, 0u, 0u, 0u};
+                        if (j[u] >= 0 && j[u] < g.dev_n)
+                            old[u] = *reinterpret_cast<const u32x4_t*>(src + (int64_t)j[u] * seg_cols + n);
                     }
-                    *reinterpret_cast<u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n) = packed;
+                } else if (dev) {  // the deviation against the cache rows being replaced
+#pragma unroll
+                    for (int u = 0; u < kBatch; ++u) {
+                        old[u] = u32x4_t{0u, 0u, 0u, 0u};
+                        if (p[u] >= 0) old[u] = *reinterpret_cast<const u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n);
+                    }
                 }
             }
-            if (dev) {
-                // the kGroups threads of one tile row are consecutive lanes (kGroups divides 64)
 #pragma unroll
-                for (int o = kGroups / 2; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o, kGroups);
-                if (cg == 0 && m < g.n_sel) g.dev_parts[(2 * m + (seg - 1)) * (seg_cols / BN) + nt] = dsum;
+            for (int u = 0; u < kBatch; ++u) {
+                const int r = r0 + (b0 + u) * kRowStep;
+                const int64_t m = m0 + r;
+                float v8[8];
+                {
+                    const f32x4_t c0 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg);
+                    const f32x4_t c1 = *reinterpret_cast<const f32x4_t*>(Cs + r * C::kLdc + 8 * cg + 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { v8[e] = c0[e]; v8[4 + e] = c1[e]; }
+                }
+                if constexpr (kRope) {  // RoPE on q and k: pairs (2k, 2k+1) within the head
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float2 t = make_float2(cs[u][e >> 1][2 * (e & 1)], cs[u][e >> 1][2 * (e & 1) + 1]);
+                        const float x0 = v8[2 * e], x1 = v8[2 * e + 1];
+                        // explicit fused forms: the rounding does not depend on how the
+                        // compiler contracts the products
+                        v8[2 * e] = fmaf(t.x, x0, -(t.y * x1));
+                        v8[2 * e + 1] = fmaf(t.y, x0, t.x * x1);
+                    }
+                }
+                const u32x4_t packed = u32x4_t{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
+                                               pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
+                if constexpr (SEG == 0) {
+                    if (m < g.n_sel) *reinterpret_cast<u32x4_t*>(g.q_out + m * seg_cols + n) = packed;
+                } else {
+                    float dsum = 0.0f;
+                    if (p[u] >= 0) {
+                        if (dev) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const float d0 = bf16_lo(old[u][e]) - bf16_lo(packed[e]);
+                                const float d1 = bf16_hi(old[u][e]) - bf16_hi(packed[e]);
+                                dsum += d0 * d0 + d1 * d1;
+                            }
+                        }
+                        *reinterpret_cast<u32x4_t*>(kvseg + (int64_t)p[u] * seg_cols + n) = packed;
+                    }
+                    if (dev) {
+                        // the kGroups threads of one tile row are consecutive lanes (kGroups divides 64)
+#pragma unroll
+                        for (int o = kGroups / 2; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o, kGroups);
+                        if (cg == 0 && m < g.n_sel) g.dev_parts[(2 * m + (SEG - 1)) * (seg_cols / BN) + nt] = dsum;
+                    }
+                }
             }
         }
-    }
+    };
+    if (seg == 0) epilogue(std::integral_constant<int, 0>{});
+    else if (seg == 1) epilogue(std::integral_constant<int, 1>{});
+    else epilogue(std::integral_constant<int, 2>{});
 }
 
 }  // namespace
