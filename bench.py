@@ -32,6 +32,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3        # MI355X fp32 vector (and fp32 matrix)
 
 
 def parse():
@@ -52,6 +53,9 @@ def parse():
                          "every layer and row gathered before the first layer")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
+    ap.add_argument("--fp32", action="store_true",
+                    help="instead of the hot path: time the fp32 partial prefill (projection, attention) on the "
+                         "tiny fp32 configuration and on a larger fp32 shape and print its JSON line")
     ap.add_argument("--dynamic-recompute", action="store_true",
                     help="time the average attention score per token and the dynamic recompute set instead")
     ap.add_argument("--schedule", choices=("fixed", "dynamic"), default="fixed",
@@ -515,6 +519,55 @@ def dynamic_recompute_line(torch, np, ss, cfg, args):
     print(json.dumps(out), flush=True)
 
 
+def fp32_line(torch, np, ss, cfg, args):
+    """The fp32 path (VALU kernels, no matrix cores): one partial-prefill
+    layer, projection and attention timed separately, on the tiny fp32
+    configuration (512 tokens, hidden 256, 4/4 heads, head_dim 64, f = 0.2)
+    and on a larger fp32 shape (4096 tokens, hidden 1024, 8/8 heads, f = 0.25).
+    Bound: fp32 vector ALU, peak 157.3 TFLOP/s."""
+    import workloads
+    out = {"metric": "fp32_partial_prefill_TFLOPs", "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "higher_is_better": True, "data": "synthetic", "dtype": "f32",
+           "config": {"workload": "one fp32 partial-prefill layer: 512 tok / hidden 256 / 4-4 heads / D 64 / f 0.2, "
+                                  "and 4096 tok / hidden 1024 / 8-8 heads / D 64 / f 0.25"}, "shapes": {}}
+    for T, d, hq, hkv, D, f in ((cfg.n_tok, cfg.dim, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, 0.2),
+                                (4096, 1024, 8, 8, 64, 0.25)):
+        n = int(np.floor(f * T + 0.5))
+        g = torch.Generator(device="cuda").manual_seed(T)
+        x = torch.randn(n, d, device="cuda", generator=g)
+        wq = torch.randn(hq * D, d, device="cuda", generator=g) * 0.02
+        wk = torch.randn(hkv * D, d, device="cuda", generator=g) * 0.02
+        wv = torch.randn(hkv * D, d, device="cuda", generator=g) * 0.02
+        kc = torch.randn(T, hkv, D, device="cuda", generator=g)
+        vc = torch.randn(T, hkv, D, device="cuda", generator=g)
+        sel = workloads.make_sel_pos(cfg, T, n, tag=500 + T)
+        pos = torch.from_numpy(sel).cuda()
+        q, _ = ss.qkv_rope(x, pos, wq, wk, wv, kc, vc, hq, hkv)
+        o = ss.prefill_attention(q, pos, kc, vc, hkv)
+        res = {}
+        for name, fn, flops in (("qkv", lambda: ss.qkv_rope(x, pos, wq, wk, wv, kc, vc, hq, hkv, q_out=q),
+                                 2.0 * n * (hq + 2 * hkv) * D * d),
+                                ("attention", lambda: ss.prefill_attention(q, pos, kc, vc, hkv, out=o),
+                                 4.0 * D * hq * float((sel.astype(np.float64) + 1).sum()))):
+            for _ in range(args.warmup):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / args.steps * 1e3
+            tf = flops / (us * 1e-6) / 1e12
+            res[name] = {"us_per_call": round(us, 2), "flops": flops,
+                         "roofline": {"bound": "alu", "achieved": tf, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                      "frac": tf / FP32_PEAK_TFLOPS}}
+        out["shapes"][f"{T}tok_h{d}_{hq}x{D}_n{n}"] = res
+    out["value"] = list(out["shapes"].values())[-1]["attention"]["roofline"]["achieved"]
+    print(json.dumps(out), flush=True)
+
+
 def dynamic_schedule_line(torch, np, ss, cfg, args):
     """The step with the dynamic schedule on the headline shape (32 Llama-3-8B
     shaped layers, 5120 tokens): first layer in full with the deviation against
@@ -586,6 +639,9 @@ def main():
         return
     if args.dynamic_recompute:
         dynamic_recompute_line(torch, np, ss, CONFIGS[2], args)
+        return
+    if args.fp32:
+        fp32_line(torch, np, ss, CONFIGS[0], args)
         return
     if args.schedule == "dynamic":
         dynamic_schedule_line(torch, np, ss, CONFIGS[2], args)

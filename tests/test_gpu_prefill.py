@@ -59,6 +59,11 @@ def _check(cfg, got, ref, x_sel, sel, w, k0, v0):
 @pytest.mark.parametrize("name,cid,n_tok,hidden,hq,hkv,d,n_sel", [
     ("tiny-fp32", 0, 512, 256, 4, 4, 64, 102),
     ("fp32-gqa", 0, 200, 128, 4, 2, 32, 50),
+    # fp32 projection over several 64-row / 64-column tiles with ragged rows; the attention's tiled form
+    # (at least 256 (16-row block, head) pairs) at each head_dim it is built for
+    ("fp32-d128-tiles", 0, 2100, 512, 8, 2, 128, 600),
+    ("fp32-d64-tiles", 0, 3000, 256, 16, 4, 64, 400),
+    ("fp32-d32-tiles", 0, 1500, 128, 16, 16, 32, 300),
     ("bf16-gqa4-ragged-split", 1, 300, 256, 8, 2, 128, 75),
     ("bf16-d64", 1, 200, 256, 4, 2, 64, 60),
     ("bf16-mha", 1, 260, 256, 2, 2, 128, 130),
