@@ -6,17 +6,23 @@
 // P_h[i][j] of every head h, averaged over the heads and over the query rows
 // i (rows before j contribute zero).  Two MFMA passes over the causal score
 // matrix, bf16 operands and fp32 accumulation, exponentials in base 2:
-//   mass_lse_kernel  one wave per (2 query blocks of 32, head): S^T = K Q^T,
-//                    so each lane owns a query column and keeps its row's
-//                    running max and sum over its 16 keys per block; the
-//                    two lane halves merge at the end -> lse2[h][i].
-//   mass_col_kernel  one wave per (2 key blocks of 32, head): S = Q K^T, so
+//   mass_lse_kernel  four waves per (8 query blocks of 32, head), two blocks
+//                    each: S^T = K Q^T, so each lane owns a query column and
+//                    keeps its row's running max and sum over its 16 keys per
+//                    block; the two lane halves merge at the end -> lse2[h][i].
+//   mass_col_kernel  four waves per (8 key blocks of 32, head): S = Q K^T, so
 //                    each lane owns a key column and sums exp2(s - lse2[i])
 //                    over its 16 rows per block -> part[h][j].
 //   mass_final_kernel sums the heads in a fixed order and divides by H_q T.
 // Each wave keeps the operands of its 2 fixed blocks (queries, resp. keys)
-// in VGPRs and streams the other operand from global memory, one 32 x 128
-// tile feeding 2 x 8 MFMAs, the next tile's loads in flight meanwhile.
+// in VGPRs; the other operand streams through a 4-stage LDS ring of 32-row
+// tiles filled by direct-to-LDS loads and shared by the workgroup's 4 waves,
+// one 32 x 128 tile feeding 2 x 8 MFMAs per wave (with one wave per
+// workgroup streaming its own tiles from L2, 790 instead of 652 us at 5120
+// tokens, bit-identical).  The normaliser pass takes no per-tile maximum: each
+// lane exponentiates against a reference it saw earlier and falls back to the
+// tile's maximum only while it has none or when the tile's sum exceeds 2^64
+// (652 -> 612 us; fp32 sums keep their relative precision above 1).
 //
 // dyn_select_kernel (one workgroup): tokens sorted by mass (descending, lower
 // position first on ties); AR is the smallest count whose prefix reaches
@@ -40,13 +46,70 @@ __device__ __forceinline__ bf16x8_t ld8(const uint16_t* p) {
 // lane -> row of the 32 x 32 MFMA output held in accumulator v
 __device__ __forceinline__ int out_row(int v, int half) { return 8 * (v >> 2) + 4 * half + (v & 3); }
 
-__global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-                                                       int64_t T, int32_t Hq, int32_t Hkv, float scale_log2e,
-                                                       float* __restrict__ lse2) {
-    const int lane = threadIdx.x, half = lane >> 5, l32 = lane & 31;
+// The streamed operand (K for the normalisers, Q for the column sums) goes
+// through a 4-stage LDS ring of 32-row tiles (32 x 128 bf16 = 8 KB) filled by
+// direct-to-LDS loads and shared by the 4 waves of a workgroup, which own 8
+// consecutive fixed blocks (2 each).  Rows are 256 B; 16-byte chunk c of row
+// r sits at chunk c ^ (r & 15), so the 16 rows that one MFMA operand read
+// touches at a time cover all banks.
+constexpr int kMassWaves = 4;
+constexpr int kMassStages = 4;
+constexpr int kMassTile = 32 * 128 * 2;                 // bytes
+constexpr int kMassLoads = kMassTile / 1024 / kMassWaves;  // 1-KB direct loads per wave per tile (2)
+
+struct MassRing {
+    uint32_t off[kMassLoads];  // per-lane byte offsets of this wave's rows within a tile's first row
+    uint32_t lds;              // LDS base of the ring
+    int wave;
+    // lane -> (row 4 i + lane / 16 of the tile, physical chunk lane % 16)
+    __device__ void init(int64_t row_stride_bytes, int w, uint32_t lds_base) {
+        wave = w;
+        lds = lds_base;
+        const int lane = threadIdx.x & 63;
+#pragma unroll
+        for (int j = 0; j < kMassLoads; ++j) {
+            const int r = 4 * (w * kMassLoads + j) + (lane >> 4);
+            const int pc = lane & 15;
+            off[j] = (uint32_t)(r * row_stride_bytes) + 16u * (uint32_t)(pc ^ (r & 15));
+        }
+    }
+    // tile whose first row is at `base` (rows past the end clamp to `last`, a
+    // row pointer of the operand's last row: computed, never used)
+    __device__ void issue(const uint16_t* base, int64_t rows_left, int64_t row_stride_bytes, int stage) {
+#pragma unroll
+        for (int j = 0; j < kMassLoads; ++j) {
+            const int r = 4 * (wave * kMassLoads + j) + ((threadIdx.x & 63) >> 4);
+            const uint32_t o = r < rows_left ? off[j]
+                                             : off[j] - (uint32_t)((r - (rows_left - 1)) * row_stride_bytes);
+            g2lds(base, o, lds + stage * kMassTile + (wave * kMassLoads + j) * 1024);
+        }
+    }
+    // operand fragment of k-step ks for row l32 (dims 8 half + 16 ks ... + 8)
+    __device__ bf16x8_t frag(int stage, int l32, int half, int ks) const {
+        const uint32_t addr = lds + stage * kMassTile + l32 * 256 + 16u * (uint32_t)((half + 2 * ks) ^ (l32 & 15));
+        return *(const __attribute__((address_space(3))) bf16x8_t*)(uintptr_t)addr;
+    }
+};
+
+// wait until at most N of this wave's tiles are in flight, then meet the other waves
+template <int N>
+__device__ __forceinline__ void ring_wait() {
+    wait_vmcnt<N * kMassLoads>();
+    ring_barrier();
+}
+
+__global__ __launch_bounds__(64 * kMassWaves) void mass_lse_kernel(const uint16_t* __restrict__ q,
+                                                                   const uint16_t* __restrict__ k, int64_t T,
+                                                                   int32_t Hq, int32_t Hkv, float scale_log2e,
+                                                                   float* __restrict__ lse2) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[kMassStages * kMassTile];
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = blockIdx.y, kvh = h / (Hq / Hkv);
     const int64_t nb = (T + 31) / 32;
-    const int64_t qb0 = (int64_t)blockIdx.x * kNB;
+    // the workgroups with the longest key ranges first
+    const int64_t wg0 = ((int64_t)gridDim.x - 1 - blockIdx.x) * (2 * kMassWaves);
+    const int64_t qb0 = wg0 + 2 * wave;
     bf16x8_t bq[kNB][8];
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
@@ -59,15 +122,28 @@ __global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict
     float m[kNB], l[kNB];
 #pragma unroll
     for (int b = 0; b < kNB; ++b) { m[b] = kNegInf; l[b] = 0.0f; }
-    const int64_t kb_end = qb0 + kNB < nb ? qb0 + kNB : nb;
-    auto load_k = [&](int64_t kb, bf16x8_t (&ak)[8]) {
-        int64_t kj = kb * 32 + l32;
-        if (kj >= T) kj = T - 1;
-        const uint16_t* krow = k + (kj * Hkv + kvh) * 128 + 8 * half;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) ak[ks] = ld8(krow + 16 * ks);
+    // key tiles of the workgroup: up to its last query block
+    const int64_t kb_end = wg0 + 2 * kMassWaves < nb ? wg0 + 2 * kMassWaves : nb;
+    const int64_t kstride = (int64_t)Hkv * 128 * 2;  // bytes between key rows
+    const uint16_t* kbase = k + (int64_t)kvh * 128;
+    MassRing ring;
+    ring.init(kstride, wave, lds_addr(smem));
+    auto issue = [&](int64_t kb) {
+        ring.issue(kbase + kb * 32 * (int64_t)Hkv * 128, T - kb * 32, kstride, (int)(kb & (kMassStages - 1)));
     };
-    auto tile = [&](int64_t kb, const bf16x8_t (&ak)[8]) {
+    for (int64_t kb = 0; kb < kMassStages - 1; ++kb)
+        if (kb < kb_end) issue(kb);
+    for (int64_t kb = 0; kb < kb_end; ++kb) {
+        // tile kb has landed: in flight after it are at most tiles kb + 1, kb + 2
+        if (kb + 2 < kb_end) ring_wait<2>();
+        else if (kb + 1 < kb_end) ring_wait<1>();
+        else ring_wait<0>();
+        // every wave is past tile kb - 1: its stage takes tile kb + 3
+        if (kb + kMassStages - 1 < kb_end) issue(kb + kMassStages - 1);
+        const int st = (int)(kb & (kMassStages - 1));
+        bf16x8_t ak[8];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) ak[ks] = ring.frag(st, l32, half, ks);
 #pragma unroll
         for (int b = 0; b < kNB; ++b) {
             if (kb > qb0 + b) continue;  // wave-uniform: the block lies above the diagonal
@@ -75,38 +151,38 @@ __global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], acc, 0, 0, 0);
             // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32];
-            // only the diagonal block has keys after its queries
-            // the max is taken on the raw scores (the scale is positive) and
-            // the scale folded into one fma per score
-            float bm = kNegInf;
+            // only the diagonal block has keys after its queries; the max is
+            // taken on the raw scores (the scale is positive) and the scale
+            // folded into one fma per score
             if (kb == qb0 + b) {
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
+                for (int v = 0; v < 16; ++v)
                     if (out_row(v, half) > l32) acc[v] = kNegInf;
-                    bm = fmaxf(bm, acc[v]);
-                }
+            }
+            // exponentials against the lane's reference m (a maximum seen
+            // earlier, scaled); only while none is set, or when the tile's sum
+            // shows values far above it, the tile's own maximum becomes the
+            // reference and l is rescaled
+            float sum = 0.0f;
+            if (m[b] != kNegInf) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -m[b]));
+            }
+            if (m[b] != kNegInf && sum <= 0x1p64f) {
+                l[b] += sum;
             } else {
+                float bm = kNegInf;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) bm = fmaxf(bm, acc[v]);
-            }
-            const float mn = fmaxf(m[b], bm * scale_log2e);
-            if (mn == kNegInf) continue;  // no key of this half seen yet
-            float sum = 0.0f;
+                const float mn = fmaxf(m[b], bm * scale_log2e);
+                if (mn == kNegInf) continue;  // no key of this half seen yet
+                sum = 0.0f;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -mn));
-            l[b] = l[b] * __builtin_amdgcn_exp2f(m[b] - mn) + sum;
-            m[b] = mn;
+                for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -mn));
+                l[b] = (m[b] == kNegInf ? 0.0f : l[b] * __builtin_amdgcn_exp2f(m[b] - mn)) + sum;
+                m[b] = mn;
+            }
         }
-    };
-    // the next tile's loads are in flight while the current one is used
-    bf16x8_t ka[8], kc[8];
-    load_k(0, ka);
-    for (int64_t kb = 0; kb < kb_end; kb += 2) {
-        if (kb + 1 < kb_end) load_k(kb + 1, kc);
-        tile(kb, ka);
-        if (kb + 1 >= kb_end) break;
-        if (kb + 2 < kb_end) load_k(kb + 2, ka);
-        tile(kb + 1, kc);
     }
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
@@ -119,14 +195,19 @@ __global__ __launch_bounds__(64) void mass_lse_kernel(const uint16_t* __restrict
     }
 }
 
-__global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-                                                       int64_t T, int64_t row_begin, int32_t Hq, int32_t Hkv,
-                                                       float scale_log2e, const float* __restrict__ lse2,
-                                                       float* __restrict__ part) {
-    const int lane = threadIdx.x, half = lane >> 5, l32 = lane & 31;
+__global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_t* __restrict__ q,
+                                                                   const uint16_t* __restrict__ k, int64_t T,
+                                                                   int64_t row_begin, int32_t Hq, int32_t Hkv,
+                                                                   float scale_log2e,
+                                                                   const float* __restrict__ lse2,
+                                                                   float* __restrict__ part) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[kMassStages * kMassTile];
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = blockIdx.y, kvh = h / (Hq / Hkv);
     const int64_t nb = (T + 31) / 32;
-    const int64_t kb0 = (int64_t)blockIdx.x * kNB;
+    const int64_t wg0 = (int64_t)blockIdx.x * (2 * kMassWaves);  // the longest row ranges first
+    const int64_t kb0 = wg0 + 2 * wave;
     bf16x8_t bk[kNB][8];
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
@@ -140,19 +221,40 @@ __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict
 #pragma unroll
     for (int b = 0; b < kNB; ++b) col[b] = 0.0f;
     const float* lse_h = lse2 + (int64_t)h * T;
-    auto load_q = [&](int64_t qb, bf16x8_t (&aq)[8], float (&L)[16]) {
-        int64_t qi = qb * 32 + l32;
-        if (qi >= T) qi = T - 1;
-        const uint16_t* qrow = q + (qi * Hq + h) * 128 + 8 * half;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) aq[ks] = ld8(qrow + 16 * ks);
+    // row tiles of the workgroup: from its first key block (or the window) to the end
+    const int64_t qb_first = wg0 > row_begin / 32 ? wg0 : row_begin / 32;
+    const int64_t qstride = (int64_t)Hq * 128 * 2;
+    const uint16_t* qbase = q + (int64_t)h * 128;
+    MassRing ring;
+    ring.init(qstride, wave, lds_addr(smem));
+    auto issue = [&](int64_t qb) {
+        ring.issue(qbase + qb * 32 * (int64_t)Hq * 128, T - qb * 32, qstride,
+                   (int)((qb - qb_first) & (kMassStages - 1)));
+    };
+    for (int64_t qb = qb_first; qb < qb_first + kMassStages - 1; ++qb)
+        if (qb < nb) issue(qb);
+    float Ln[16];  // the next tile's normalisers
+    auto load_l = [&](int64_t qb, float (&L)[16]) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int64_t r = qb * 32 + out_row(v, half);
             L[v] = r < T && r >= row_begin ? lse_h[r] : __builtin_inff();  // rows outside the window add 0
         }
     };
-    auto tile = [&](int64_t qb, const bf16x8_t (&aq)[8], const float (&L)[16]) {
+    if (qb_first < nb) load_l(qb_first, Ln);
+    for (int64_t qb = qb_first; qb < nb; ++qb) {
+        float L[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) L[v] = Ln[v];
+        if (qb + 2 < nb) ring_wait<2>();
+        else if (qb + 1 < nb) ring_wait<1>();
+        else ring_wait<0>();
+        if (qb + kMassStages - 1 < nb) issue(qb + kMassStages - 1);
+        if (qb + 1 < nb) load_l(qb + 1, Ln);
+        const int st = (int)((qb - qb_first) & (kMassStages - 1));
+        bf16x8_t aq[8];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) aq[ks] = ring.frag(st, l32, half, ks);
 #pragma unroll
         for (int b = 0; b < kNB; ++b) {
             if (qb < kb0 + b) continue;  // wave-uniform: every row of the block precedes the keys
@@ -171,17 +273,6 @@ __global__ __launch_bounds__(64) void mass_col_kernel(const uint16_t* __restrict
                 for (int v = 0; v < 16; ++v) col[b] += __builtin_amdgcn_exp2f(acc[v] * scale_log2e - L[v]);
             }
         }
-    };
-    bf16x8_t qa[8], qc[8];
-    float La[16], Lc[16];
-    const int64_t qb_first = kb0 > row_begin / 32 ? kb0 : row_begin / 32;
-    if (qb_first < nb) load_q(qb_first, qa, La);
-    for (int64_t qb = qb_first; qb < nb; qb += 2) {
-        if (qb + 1 < nb) load_q(qb + 1, qc, Lc);
-        tile(qb, qa, La);
-        if (qb + 1 >= nb) break;
-        if (qb + 2 < nb) load_q(qb + 2, qa, La);
-        tile(qb + 1, qc, Lc);
     }
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
@@ -474,15 +565,16 @@ hipError_t launch_attention_mass(const void* q, const void* k, int64_t n_tok, in
     float* part = lse2 + (int64_t)n_q_heads * n_tok;
     const float sl2e = sm_scale * 1.4426950408889634f;
     const int64_t nb = (n_tok + 31) / 32;
-    const dim3 grid((unsigned)((nb + kNB - 1) / kNB), (unsigned)n_q_heads);
+    const dim3 grid((unsigned)((nb + 2 * kMassWaves - 1) / (2 * kMassWaves)), (unsigned)n_q_heads);
     const auto* qp = static_cast<const uint16_t*>(q);
     const auto* kp = static_cast<const uint16_t*>(k);
     // the row normalisers do not depend on row_begin: a window pass after a
     // pass over the same q and K finds them in the workspace
     if (!reuse_normalisers)
-        hipLaunchKernelGGL(mass_lse_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads, sl2e, lse2);
-    hipLaunchKernelGGL(mass_col_kernel, grid, dim3(64), 0, s, qp, kp, n_tok, row_begin, n_q_heads, n_kv_heads, sl2e,
-                       lse2, part);
+        hipLaunchKernelGGL(mass_lse_kernel, grid, dim3(64 * kMassWaves), 0, s, qp, kp, n_tok, n_q_heads, n_kv_heads,
+                           sl2e, lse2);
+    hipLaunchKernelGGL(mass_col_kernel, grid, dim3(64 * kMassWaves), 0, s, qp, kp, n_tok, row_begin, n_q_heads,
+                       n_kv_heads, sl2e, lse2, part);
     hipLaunchKernelGGL(mass_final_kernel, dim3((unsigned)((n_tok + 255) / 256)), dim3(256), 0, s, part, n_tok,
                        n_tok - row_begin, n_q_heads, mass);
     return hipGetLastError();
