@@ -80,8 +80,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "48ba106da7ee37b2143538bfcdf5f61765758f927e94117ab34ca2512136e1a4",
-                "bytes_per_call": 93986446}
+ATTN_TRAFFIC = {"source_sha256": "68012bbe8eea6bd67f0525947982761e646050b93cbba80b96d30a66f8733801",
+                "bytes_per_call": 93505174}
 
 
 def source_sha256(rel):
