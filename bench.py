@@ -80,8 +80,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "68012bbe8eea6bd67f0525947982761e646050b93cbba80b96d30a66f8733801",
-                "bytes_per_call": 93505174}
+ATTN_TRAFFIC = {"source_sha256": "7f055f5adb28bd00e3d9e99552c61bae08e5ed3f0b5d5156eb03de260bf2ebc6",
+                "bytes_per_call": 94070969}
 
 
 def source_sha256(rel):

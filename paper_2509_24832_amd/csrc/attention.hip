@@ -691,9 +691,9 @@ __global__ __launch_bounds__(64 * kNW, 1) void attention_kernel(AttnArgs a) {
 }
 
 // Log-sum-exp merge of a cut row tile's pieces.  One workgroup per (cut row
-// tile, wave slice, column block, kv head): the 32 columns x D values that
-// attention wave `wave` held in block nb, laid out as [i][r][lane] f32x4 per
-// piece, so every load is a coalesced 1 KB row.  Thread t handles lane
+// tile, 32-column block, kv head): the 32 columns x D values of block cb
+// (attention wave cb held them), laid out as [i][r][lane] f32x4 per piece,
+// so every load is a coalesced 1 KB row.  Thread t handles lane
 // t % 64 and the (i, r) pairs t / 64 + 4k.  Head g runs on the XCD that
 // wrote its pieces (b % 8 == g with 8 kv heads).  Pieces are read kPc at a
 // time, all their loads in flight together, and merged into a running
@@ -705,13 +705,13 @@ __device__ __forceinline__ void combine_item(const AttnArgs& a, const int32_t* h
     constexpr int kPc = 4;
     const int g = item % a.Hkv;
     const int rest = item / a.Hkv;
-    const int wave = (rest >> 1) & 3, nb = rest & 1;
+    const int cb = rest & 7;  // 32-column block of the tile
     const int k = rest >> 3;  // cut row tile
     const int32_t* ent = hdr + kPlanHdr + 4 * a.P + 8 * a.n_tiles + 4 * k;
     const int tile = sload(ent), pbase = sload(ent + 1), nu = sload(ent + 2);
     const int tid = threadIdx.x, lane = tid & 63, q4 = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
-    const int col = 64 * wave + 32 * nb + l32;
+    const int col = 32 * cb + l32;
     const int64_t row = ((int64_t)tile << a.lgR) + (col & (a.R - 1));
     if (row >= a.n_sel) return;
     const int32_t p = a.pos[row];
@@ -719,8 +719,8 @@ __device__ __forceinline__ void combine_item(const AttnArgs& a, const int32_t* h
     const float cl2 = a.cl2;
     const int64_t sl0 = (int64_t)g * a.max_slots + pbase;
     const float2* ml = a.part_ml + sl0 * NCOL + col;
-    const u32x2_t* po0 = a.part_o + ((sl0 * 4 + wave) * 2 + nb) * (kMd * 4 * 64) + lane;
-    constexpr int64_t kPieceStride = 4 * 2 * kMd * 4 * 64;  // u32x2 per slot
+    const u32x2_t* po0 = a.part_o + (sl0 * 8 + cb) * (kMd * 4 * 64) + lane;
+    constexpr int64_t kPieceStride = 8 * kMd * 4 * 64;  // u32x2 per slot (8 column blocks)
     float M = -1.0e30f, L = 0.0f;
     f32x4_t o[kPer];
 #pragma unroll
@@ -774,7 +774,7 @@ __device__ __forceinline__ void combine_item(const AttnArgs& a, const int32_t* h
     }
 }
 
-// Items (cut row tile, wave slice, column block, kv head) in strides of the
+// Items (cut row tile, column block, kv head) in strides of the
 // grid, which the launch keeps at a multiple of 8 and far below the item
 // bound, so that workgroups are not spent on items a call does not have.
 template <int D>
