@@ -295,6 +295,39 @@ def stage_times(torch, path, reps):
     return out
 
 
+def flushed_medians(torch, path, reps):
+    """Median durations over `reps` single runs, each after a 512 MiB write
+    that pushes the previous run's data out of L2 and the 256 MB Infinity
+    Cache: one whole step, and one partial-layer prefill_attention call (a
+    layer in the middle of the stack).  A HIP event pair on the launch stream
+    brackets each run; the flush is outside it."""
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    mid = max(1, path.L // 2)
+
+    def runs(fn):
+        t = []
+        for _ in range(reps):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1))
+        t.sort()
+        return {"median_ms": t[len(t) // 2] if len(t) % 2 else 0.5 * (t[len(t) // 2 - 1] + t[len(t) // 2]),
+                "min_ms": t[0], "max_ms": t[-1]}
+
+    path.step()
+    out = {"reps": reps, "flush_bytes": flush.numel(), "step": runs(path.step),
+           "attn_partial_layer": runs(lambda: path.s_attn(mid))}
+    path.step()
+    torch.cuda.synchronize()
+    del flush
+    return out
+
+
 def attention_flops(sel_pos, hq, D):
     """4 * D * Hq * sum_s (p_s + 1): QK^T and PV multiply-adds of causal attention."""
     return 4.0 * D * hq * float((sel_pos.astype("float64") + 1.0).sum())
@@ -347,7 +380,7 @@ def cpu_baseline(cfg, frac, budget_s):
     sample = (f"oracle on {nr} of {T} rows for RoPE/LSH/match, 1 of {2 * L} gathered layer tensors, {nq} selected "
               f"rows for QKV and attention; each stage scaled by its work to one full step (f={frac}), extrapolated")
     return {"value": T / total, "unit": "tokens/s", "cores": orc.num_threads(), "kind": "oracle", "sample": sample,
-            "est_step_s": total, "est_stage_s": {k2: round(v2, 3) for k2, v2 in est.items()}}
+            "est_step_s": total, "est_stage_s": {k2: round(v2, 6) for k2, v2 in est.items()}}
 
 
 def bank_similarity_line(torch, np, ss, cfg, args):
@@ -668,6 +701,8 @@ def main():
     ms, wall_ms = time_steps(torch, path, args.steps, args.warmup)
     # per-call durations: each stage timed as a run of its own calls after the timed region
     stages = stage_times(torch, path, max(2, args.steps // 4))
+    # medians of single runs with the caches flushed before each (after the timed region, which warmed up)
+    flushed = flushed_medians(torch, path, max(20, args.steps))
     sel_h = path.sel.cpu().numpy()
     T, L, hq, hkv, D, d = path.T, path.L, path.hq, path.hkv, path.D, path.d
     n_sel = path.n_sel
@@ -719,6 +754,7 @@ def main():
         "stage_sum_ms_per_step": sum(v for k, v in stages.items() if k not in ("qkv", "attn")) +
                                  (L - 1) * (stages["qkv"] + stages["attn"]),
         "wall_ms_per_step": wall_ms,
+        "flushed_median": flushed,
         "gather": {"GB/s": gather_bytes / (gather_ms * 1e-3) / 1e9, "frac_of_hbm": gather_bytes / (gather_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS},
         "attention_TFLOPs": {"partial_layer": attn_flops / (attn_ms * 1e-3) / 1e12,
                              "layer0_full": attn0_flops / (attn0_ms * 1e-3) / 1e12},

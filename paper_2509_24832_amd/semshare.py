@@ -279,7 +279,8 @@ def gather_kv(ref_k: torch.Tensor, ref_v: Optional[torch.Tensor], idx: torch.Ten
               out_k: Optional[torch.Tensor] = None, out_v: Optional[torch.Tensor] = None,
               except_pos: Optional[torch.Tensor] = None, n_except: Optional[int] = None):
     """out[l][t] = ref[l][idx[t]]; ref_* [L, n_ref, Hkv, D] -> out_* [L, n_tgt, Hkv, D].  With except_pos
-    (strictly ascending int32 target rows; the first n_except of it, 0 <= n_except <= except_pos.numel())
+    (ascending int32 target rows, repeats allowed; the first n_except of it, 0 <= n_except <=
+    min(except_pos.numel(), n_tgt))
     those rows are left as they are."""
     _dev(ref_k, "ref_k")
     _dev(idx, "idx", torch.int32)

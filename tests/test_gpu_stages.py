@@ -237,14 +237,17 @@ def test_gather_kv_bitwise(cid, L, n_ref, n_tgt):
     assert np.array_equal(host(ov), orc.gather_rows(v, idx))
 
 
-@pytest.mark.parametrize("n_except", [0, 1, 250, 1000])
-def test_gather_except_leaves_listed_rows(n_except):
+@pytest.mark.parametrize("n_except,repeats", [(0, False), (1, False), (250, False), (1000, False), (600, True)])
+def test_gather_except_leaves_listed_rows(n_except, repeats):
+    """The list is ascending, not necessarily strict: with repeats (600 draws
+    with replacement) every listed row is still left alone exactly once."""
     cfg = CONFIGS[1]
     L, n_ref, n_tgt = 3, 777, 1000
-    announce(f"gather except n_except={n_except}")
+    announce(f"gather except n_except={n_except} repeats={repeats}")
     k, v = workloads.make_cache(cfg, L, n_ref, tag=9)
     idx = np.random.default_rng(9).integers(0, n_ref, n_tgt).astype(np.int32)
-    exc = np.sort(np.random.default_rng(10).choice(n_tgt, n_except, replace=False)).astype(np.int32)
+    exc = np.sort(np.random.default_rng(10).choice(n_tgt, n_except, replace=repeats)).astype(np.int32)
+    assert not repeats or len(np.unique(exc)) < n_except
     ok = torch.full((L, n_tgt) + k.shape[2:], 7.0, dtype=torch.bfloat16, device="cuda")
     ov = torch.full((L, n_tgt) + k.shape[2:], -3.0, dtype=torch.bfloat16, device="cuda")
     ss.gather_kv(dev(k, "bf16"), dev(v, "bf16"), dev_i32(idx), out_k=ok, out_v=ov, except_pos=dev_i32(exc))
