@@ -832,13 +832,25 @@ __global__ __launch_bounds__(1024) void plan_kernel(AttnArgs a) {
         s_lo[tid] = INT_MAX;
         s_hi[tid] = -1;
         __syncthreads();
+        // each wave's 64 rows are aligned segments of min(R, 64) rows of one
+        // row tile: reduced in registers, one LDS update per segment
         const int64_t r0 = (int64_t)base * a.R, r1 = min(a.n_sel, (int64_t)(base + 1024) * a.R);
-        for (int64_t r = r0 + tid; r < r1; r += 1024) {
-            const int32_t p = a.pos[r];
-            if (p >= 0 && p < a.n_tok) {
+        const int seg = a.R < 64 ? a.R : 64;
+        for (int64_t rb = r0; rb < r1; rb += 1024) {  // the same trip count in every lane
+            const int64_t r = rb + tid;
+            int32_t lo = INT_MAX, hi = -1;
+            if (r < r1) {
+                const int32_t p = a.pos[r];
+                if (p >= 0 && p < a.n_tok) lo = hi = p;
+            }
+            for (int o = 1; o < seg; o <<= 1) {
+                lo = min(lo, __shfl_xor(lo, o));
+                hi = max(hi, __shfl_xor(hi, o));
+            }
+            if ((tid & (seg - 1)) == 0 && r < r1 && hi >= 0) {
                 const int k = (int)(r / a.R - base);
-                atomicMin(&s_lo[k], p);
-                atomicMax(&s_hi[k], p);
+                atomicMin(&s_lo[k], lo);
+                atomicMax(&s_hi[k], hi);
             }
         }
         __syncthreads();

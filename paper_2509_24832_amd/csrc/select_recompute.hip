@@ -2,16 +2,24 @@
 // n_sel positions of largest deviation, ties to the lower position, emitted
 // in ascending order.
 //
-// One 1024-thread workgroup.  For non-negative floats the bit pattern orders
+// One 1024-thread workgroup; thread t owns the contiguous positions
+// [t E, t E + E), E = ceil(n / 1024), held in registers when E <= 8 (read
+// once, through LDS so the global reads are coalesced) and read again from
+// global memory otherwise.  For non-negative floats the bit pattern orders
 // like the value, so a 4-pass, 8-bit-digit radix select over the bits finds
 // the threshold value T with count(> T) < n_sel <= count(>= T); each pass
-// finds its digit by a block-wide scan of the 256 counts.  A final pass
-// walks the positions in order and keeps every value > T plus the first
-// (n_sel - count(> T)) values == T, compacting with block-wide prefix sums,
-// which yields the ascending output directly.  With a candidate map the
-// values belong to candidates map[0 .. n) (ascending positions, e.g. the
-// tokens the previous layer recomputed) and the selected candidates'
-// positions are written instead of their indices.
+// finds its digit by a block-wide scan of the 256 counts.  The counts are
+// aggregated per wave before they reach the LDS histogram (the lanes sharing
+// the first pending lane's digit add once, twice over, then the rest one by
+// one): deviations share their exponent, and 64 lanes adding to one LDS
+// word would otherwise take turns.  The output is one block-wide scan of
+// each thread's (> T, == T) counts: with G and E the counts before a
+// position, a position > T goes to G + min(E, need) and a position == T with
+// E < need to G + E, where need is the number of copies of T taken; this
+// yields the ascending output directly.  With a candidate map the values
+// belong to candidates map[0 .. n) (ascending positions, e.g. the tokens the
+// previous layer recomputed) and the selected candidates' positions are
+// written instead of their indices.
 #include "semshare_internal.h"
 
 namespace semshare {
@@ -50,13 +58,51 @@ __device__ __forceinline__ void block_scan2(uint32_t a, uint32_t b, uint32_t& ea
     __syncthreads();
 }
 
+constexpr int kReg = 8;  // positions per thread held in registers (n <= 8192)
+
+// Adds one count for digit d of every lane with act set, aggregated per wave
+// (all lanes of the wave call it together).
+__device__ __forceinline__ void add_digit(uint32_t* hist, uint32_t d, bool act) {
+    const int lane = threadIdx.x & 63;
+    bool pend = act;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const uint64_t live = __ballot(pend);
+        if (live == 0) return;
+        const int lead = __ffsll((unsigned long long)live) - 1;
+        const uint32_t dl = __shfl(d, lead);
+        const bool mine = pend && d == dl;
+        const uint64_t same = __ballot(mine);
+        if (lane == lead) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
+        if (mine) pend = false;
+    }
+    if (pend) atomicAdd(&hist[d], 1u);
+}
+
+template <bool kInRegs>
 __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ sigma, int32_t n_tok,
                                                     int32_t n_sel, const int32_t* __restrict__ map,
                                                     int32_t* __restrict__ out) {
     __shared__ uint32_t hist[256];
     __shared__ uint32_t s_digit, s_need;
     __shared__ uint32_t sw[kWaves][2];
+    __shared__ uint32_t s_keys[kInRegs ? kT * kReg : 1];
     const int tid = threadIdx.x;
+    const int32_t per = (n_tok + kT - 1) / kT;  // positions per thread (the same for every thread)
+    const int32_t i0 = tid * per;
+    const int32_t cnt = n_tok - i0 < 0 ? 0 : (n_tok - i0 < per ? n_tok - i0 : per);
+
+    uint32_t key[kInRegs ? kReg : 1];
+    if constexpr (kInRegs) {
+        for (int32_t i = tid; i < n_tok; i += kT) s_keys[i] = key_of(sigma[i]);
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kReg; ++j) key[j] = j < cnt ? s_keys[i0 + j] : 0u;
+    }
+    auto key_at = [&](int j) -> uint32_t {
+        if constexpr (kInRegs) return key[j];
+        else return key_of(sigma[i0 + j]);
+    };
 
     uint32_t prefix = 0, hi_mask = 0, need = (uint32_t)n_sel;
     for (int shift = 24; shift >= 0; shift -= 8) {
@@ -66,9 +112,18 @@ __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ si
             s_need = need;
         }
         __syncthreads();
-        for (int32_t i = tid; i < n_tok; i += kT) {
-            const uint32_t u = key_of(sigma[i]);
-            if ((u & hi_mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
+        if constexpr (kInRegs) {
+#pragma unroll
+            for (int j = 0; j < kReg; ++j)
+                if (j < per) {  // uniform: every lane of the wave calls add_digit together
+                    const uint32_t u = key[j];
+                    add_digit(hist, (u >> shift) & 255u, j < cnt && (u & hi_mask) == prefix);
+                }
+        } else {
+            for (int32_t j = 0; j < per; ++j) {
+                const uint32_t u = j < cnt ? key_at(j) : 0u;
+                add_digit(hist, (u >> shift) & 255u, j < cnt && (u & hi_mask) == prefix);
+            }
         }
         __syncthreads();
         // the digit: counts of the higher digits summed from the top, the one
@@ -91,20 +146,39 @@ __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ si
     }
     const uint32_t thr = prefix;  // the n_sel-th largest key; `need` of its copies are taken
 
-    uint32_t base = 0, eq_taken = 0;
-    for (int32_t c0 = 0; c0 < n_tok; c0 += kT) {
-        const int32_t i = c0 + tid;
-        const uint32_t u = i < n_tok ? key_of(sigma[i]) : 0u;
-        const uint32_t gt = i < n_tok && u > thr;
-        const uint32_t eq = i < n_tok && u == thr;
-        uint32_t e_eq, e_dummy, t_eq, t_dummy;
-        block_scan2(eq, 0u, e_eq, e_dummy, t_eq, t_dummy, sw);
-        const uint32_t take = gt || (eq && eq_taken + e_eq < need);
-        uint32_t e_take, e_d2, t_take, t_d2;
-        block_scan2(take, 0u, e_take, e_d2, t_take, t_d2, sw);
-        if (take) out[base + e_take] = map ? map[i] : i;
-        base += t_take;
-        eq_taken += t_eq;
+    uint32_t ngt = 0, neq = 0;
+    if constexpr (kInRegs) {
+#pragma unroll
+        for (int j = 0; j < kReg; ++j)
+            if (j < cnt) {
+                ngt += key[j] > thr;
+                neq += key[j] == thr;
+            }
+    } else {
+        for (int32_t j = 0; j < cnt; ++j) {
+            const uint32_t u = key_at(j);
+            ngt += u > thr;
+            neq += u == thr;
+        }
+    }
+    uint32_t g, e, tg, te;
+    block_scan2(ngt, neq, g, e, tg, te, sw);
+    auto emit = [&](int j, uint32_t u) {
+        const int32_t i = i0 + j;
+        if (u > thr) {
+            out[g + (e < need ? e : need)] = map ? map[i] : i;
+            ++g;
+        } else if (u == thr) {
+            if (e < need) out[g + e] = map ? map[i] : i;
+            ++e;
+        }
+    };
+    if constexpr (kInRegs) {
+#pragma unroll
+        for (int j = 0; j < kReg; ++j)
+            if (j < cnt) emit(j, key[j]);
+    } else {
+        for (int32_t j = 0; j < cnt; ++j) emit(j, key_at(j));
     }
 }
 
@@ -112,8 +186,12 @@ __global__ __launch_bounds__(kT) void select_kernel(const float* __restrict__ si
 
 hipError_t launch_select_recompute(const float* sigma, int64_t n_tok, int64_t n_sel,
                                    int32_t* sel_pos, hipStream_t s, const int32_t* map) {
-    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kT), 0, s, sigma, (int32_t)n_tok, (int32_t)n_sel, map,
-                       sel_pos);
+    if (n_tok <= (int64_t)kT * kReg)
+        hipLaunchKernelGGL(select_kernel<true>, dim3(1), dim3(kT), 0, s, sigma, (int32_t)n_tok, (int32_t)n_sel, map,
+                           sel_pos);
+    else
+        hipLaunchKernelGGL(select_kernel<false>, dim3(1), dim3(kT), 0, s, sigma, (int32_t)n_tok, (int32_t)n_sel,
+                           map, sel_pos);
     return hipGetLastError();
 }
 
