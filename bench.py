@@ -80,8 +80,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "7f055f5adb28bd00e3d9e99552c61bae08e5ed3f0b5d5156eb03de260bf2ebc6",
-                "bytes_per_call": 94070969}
+ATTN_TRAFFIC = {"source_sha256": "796989eb5edfb09a50a9a203abafbe24ffdcd40a9ef58be6b821814250c78818",
+                "bytes_per_call": 93604751}
 
 
 def source_sha256(rel):
