@@ -53,6 +53,10 @@ def parse():
                          "every layer and row gathered before the first layer")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
+    ap.add_argument("--vendor-compare", action="store_true",
+                    help="instead of the hot path: time the two dominant operations against the platform's own "
+                         "library path (torch SDPA for the first layer's causal attention, torch.matmul on hipBLASLt "
+                         "for the projection) and print its JSON line")
     ap.add_argument("--fp32", action="store_true",
                     help="instead of the hot path: time the fp32 partial prefill (projection, attention) on the "
                          "tiny fp32 configuration and on a larger fp32 shape and print its JSON line")
@@ -552,6 +556,79 @@ def dynamic_recompute_line(torch, np, ss, cfg, args):
     print(json.dumps(out), flush=True)
 
 
+def vendor_compare_line(torch, np, ss, cfg, args):
+    """The two dominant operations of the step against the platform's own
+    library path on the same box, same inputs (5120 tokens, 32 q / 8 kv heads,
+    head_dim 128, hidden 4096, bf16): the first layer's causal attention over
+    all rows (prefill_attention vs torch's scaled_dot_product_attention, flash
+    backend, grouped-query heads), and a partial layer's projection of the
+    1280 selected rows (qkv_rope, which also applies RoPE and scatters K/V into
+    the cache, vs a plain torch.matmul on hipBLASLt that does neither).  Event
+    timing over runs of back-to-back calls; the largest difference between the
+    two results is reported as a check."""
+    import torch.nn.functional as F
+    T, hq, hkv, D, d = cfg.n_tok, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.dim
+    n_sel = cfg.n_sel(0.25)
+    bf = torch.bfloat16
+    g = torch.Generator(device="cuda").manual_seed(0)
+    q = torch.randn(T, hq, D, device="cuda", generator=g).to(bf)
+    k = torch.randn(T, hkv, D, device="cuda", generator=g).to(bf)
+    v = torch.randn(T, hkv, D, device="cuda", generator=g).to(bf)
+    pos = torch.arange(T, dtype=torch.int32, device="cuda")
+    reps = max(10, args.steps)
+
+    def timed(fn):
+        for _ in range(max(3, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    out = torch.empty_like(q)
+    ws = torch.empty(ss.prefill_attention_workspace_bytes(T, T, hq, hkv, D, bf), dtype=torch.uint8, device="cuda")
+    attn_ours = timed(lambda: ss.prefill_attention(q, pos, k, v, hkv, out=out, workspace=ws))
+    qt, kt, vt = (t.transpose(0, 1).unsqueeze(0).contiguous() for t in (q, k, v))
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+        o = F.scaled_dot_product_attention(qt, kt, vt, is_causal=True, enable_gqa=True)
+        attn_torch = timed(lambda: F.scaled_dot_product_attention(qt, kt, vt, is_causal=True, enable_gqa=True))
+    attn_diff = (o[0].transpose(0, 1).float() - out.float()).abs().max().item()
+    fl = 4.0 * D * hq * T * (T + 1) / 2.0
+    # projection of the selected rows
+    x = (torch.randn(n_sel, d, device="cuda", generator=g) * 0.5).to(bf)
+    w = [(torch.randn(r * D, d, device="cuda", generator=g) * 0.02).to(bf) for r in (hq, hkv, hkv)]
+    sel = torch.sort(torch.randperm(T, device="cuda", generator=g)[:n_sel])[0].to(torch.int32)
+    kc, vc = torch.zeros(T, hkv, D, dtype=bf, device="cuda"), torch.zeros(T, hkv, D, dtype=bf, device="cuda")
+    q_out = torch.empty(n_sel, hq, D, dtype=bf, device="cuda")
+    ws2 = torch.empty(ss.qkv_rope_workspace_bytes(n_sel, hq, hkv, D, bf), dtype=torch.uint8, device="cuda")
+    table = torch.empty(ss.rope_table_bytes(n_sel, D), dtype=torch.uint8, device="cuda")
+    ss.rope_table(sel, T, D, out=table)
+    qkv_ours = timed(lambda: ss.qkv_rope(x, sel, w[0], w[1], w[2], kc, vc, hq, hkv, q_out=q_out, workspace=ws2,
+                                         rope_table=table))
+    wcat = torch.cat(w, 0).contiguous()
+    y = torch.empty(n_sel, wcat.shape[0], dtype=bf, device="cuda")
+    qkv_torch = timed(lambda: torch.matmul(x, wcat.t(), out=y))
+    v_diff = (y[:, (hq + hkv) * D:].float().view(n_sel, hkv, D) - vc[sel.long()].float()).abs().max().item()
+    qfl = 2.0 * n_sel * (hq + 2 * hkv) * D * d
+    out_line = {"metric": "vendor_compare_us", "unit": "us", "n_gpus": 1, "steps": reps, "warmup": args.warmup,
+                "higher_is_better": False, "data": "synthetic", "dtype": "bf16",
+                "config": {"workload": f"first-layer causal attention over {T} tokens (32 q / 8 kv heads, head_dim "
+                                       f"128) and the projection of {n_sel} selected rows (hidden 4096 -> 6144)"},
+                "attention_layer0": {"ours_us": attn_ours, "torch_sdpa_flash_us": attn_torch,
+                                     "ours_TFLOPs": fl / attn_ours / 1e6, "torch_TFLOPs": fl / attn_torch / 1e6,
+                                     "speedup": attn_torch / attn_ours, "max_abs_diff": attn_diff},
+                "qkv_partial": {"ours_us": qkv_ours, "torch_matmul_us": qkv_torch,
+                                "ours_TFLOPs": qfl / qkv_ours / 1e6, "torch_TFLOPs": qfl / qkv_torch / 1e6,
+                                "speedup": qkv_torch / qkv_ours, "v_rows_max_abs_diff": v_diff,
+                                "note": "ours also applies RoPE to q and k and scatters k and v into the cache"}}
+    print(json.dumps(out_line), flush=True)
+
+
 def fp32_line(torch, np, ss, cfg, args):
     """The fp32 path (VALU kernels, no matrix cores): one partial-prefill
     layer, projection and attention timed separately, on the tiny fp32
@@ -672,6 +749,9 @@ def main():
         return
     if args.dynamic_recompute:
         dynamic_recompute_line(torch, np, ss, CONFIGS[2], args)
+        return
+    if args.vendor_compare:
+        vendor_compare_line(torch, np, ss, CONFIGS[2], args)
         return
     if args.fp32:
         fp32_line(torch, np, ss, CONFIGS[0], args)
