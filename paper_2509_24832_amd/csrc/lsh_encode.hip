@@ -141,18 +141,21 @@ __global__ __launch_bounds__(64 * NB) void lsh_encode_ring_kernel(const uint16_t
 // RoPE-embedded rows): the same ring, but each workgroup owns R <= 32 rows
 // (R chosen so that the rows spread over every CU) and rotates the x rows of
 // a chunk in LDS once it has landed, one chunk ahead of the products.
-// The workgroup has twice the MFMA waves: the extra ones load nothing and
-// multiply nothing, they halve the rotation work of each wave and give every
-// SIMD a second wave.  Thread k rotates the pairs k, k + 128 NB, ... of the
-// chunk's R x 32 (even, odd) pairs; since 128 NB is a multiple of 32 its pair
-// column k % 32 is fixed, so its theta follows the chunks by one fp64 multiply (theta_{k+32}
-// = theta_k * base^(-64 / dim)).  The angle is reduced in fp64 revolutions
+// The workgroup has three waves per MFMA wave: the MFMA waves load and
+// multiply, the other 2 NB waves only rotate (measured per chunk with cycle
+// stamps: when the MFMA waves also rotated, the rotation was the longest
+// part of their chunk and the other waves waited at the barrier).  Rotating
+// thread k rotates the pairs k, k + 128 NB, ... of the chunk's R x 32
+// (even, odd) pairs; since 128 NB is a multiple of 32 its pair column k % 32
+// is fixed, so its theta follows the chunks by one fp64 multiply
+// (theta_{k+32} = theta_k * base^(-64 / dim)).  The angle is reduced in fp64 revolutions
 // and rotated with the hardware sine and cosine; the rotated pair is rounded
 // to bf16, as the unfused path stores it.  The codes therefore equal those of
 // rope_embed + lsh_encode except where a projection lies within rounding
 // distance of zero.
-template <int NB>  // n_bits / 32 = MFMA waves (2 or 4); as many more waves only rotate
-__global__ __launch_bounds__(128 * NB) void rope_lsh_ring_kernel(const uint16_t* __restrict__ x,
+constexpr int kRotWaves = 3;  // waves per MFMA wave: 1 multiplies and loads, 2 rotate
+template <int NB>  // n_bits / 32 = MFMA waves (2 or 4); twice as many more waves only rotate
+__global__ __launch_bounds__(64 * kRotWaves * NB) void rope_lsh_ring_kernel(const uint16_t* __restrict__ x,
                                                                 const uint16_t* __restrict__ planes,
                                                                 uint32_t* __restrict__ codes32, int64_t n_tok,
                                                                 int32_t dim, int32_t rows, int64_t pos0,
@@ -167,7 +170,7 @@ __global__ __launch_bounds__(128 * NB) void rope_lsh_ring_kernel(const uint16_t*
     const int64_t last = (row0 + rows < n_tok ? row0 + rows : n_tok) - 1 - row0;  // last live row of the tile
     const uint32_t smem_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)smem;
 
-    const bool mma_wave = wave < NB;  // waves NB .. 2 NB - 1 load nothing and only rotate
+    const bool mma_wave = wave < NB;  // waves NB .. 3 NB - 1 load nothing and only rotate
     // direct-load sources as in lsh_encode_ring_kernel; x rows past the
     // tile's last live row repeat it (computed, never stored)
     uint32_t off[C::kLoadsPerWave];
@@ -215,23 +218,26 @@ __global__ __launch_bounds__(128 * NB) void rope_lsh_ring_kernel(const uint16_t*
     // m theta in revolutions, reduced in fp64, then v_sin_f32 / v_cos_f32
     // (which take revolutions)
     auto rotate = [&](int st_r) {
-        // up to four pairs per thread (R <= 32 rows x 32 pairs over >= 256
-        // threads): all loads first, then four independent chains, then the
-        // stores, so one wave per SIMD still overlaps their latencies
+        // up to four pairs per thread (R <= 32 rows x 32 pairs over the
+        // 128 NB >= 256 rotating threads): all loads first, then independent
+        // chains, then the stores, so that their latencies overlap
         const uint32_t sb = smem_base + st_r * C::kStage;
-        constexpr int kIt = 32 * 32 / (128 * NB);
+        if (mma_wave) return;
+        const int rt = tid - 64 * NB;  // thread index among the rotating waves
+        constexpr int kRt = 64 * (kRotWaves - 1) * NB;  // rotating threads
+        constexpr int kIt = 32 * 32 / kRt;
         uint32_t w[kIt];
         __attribute__((address_space(3))) uint32_t* q[kIt];
 #pragma unroll
         for (int i = 0; i < kIt; ++i) {
-            const int r = (tid + 128 * NB * i) >> 5;
+            const int r = (rt + kRt * i) >> 5;
             const uint32_t addr = sb + (uint32_t)r * 128u + ((uint32_t)((kl >> 2) ^ ((r >> 1) & 7)) << 4) + rot_col;
             q[i] = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)addr;
-            w[i] = tid + 128 * NB * i < n_pairs ? *q[i] : 0u;
+            w[i] = rt + kRt * i < n_pairs ? *q[i] : 0u;
         }
 #pragma unroll
         for (int i = 0; i < kIt; ++i) {
-            const int r = (tid + 128 * NB * i) >> 5;
+            const int r = (rt + kRt * i) >> 5;
             const double tr = (double)(pos0 + row0 + r) * theta_rev;
             const float rev = (float)(tr - floor(tr));
             const float sn = __builtin_amdgcn_sinf(rev), cs = __builtin_amdgcn_cosf(rev);
@@ -240,7 +246,7 @@ __global__ __launch_bounds__(128 * NB) void rope_lsh_ring_kernel(const uint16_t*
         }
 #pragma unroll
         for (int i = 0; i < kIt; ++i)
-            if (tid + 128 * NB * i < n_pairs) *q[i] = w[i];
+            if (rt + kRt * i < n_pairs) *q[i] = w[i];
         if (++rot_chunk == nk) {  // the order wraps to chunk 0
             rot_chunk = 0;
             theta_rev = theta_rev0;
@@ -376,9 +382,9 @@ hipError_t launch_rope_lsh_encode(const void* x, const void* planes, uint64_t* c
     auto* cp = reinterpret_cast<uint32_t*>(codes);
     const double lb = log2(base);
     if (n_bits == 64)
-        hipLaunchKernelGGL(rope_lsh_ring_kernel<2>, grid, dim3(256), 0, s, xp, pp, cp, n_tok, dim, (int32_t)rows, pos0, lb);
+        hipLaunchKernelGGL(rope_lsh_ring_kernel<2>, grid, dim3(64 * kRotWaves * 2), 0, s, xp, pp, cp, n_tok, dim, (int32_t)rows, pos0, lb);
     else
-        hipLaunchKernelGGL(rope_lsh_ring_kernel<4>, grid, dim3(512), 0, s, xp, pp, cp, n_tok, dim, (int32_t)rows, pos0, lb);
+        hipLaunchKernelGGL(rope_lsh_ring_kernel<4>, grid, dim3(64 * kRotWaves * 4), 0, s, xp, pp, cp, n_tok, dim, (int32_t)rows, pos0, lb);
     return hipGetLastError();
 }
 
