@@ -264,8 +264,10 @@ def time_steps(torch, path, steps, warmup):
 def stage_times(torch, path, reps):
     """Per-call duration of every stage of a step.  A stage is timed as a run
     of its own calls with the inputs of a real step (one full step first),
-    between one HIP event pair on the launch stream: `reps` calls of a
-    once-per-step stage, `reps` passes over layers 1..L-1 of a per-layer one.
+    between one HIP event pair on the launch stream: 5 * reps (at least 10)
+    calls of a once-per-step stage (some take a few microseconds, so a short
+    run would mostly time the host), `reps` passes over layers 1..L-1 of a
+    per-layer one.
     No event sits between the calls of a run, so the figure is the kernels'
     time plus the launch gaps of back-to-back calls."""
     path.step()
@@ -274,16 +276,17 @@ def stage_times(torch, path, reps):
     once += [("gather_rest", path.s_gather_rest)] if path.gather_except else [("gather", path.s_gather)]
     once += [("qkv0", path.s_qkv0), ("attn0", path.s_attn0), ("select", path.s_select), ("xsel", path.s_xsel)]
     out = {}
+    n_once = max(10, 5 * reps)
     for name, fn in once:
         fn()
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0.record(stream)
-        for _ in range(reps):
+        for _ in range(n_once):
             fn()
         t1.record(stream)
         torch.cuda.synchronize()
-        out[name] = t0.elapsed_time(t1) / reps
+        out[name] = t0.elapsed_time(t1) / n_once
     for name, fn in (("qkv", path.s_qkv), ("attn", path.s_attn)):
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
