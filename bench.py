@@ -720,8 +720,8 @@ def dynamic_schedule_line(torch, np, ss, cfg, args):
            "recomputed_tokens_total": T + sum(n_rec), "kept_rows_first_layer": rec.n_kept0,
            "kept_rows_last_layer": rec.layers[-1].n_kept if rec.layers else rec.n_kept0,
            "kv_cache_rows_kept_frac": kept, "kv_cache_bytes_saved_frac": 1.0 - kept,
-           "timing": "wall clock over the steps (the schedule reads back per-layer counts, so the host waits "
-                     "for the device once per layer)"}
+           "timing": "wall clock over the steps (the schedule reads two counts back after the first layer, so the "
+                     "host waits for the device there once per step)"}
     print(json.dumps(out), flush=True)
 
 

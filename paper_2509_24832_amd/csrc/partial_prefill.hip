@@ -54,14 +54,18 @@ size_t qkv_workspace_dev_offset(int64_t n_sel, int32_t head_dim, int dtype) {
     return dtype == SEMSHARE_BF16 ? align256((size_t)n_sel * (head_dim / 2) * sizeof(float2)) : 0;
 }
 
-int32_t qkv_dev_parts(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype) {
+int32_t qkv_dev_parts(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype) {
     const int32_t cols = n_kv_heads * head_dim;
-    return dtype == SEMSHARE_BF16 ? cols / qkv_gemm_bn(n_q_heads, n_kv_heads, head_dim) : cols / 2;
+    return dtype == SEMSHARE_BF16 ? cols / qkv_gemm_bn(n_sel, n_q_heads, n_kv_heads, head_dim) : cols / 2;
 }
 
+// The deviation parts are sized for the narrowest tiles (128 columns) whatever
+// the call's tile width, so that the size grows with n_sel: a workspace sized
+// for n rows serves every call with fewer.
 size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype) {
-    return qkv_workspace_dev_offset(n_sel, head_dim, dtype) +
-           align256((size_t)n_sel * 2 * qkv_dev_parts(n_q_heads, n_kv_heads, head_dim, dtype) * sizeof(float));
+    const int32_t cols = n_kv_heads * head_dim;
+    const int32_t max_parts = dtype == SEMSHARE_BF16 ? (cols + 127) / 128 : cols / 2;
+    return qkv_workspace_dev_offset(n_sel, head_dim, dtype) + align256((size_t)n_sel * 2 * max_parts * sizeof(float));
 }
 
 hipError_t launch_rope_table(const int32_t* sel_pos, int64_t n_sel, int64_t n_tok, int32_t head_dim,
@@ -83,7 +87,7 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
                            ? reinterpret_cast<float*>(ws + qkv_workspace_dev_offset(a.n_sel, a.head_dim, SEMSHARE_BF16))
                            : nullptr;
     if (!a.rope_table) launch_rope_table(a.sel_pos, a.n_sel, a.n_tok, a.head_dim, a.rope_base, ws, s);
-    const int32_t bn = qkv_gemm_bn(a.n_q_heads, a.n_kv_heads, a.head_dim);
+    const int32_t bn = qkv_gemm_bn(a.n_sel, a.n_q_heads, a.n_kv_heads, a.head_dim);
     GemmArgs g{};
     g.x = static_cast<const uint16_t*>(a.x_sel);
     g.pos = a.sel_pos;
@@ -113,7 +117,7 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     if (a.deviation_out)
         hipLaunchKernelGGL(dev_final_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_parts,
                            a.deviation_out, a.n_sel,
-                           qkv_dev_parts(a.n_q_heads, a.n_kv_heads, a.head_dim, SEMSHARE_BF16));
+                           qkv_dev_parts(a.n_sel, a.n_q_heads, a.n_kv_heads, a.head_dim, SEMSHARE_BF16));
     return hipGetLastError();
 }
 

@@ -369,7 +369,7 @@ hipError_t launch_qkv_f32(const QkvArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(qkv_f32_kernel, grid, dim3(256), 0, s, q, cols);
     if (dev_parts)
         hipLaunchKernelGGL(dev_final_f32_kernel, dim3((unsigned)((a.n_sel + 255) / 256)), dim3(256), 0, s, dev_parts,
-                           a.deviation_out, a.n_sel, qkv_dev_parts(a.n_q_heads, a.n_kv_heads, a.head_dim, SEMSHARE_FP32));
+                           a.deviation_out, a.n_sel, qkv_dev_parts(a.n_sel, a.n_q_heads, a.n_kv_heads, a.head_dim, SEMSHARE_FP32));
     return hipGetLastError();
 }
 

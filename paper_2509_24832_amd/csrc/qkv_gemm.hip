@@ -340,9 +340,16 @@ __global__ __launch_bounds__(64 * NW, 1) void qkv_gemm_kernel(GemmArgs g) {
 
 }  // namespace
 
-int32_t qkv_gemm_bn(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim) {
+int32_t qkv_gemm_bn(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim) {
     const int32_t nq = n_q_heads * head_dim, nkv = n_kv_heads * head_dim;
-    return (nq % 256 == 0 && nkv % 256 == 0) ? 256 : 128;
+    if (nq % 256 != 0 || nkv % 256 != 0) return 128;
+    // 256-wide tiles, unless so few rows are selected that twice as many
+    // 128-wide tiles still fit one pass over the CUs: a tile's K loop takes
+    // about the same time whatever its row count, so with few row tiles the
+    // narrower ones finish the call in about half the time
+    const int64_t n_mt = (n_sel + 127) / 128;
+    const int64_t n_nt = (nq + 2 * (int64_t)nkv) / 256;
+    return 2 * n_mt * n_nt <= 256 ? 128 : 256;
 }
 
 hipError_t launch_qkv_gemm(const GemmArgs& g, int32_t bn, hipStream_t s) {

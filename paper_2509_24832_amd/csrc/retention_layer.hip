@@ -7,10 +7,12 @@
 // a lower row, every later one at a higher).
 //
 // One 1024-thread workgroup.  The kept set is a bitmask in LDS (one bit per
-// position, n_tok <= 2^20); every thread then owns a contiguous run of
-// words, counts its kept positions, and after a block-wide scan writes them
-// (and the reference row each one copies) in ascending order.  The rows of
-// the recomputed tokens are found by binary search in the written list.
+// position, n_tok <= 2^20), built one position per lane from coalesced reads
+// of the ranking (a wave's ballot gives two words at once); every thread then
+// owns a contiguous run of words, counts its kept positions, and after a
+// block-wide scan writes them (and the reference row each one copies) in
+// ascending order.  The row of a recomputed token is the number of kept
+// positions before it, counted in LDS from its word's owner's offset.
 #include "semshare_internal.h"
 
 namespace semshare {
@@ -50,16 +52,18 @@ __global__ __launch_bounds__(kT) void retention_layer_kernel(const int32_t* __re
                                                              int32_t* __restrict__ n_kept) {
     __shared__ uint32_t bits[kMaxWords];
     __shared__ uint32_t sw[kT / 64];
-    const int tid = threadIdx.x;
+    __shared__ uint32_t s_off[kT];  // each thread's first row in the kept list
+    const int tid = threadIdx.x, lane = tid & 63;
     const int32_t n_words = (n_tok + 31) / 32;
-    for (int32_t w = tid; w < n_words; w += kT) {
-        // the positions of word w ranked below n_retain
-        uint32_t m = 0;
-        for (int b = 0; b < 32; ++b) {
-            const int32_t p = 32 * w + b;
-            if (p < n_tok && rank[p] >= 0 && rank[p] < n_retain) m |= 1u << b;
-        }
-        bits[w] = m;
+    // the positions ranked below n_retain: a wave covers 64 consecutive
+    // positions, two words (the trip count is the same in every lane)
+    for (int32_t base = 0; base < 32 * n_words; base += kT) {
+        const int32_t p = base + tid;
+        const bool keep = p < n_tok && rank[p] >= 0 && rank[p] < n_retain;
+        const uint64_t m = __ballot(keep);
+        const int32_t w = (base + (tid & ~63)) >> 5;
+        if (lane == 0 && w < n_words) bits[w] = (uint32_t)m;
+        if (lane == 0 && w + 1 < n_words) bits[w + 1] = (uint32_t)(m >> 32);
     }
     __syncthreads();
     for (int32_t i = tid; i < n_sel; i += kT) {  // recomputed tokens are never evicted
@@ -68,12 +72,13 @@ __global__ __launch_bounds__(kT) void retention_layer_kernel(const int32_t* __re
     }
     __syncthreads();
     // thread t owns words [t * per, (t + 1) * per)
-    const int32_t per = (n_words + kT - 1) / kT;
+    const int32_t per = n_words > 0 ? (n_words + kT - 1) / kT : 1;
     const int32_t w0 = tid * per, w1 = min(w0 + per, n_words);
     uint32_t cnt = 0;
     for (int32_t w = w0; w < w1; ++w) cnt += __popc(bits[w]);
     uint32_t total;
     uint32_t o = block_excl_scan(cnt, &total, sw);
+    s_off[tid] = o;
     for (int32_t w = w0; w < w1; ++w) {
         uint32_t m = bits[w];
         while (m) {
@@ -86,17 +91,22 @@ __global__ __launch_bounds__(kT) void retention_layer_kernel(const int32_t* __re
         }
     }
     if (tid == 0) *n_kept = (int32_t)total;
-    __threadfence();
     __syncthreads();
-    // the row of every recomputed token in the compacted cache
+    // the row of every recomputed token in the compacted cache: the kept
+    // positions before it (its word's owner's first row, the owner's words
+    // before its word, the lower bits of its word)
     for (int32_t i = tid; i < n_sel; i += kT) {
         const int32_t p = sel_pos[i];
-        int32_t lo = 0, hi = (int32_t)total;
-        while (lo < hi) {
-            const int32_t mid = (lo + hi) >> 1;
-            if (kept_pos[mid] < p) lo = mid + 1; else hi = mid;
+        int32_t row = -1;
+        if (p >= 0 && p < n_tok) {
+            const int32_t w = p >> 5, b = p & 31;
+            const int32_t t = w / per;
+            uint32_t r = s_off[t];
+            for (int32_t v = t * per; v < w; ++v) r += __popc(bits[v]);
+            r += __popc(bits[w] & ((1u << b) - 1u));
+            if ((bits[w] >> b) & 1u) row = (int32_t)r;
         }
-        sel_rows[i] = (p >= 0 && p < n_tok && lo < (int32_t)total && kept_pos[lo] == p) ? lo : -1;
+        sel_rows[i] = row;
     }
 }
 

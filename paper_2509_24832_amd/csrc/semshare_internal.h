@@ -224,7 +224,7 @@ struct AttnPlan {
 
 size_t qkv_workspace_bytes(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);
 size_t qkv_workspace_dev_offset(int64_t n_sel, int32_t head_dim, int dtype);
-int32_t qkv_dev_parts(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);
+int32_t qkv_dev_parts(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype);
 
 // The bf16 projection GEMM (qkv_gemm.hip).
 struct GemmArgs {
@@ -244,7 +244,7 @@ struct GemmArgs {
     const int32_t* dev_idx;      // position p -> row dev_idx[p] of dev_src (outside [0, dev_n): a zero row)
     int64_t dev_n;
 };
-int32_t qkv_gemm_bn(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim);
+int32_t qkv_gemm_bn(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim);
 hipError_t launch_qkv_gemm(const GemmArgs& g, int32_t bn, hipStream_t s);
 AttnPlan plan_attention(int64_t n_sel, int64_t n_tok, int32_t n_q_heads, int32_t n_kv_heads,
                         int32_t head_dim, int dtype);

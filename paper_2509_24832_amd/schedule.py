@@ -1,8 +1,11 @@
 """The layer schedule of one target prompt with the dynamic recompute set and
 retention (Sections 4.2, 4.3.3 and 4.3.4; Appendix A.5 and A.6), as a
 sequence of libsemshare calls.  Host-side sequencing only: every step runs in
-the library's kernels; the host reads back the few counts that size later
-calls (AR, the number recomputed, the number kept per layer).
+the library's kernels.  The host reads back two counts once per prompt, after
+the first layer (AR with the number recomputed, and the number kept on
+layer 0); later layers' sizes follow from them on the host (the recompute
+counts exactly, the kept counts as a bound, see below), so the layers are
+launched without waiting for the device.
 
 Layer indices here start at 0 (the paper's first layer is layer 0):
 
@@ -154,9 +157,17 @@ class DynamicSchedule:
                 n_l = max(1, min(n_prev, int(math.floor(n_prev * self.alpha_recomp[l] + 0.5))))
                 ss.select_recompute_nested(self.sig[(l - 1) % 2][:n_prev], prev[:n_prev], n_l, out=cur[:n_l])
             retain *= self.alpha_retain[l]
+            n_ret = int(math.floor(retain + 0.5))
             s_l = cur[:n_l]
-            kept, src, rows, nk_t = ss.retention_layer(rank, int(math.floor(retain + 0.5)), s_l, self.idx)
-            nk = self._n(nk_t)
+            kept, src, rows, nk_t = ss.retention_layer(rank, n_ret, s_l, self.idx)
+            # The layer keeps at most n_ret + n_l rows (the retained ones and its
+            # recomputed ones): its cache, gather, projection and attention are
+            # sized by that bound instead of the count on the device.  Rows past
+            # the kept ones are gathered too (copies of reference rows, or zeros
+            # for indices out of range: finite either way) and never attended,
+            # since every recomputed row's causal range ends at its own row,
+            # which is a kept one.
+            nk = min(T, n_ret + n_l)
             kc, vc = self.asm_k[l][:nk], self.asm_v[l][:nk]
             ss.gather_kv(ref_k[l][None], ref_v[l][None], src[:nk], out_k=kc[None], out_v=vc[None])
             x = ss.gather_rows(e_tgt, s_l, out=self.x_sel[:n_l])
@@ -169,6 +180,8 @@ class DynamicSchedule:
             out = ss.prefill_attention(q, rows, kc, vc, hkv, workspace=self.ws, plan=plan)
             m("layer")
             if record:
-                rec.layers.append(LayerRecord(clone(s_l), clone(kept[:nk]), clone(rows), nk, clone(sig), out))
+                n_kept = self._n(nk_t)
+                assert n_kept <= nk, "kept rows beyond their bound"
+                rec.layers.append(LayerRecord(clone(s_l), clone(kept[:n_kept]), clone(rows), n_kept, clone(sig), out))
             n_prev = n_l
         return rec
