@@ -167,7 +167,8 @@ semshare_status_t semshare_gather_kv_except(const void* ref_k, const void* ref_v
  *     ||V_cache[p] - v||_2 over the row's n_kv_heads*head_dim entries, against
  *     the row held before step 3 (KV deviation, Appendix A.4), with k and v
  *     as rounded to dtype.  The sums are formed in a fixed order, so the
- *     result is reproducible bit for bit.
+ *     result is reproducible bit for bit (the order depends on n_sel and
+ *     the head shape, which set the projection's tile width).
  *  3. Cache rows sel_pos[i] are overwritten with k (post-RoPE) and v.
  *  4. If out != NULL: for every selected row and query head h,
  *     out = softmax_{j <= p}(q_h . K[j][h/G] * sm_scale) V[j][h/G] over the
