@@ -181,6 +181,28 @@ def test_partial_prefill_workspace_sizes(lib):
     assert W(1280, 5120, 4096, 32, 8, 128, 1) > W(1280, 5120, 4096, 32, 8, 128, 1) - 1
 
 
+def test_workspaces_grow_with_the_row_count(lib):
+    """A workspace sized for n selected rows serves every call with fewer: the
+    projection's deviation parts follow its tile width, which narrows when few
+    rows are selected (here across 640 / 641 rows at 32 q / 8 kv heads), so its
+    workspace reserves the narrow tiles' count; the attention mass workspace
+    grows with the token count."""
+    L = lib
+    for heads in ((32, 8), (64, 8), (8, 8), (32, 4)):
+        prev = 0
+        for n in list(range(0, 2200, 1)) + [5120, 32768]:
+            w = L.semshare_qkv_rope_workspace(n, heads[0], heads[1], 128, 1)
+            assert w >= prev, (heads, n)
+            prev = w
+            wp = L.semshare_partial_prefill_workspace(n, 5120, 4096, heads[0], heads[1], 128, 1)
+            assert wp >= w, (heads, n)
+    prev = 0
+    for t in (1, 33, 1000, 5120, 8192):
+        w = L.semshare_attention_mass_workspace(t, 32)
+        assert w >= prev and w >= 2 * 32 * t * 4
+        prev = w
+
+
 def test_select_validation(lib):
     assert _st("semshare_select_recompute", FAKE, 10, 11, FAKE, None) == b.E_INVAL
     assert _st("semshare_select_recompute", FAKE, (1 << 20) + 1, 5, FAKE, None) == b.E_UNSUPPORTED
