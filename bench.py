@@ -51,6 +51,11 @@ def parse():
                     help="except: the first layer's deviation reads the matched reference rows directly and the "
                          "layers after it are gathered after the selection, without the recomputed rows; all: "
                          "every layer and row gathered before the first layer")
+    ap.add_argument("--gather-stream", choices=("serial", "overlap"), default="serial",
+                    help="with --gather except: serial: one gather call for layers 1..L-1 before layer 1; overlap: "
+                         "each later layer's gather runs on a second stream (default priority) and that layer's "
+                         "attention waits for it (the same results; measured slower: the copies slow the compute "
+                         "kernels they share the CUs and HBM with by more than they hide)")
     ap.add_argument("--matcher", choices=("mfma", "xor"), default="mfma",
                     help="top-1 Hamming matcher of the hot path: int8 MFMA or XOR/popcount (bit-identical outputs)")
     ap.add_argument("--vendor-compare", action="store_true",
@@ -105,6 +110,9 @@ class Path:
         self.matcher = ss.match_mfma
         self.fused_encode = True
         self.gather_except = True
+        self.gather_overlap = False
+        self.side = torch.cuda.Stream()  # default priority
+        self.gather_done = [torch.cuda.Event() for _ in range(cfg.n_layers)]
         dev = "cuda"
         bf = torch.bfloat16
         T, d, L = cfg.n_tok, cfg.dim, cfg.n_layers
@@ -215,6 +223,19 @@ class Path:
             self.ss.gather_kv(self.ref_k[1:], self.ref_v[1:], self.idx, out_k=self.asm_k[1:], out_v=self.asm_v[1:],
                               except_pos=self.sel)
 
+    def s_gather_layers_async(self):
+        """The except-gather of layers 1..L-1 as one call per layer on the side
+        stream, after the selection; layer l's attention waits for its event.
+        A projection only writes its layer's selected rows, which the gather
+        leaves alone, so it need not wait."""
+        torch = self.torch
+        self.side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(self.side):
+            for l in range(1, self.L):
+                self.ss.gather_kv(self.ref_k[l:l + 1], self.ref_v[l:l + 1], self.idx, out_k=self.asm_k[l:l + 1],
+                                  out_v=self.asm_v[l:l + 1], except_pos=self.sel)
+                self.gather_done[l].record(self.side)
+
     def s_xsel(self):
         self.ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
 
@@ -235,10 +256,17 @@ class Path:
         self.s_qkv0()
         self.s_attn0()
         self.s_select()
-        self.s_gather_rest()
+        overlap = self.gather_except and self.gather_overlap
+        if overlap:
+            self.s_gather_layers_async()
+        else:
+            self.s_gather_rest()
         self.s_xsel()
+        main = self.torch.cuda.current_stream()
         for l in range(1, self.L):
             self.s_qkv(l)
+            if overlap:
+                main.wait_event(self.gather_done[l])  # the last one also covers every earlier gather
             self.s_attn(l)
 
 
@@ -767,6 +795,7 @@ def main():
     path.matcher = ss.match_mfma if args.matcher == "mfma" else ss.match
     path.fused_encode = args.encode == "fused"
     path.gather_except = args.gather == "except"
+    path.gather_overlap = args.gather_stream == "overlap"
 
     if args.copy_calibration_mib:
         # fill the source, then a 1 GiB buffer that pushes it out of L2 and the
@@ -830,7 +859,8 @@ def main():
         "config": {"workload": f"5120-token target vs 5120-token cached reference, 32 Llama-3-8B-shaped attention "
                                f"layers (hidden 4096, 32q/8kv heads, head_dim 128), 128-bit LSH, recompute "
                                f"fraction {args.frac}", "n_tok": T, "layers": L, "recompute_frac": args.frac,
-                   "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode, "gather": args.gather},
+                   "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode, "gather": args.gather,
+                   "gather_stream": args.gather_stream if args.gather == "except" else None},
         "partial_prefill_tokens_per_s": T / (pp_ms * 1e-3),
         "match_token_pairs_per_s": T * T / (match_ms * 1e-3),
         "stage_ms": {k: round(v, 4) for k, v in stages.items()},
