@@ -13,7 +13,7 @@ The reference side (its RoPE/LSH codes and its own K/V cache) is prepared
 once before timing, as at cache-insert time.  Inputs are seeded synthetic
 data resident in HBM before the timed region starts.
 
-    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--frac 0.25]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 20] [--frac 0.25]
 
 Prints one JSON line (see the keys below).
 """
@@ -38,8 +38,8 @@ FP32_PEAK_TFLOPS = 157.3        # MI355X fp32 vector (and fp32 matrix)
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--frac", type=float, default=0.25, help="recompute fraction of the headline line")
     ap.add_argument("--sweep", default="0.10,0.25,0.50,1.00",
                     help="recompute fractions also timed ('' to skip); 1.00 is the full-prefill analogue")
