@@ -142,6 +142,8 @@ hipError_t launch_gather_rows(const void* src_a, const void* src_b, const int32_
                               n_except);
     else if (row_bytes >= 8192)  // wide rows: one row per wave, 8 KB of it per pass
         launch_shape<1, 1, 8>(src_a, src_b, idx, n_tgt, n_ref, dst_a, dst_b, n_layers, row_bytes, s, nullptr, 0);
+    else if ((n_tgt + 7) / 8 * n_layers * (src_b ? 2 : 1) < 2048)  // few rows: 2 per wave, so all CUs get some
+        launch_shape<2, 1, 2>(src_a, src_b, idx, n_tgt, n_ref, dst_a, dst_b, n_layers, row_bytes, s, nullptr, 0);
     else
         launch_shape<8, 1, 2>(src_a, src_b, idx, n_tgt, n_ref, dst_a, dst_b, n_layers, row_bytes, s, nullptr, 0);
     return hipGetLastError();
