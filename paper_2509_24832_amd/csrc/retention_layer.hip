@@ -8,11 +8,11 @@
 //
 // One 1024-thread workgroup.  The kept set is a bitmask in LDS (one bit per
 // position, n_tok <= 2^20), built one position per lane from coalesced reads
-// of the ranking (a wave's ballot gives two words at once); every thread then
-// owns a contiguous run of words, counts its kept positions, and after a
-// block-wide scan writes them (and the reference row each one copies) in
-// ascending order.  The row of a recomputed token is the number of kept
-// positions before it, counted in LDS from its word's owner's offset.
+// of the ranking (a wave's ballot gives two words at once); then, one block
+// of 1024 positions at a time, a block-wide scan of the kept flags places
+// every kept position (and the reference row it copies) in ascending order.
+// The row of a recomputed token is the number of kept positions before it,
+// counted in LDS from its block's first row.
 #include "semshare_internal.h"
 
 namespace semshare {
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kT) void retention_layer_kernel(const int32_t* __re
                                                              int32_t* __restrict__ n_kept) {
     __shared__ uint32_t bits[kMaxWords];
     __shared__ uint32_t sw[kT / 64];
-    __shared__ uint32_t s_off[kT];  // each thread's first row in the kept list
+    __shared__ uint32_t s_blk[kMaxRetainTok / kT];  // each block of kT positions' first row in the kept list
     const int tid = threadIdx.x, lane = tid & 63;
     const int32_t n_words = (n_tok + 31) / 32;
     // the positions ranked below n_retain: a wave covers 64 consecutive
@@ -71,38 +71,35 @@ __global__ __launch_bounds__(kT) void retention_layer_kernel(const int32_t* __re
         if (p >= 0 && p < n_tok) atomicOr(&bits[p >> 5], 1u << (p & 31));
     }
     __syncthreads();
-    // thread t owns words [t * per, (t + 1) * per)
-    const int32_t per = n_words > 0 ? (n_words + kT - 1) / kT : 1;
-    const int32_t w0 = tid * per, w1 = min(w0 + per, n_words);
-    uint32_t cnt = 0;
-    for (int32_t w = w0; w < w1; ++w) cnt += __popc(bits[w]);
-    uint32_t total;
-    uint32_t o = block_excl_scan(cnt, &total, sw);
-    s_off[tid] = o;
-    for (int32_t w = w0; w < w1; ++w) {
-        uint32_t m = bits[w];
-        while (m) {
-            const int b = __ffs(m) - 1;
-            m &= m - 1;
-            const int32_t p = 32 * w + b;
+    // the kept positions in ascending order: each block of kT positions is
+    // compacted in parallel (one position per thread, a block-wide scan of
+    // the kept flags), with coalesced reads of the match index; s_blk holds
+    // each block's first row for the rows of the recomputed tokens below
+    uint32_t base_out = 0;
+    for (int32_t base = 0; base < 32 * n_words; base += kT) {  // the same trip count in every thread
+        const int32_t p = base + tid;
+        const uint32_t keep = p < n_tok ? (bits[p >> 5] >> (p & 31)) & 1u : 0u;
+        uint32_t total;
+        const uint32_t o = base_out + block_excl_scan(keep, &total, sw);
+        if (tid == 0) s_blk[base / kT] = base_out;
+        if (keep) {
             kept_pos[o] = p;
             if (src_idx) src_idx[o] = idx[p];
-            ++o;
         }
+        base_out += total;
     }
-    if (tid == 0) *n_kept = (int32_t)total;
+    if (tid == 0) *n_kept = (int32_t)base_out;
     __syncthreads();
     // the row of every recomputed token in the compacted cache: the kept
-    // positions before it (its word's owner's first row, the owner's words
-    // before its word, the lower bits of its word)
+    // positions before it (its block's first row, the block's words before
+    // its word, the lower bits of its word)
     for (int32_t i = tid; i < n_sel; i += kT) {
         const int32_t p = sel_pos[i];
         int32_t row = -1;
         if (p >= 0 && p < n_tok) {
-            const int32_t w = p >> 5, b = p & 31;
-            const int32_t t = w / per;
-            uint32_t r = s_off[t];
-            for (int32_t v = t * per; v < w; ++v) r += __popc(bits[v]);
+            const int32_t w = p >> 5, b = p & 31, blk = p / kT;
+            uint32_t r = s_blk[blk];
+            for (int32_t v = blk * (kT / 32); v < w; ++v) r += __popc(bits[v]);
             r += __popc(bits[w] & ((1u << b) - 1u));
             if ((bits[w] >> b) & 1u) row = (int32_t)r;
         }
