@@ -40,9 +40,13 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--frac", type=float, default=0.25, help="recompute fraction of the headline line")
-    ap.add_argument("--sweep", default="0.10,0.25,0.50,1.00",
-                    help="recompute fractions also timed ('' to skip); 1.00 is the full-prefill analogue")
+    ap.add_argument("--config", type=int, choices=(2, 4), default=2,
+                    help="2: 5120-token prompts (the headline); 4: 32768-token prompts (long context)")
+    ap.add_argument("--frac", type=float, default=None,
+                    help="recompute fraction of the headline line (default 0.25 at config 2, 0.10 at config 4)")
+    ap.add_argument("--sweep", default=None,
+                    help="recompute fractions also timed ('' to skip; default 0.10,0.25,0.50,1.00 at config 2, "
+                         "none at config 4); 1.00 is the full-prefill analogue")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0, help="approximate oracle time of the CPU sample")
     ap.add_argument("--encode", choices=("fused", "two-pass"), default="fused",
@@ -790,7 +794,11 @@ def main():
     if args.schedule == "dynamic":
         dynamic_schedule_line(torch, np, ss, CONFIGS[2], args)
         return
-    cfg = CONFIGS[2]
+    cfg = CONFIGS[args.config]
+    if args.frac is None:
+        args.frac = 0.25 if cfg.cid == 2 else cfg.recompute_fracs[0]
+    if args.sweep is None:
+        args.sweep = "0.10,0.25,0.50,1.00" if cfg.cid == 2 else ""
     path = Path(torch, ss, cfg)
     path.matcher = ss.match_mfma if args.matcher == "mfma" else ss.match
     path.fused_encode = args.encode == "fused"
@@ -840,11 +848,12 @@ def main():
     traffic = None
     if ATTN_TRAFFIC["source_sha256"] and \
             source_sha256("paper_2509_24832_amd/csrc/attention.hip") == ATTN_TRAFFIC["source_sha256"] and \
-            abs(args.frac - 0.25) < 1e-9:
+            abs(args.frac - 0.25) < 1e-9 and cfg.cid == 2:
         traffic = ATTN_TRAFFIC["bytes_per_call"]
     achieved = attn_call_flops / (attn_call_ms * 1e-3) / 1e12
     res = {
-        "metric": "partial-prefill tokens/s + LSH match token-pairs/s at 5k tokens, Llama-3-8B shape",
+        "metric": "partial-prefill tokens/s + LSH match token-pairs/s at "
+                  f"{'5k' if cfg.cid == 2 else '32k'} tokens, Llama-3-8B shape",
         "value": T / (ms * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -856,7 +865,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"5120-token target vs 5120-token cached reference, 32 Llama-3-8B-shaped attention "
+        "config": {"workload": f"{T}-token target vs {T}-token cached reference, 32 Llama-3-8B-shaped attention "
                                f"layers (hidden 4096, 32q/8kv heads, head_dim 128), 128-bit LSH, recompute "
                                f"fraction {args.frac}", "n_tok": T, "layers": L, "recompute_frac": args.frac,
                    "n_recompute": n_sel, "matcher": args.matcher, "encode": args.encode, "gather": args.gather,
