@@ -650,7 +650,8 @@ def vendor_compare_line(torch, np, ss, cfg, args):
     qkv_torch = timed(lambda: torch.matmul(x, wcat.t(), out=y))
     v_diff = (y[:, (hq + hkv) * D:].float().view(n_sel, hkv, D) - vc[sel.long()].float()).abs().max().item()
     qfl = 2.0 * n_sel * (hq + 2 * hkv) * D * d
-    out_line = {"metric": "vendor_compare_us", "unit": "us", "n_gpus": 1, "steps": reps, "warmup": args.warmup,
+    out_line = {"metric": "vendor_compare_us", "value": attn_ours, "unit": "us", "n_gpus": 1, "steps": reps,
+                "warmup": args.warmup,
                 "higher_is_better": False, "data": "synthetic", "dtype": "bf16",
                 "config": {"workload": f"first-layer causal attention over {T} tokens (32 q / 8 kv heads, head_dim "
                                        f"128) and the projection of {n_sel} selected rows (hidden 4096 -> 6144)"},
