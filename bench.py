@@ -93,8 +93,8 @@ def parse():
 # step averaged), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs of this bench
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
-ATTN_TRAFFIC = {"source_sha256": "796989eb5edfb09a50a9a203abafbe24ffdcd40a9ef58be6b821814250c78818",
-                "bytes_per_call": 93604751}
+ATTN_TRAFFIC = {"source_sha256": "655f0832f7023c3c55e80f8258eaed498f72414721d2e5fbce93bf4983d10604",
+                "bytes_per_call": 94617507}
 
 
 def source_sha256(rel):
