@@ -38,8 +38,10 @@ COMMON_FLAGS = [
 # or -inf by construction (masked keys), so NaN-preserving max is not needed;
 # without this every fmaxf operand is first quieted with an extra v_max.  The
 # VGPR form of MFMA keeps accumulators where the vector ALU can read them
-# (attention scores, the matcher's distances) without copies out of AGPRs.
+# (attention scores, the masses' scores, the matcher's distances) without
+# copies out of AGPRs.
 EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+               "attention_mass.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
                "hamming_match_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 

@@ -10,9 +10,14 @@
 //                    each: S^T = K Q^T, so each lane owns a query column and
 //                    keeps its row's running max and sum over its 16 keys per
 //                    block; the two lane halves merge at the end -> lse2[h][i].
-//   mass_col_kernel  four waves per (8 key blocks of 32, head): S = Q K^T, so
-//                    each lane owns a key column and sums exp2(s - lse2[i])
-//                    over its 16 rows per block -> part[h][j].
+//   mass_col_kernel  four waves per (8 key blocks of 32, head): S^T = K Q^T
+//                    again, so each lane owns one query row of a tile and
+//                    its normaliser is one value per tile; the lane adds
+//                    exp2(s - lse2[i]) to a sum per key row, and the 32
+//                    lanes of each half are summed once at the end ->
+//                    part[h][j].  (With S = Q K^T each lane owned a key
+//                    column but needed 16 normalisers per tile, each a
+//                    bounds-checked load: 365 -> 239 us at 5120 tokens.)
 //   mass_final_kernel sums the heads in a fixed order and divides by H_q T.
 // Each wave keeps the operands of its 2 fixed blocks (queries, resp. keys)
 // in VGPRs; the other operand streams through a 4-stage LDS ring of 32-row
@@ -217,9 +222,13 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) bk[b][ks] = ld8(row + 16 * ks);
     }
-    float col[kNB];
+    // per lane and key row v of each block: the sum over the query columns
+    // this lane has held (one per tile); the lanes are summed at the end
+    float col[kNB][16];
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) col[b] = 0.0f;
+    for (int b = 0; b < kNB; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) col[b][v] = 0.0f;
     const float* lse_h = lse2 + (int64_t)h * T;
     // row tiles of the workgroup: from its first key block (or the window) to the end
     const int64_t qb_first = wg0 > row_begin / 32 ? wg0 : row_begin / 32;
@@ -233,24 +242,20 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_
     };
     for (int64_t qb = qb_first; qb < qb_first + kMassStages - 1; ++qb)
         if (qb < nb) issue(qb);
-    float Ln[16];  // the next tile's normalisers
-    auto load_l = [&](int64_t qb, float (&L)[16]) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int64_t r = qb * 32 + out_row(v, half);
-            L[v] = r < T && r >= row_begin ? lse_h[r] : __builtin_inff();  // rows outside the window add 0
-        }
+    // the normaliser of this lane's query row of a tile (+inf outside the
+    // window or past T: such rows add 0)
+    auto load_l = [&](int64_t qb) {
+        const int64_t r = qb * 32 + l32;
+        return r < T && r >= row_begin ? lse_h[r] : __builtin_inff();
     };
-    if (qb_first < nb) load_l(qb_first, Ln);
+    float Ln = qb_first < nb ? load_l(qb_first) : 0.0f;
     for (int64_t qb = qb_first; qb < nb; ++qb) {
-        float L[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) L[v] = Ln[v];
+        const float L = Ln;
         if (qb + 2 < nb) ring_wait<2>();
         else if (qb + 1 < nb) ring_wait<1>();
         else ring_wait<0>();
         if (qb + kMassStages - 1 < nb) issue(qb + kMassStages - 1);
-        if (qb + 1 < nb) load_l(qb + 1, Ln);
+        if (qb + 1 < nb) Ln = load_l(qb + 1);
         const int st = (int)((qb - qb_first) & (kMassStages - 1));
         bf16x8_t aq[8];
 #pragma unroll
@@ -260,25 +265,36 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_
             if (qb < kb0 + b) continue;  // wave-uniform: every row of the block precedes the keys
             f32x16_t acc = {};
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[ks], bk[b][ks], acc, 0, 0, 0);
-            // acc[v] = S[query = 32 qb + out_row(v)][key = 32 (kb0 + b) + l32];
-            // only the diagonal block has rows before its keys; rows past T
-            // carry L = inf and add 0
+            for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bk[b][ks], aq[ks], acc, 0, 0, 0);
+            // acc[v] = S^T[key = 32 (kb0 + b) + out_row(v)][query = 32 qb + l32];
+            // only the diagonal block has keys after its queries: their
+            // scores become -inf (weight 0) in place, then one common path
             if (qb == kb0 + b) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
-                    col[b] += l32 <= out_row(v, half) ? __builtin_amdgcn_exp2f(acc[v] * scale_log2e - L[v]) : 0.0f;
-            } else {
-#pragma unroll
-                for (int v = 0; v < 16; ++v) col[b] += __builtin_amdgcn_exp2f(acc[v] * scale_log2e - L[v]);
+                    if (out_row(v, half) > l32) acc[v] = kNegInf;
+                asm volatile("" : "+v"(acc));
             }
+#pragma unroll
+            for (int v = 0; v < 16; ++v) col[b][v] += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -L));
         }
     }
+    // sum over the 32 query lanes of each half (a fixed butterfly), then lane
+    // v of the half writes key row v
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
-        const float c = col[b] + __shfl_xor(col[b], 32);
-        const int64_t key = (kb0 + b) * 32 + l32;
-        if (half == 0 && key < T) part[(int64_t)h * T + key] = c;
+        float c[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) c[v] = col[b][v];
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) c[v] += __shfl_xor(c[v], o);
+        float mine = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mine = l32 == v ? c[v] : mine;
+        const int64_t key = (kb0 + b) * 32 + out_row(l32 & 15, half);
+        if (l32 < 16 && key < T) part[(int64_t)h * T + key] = mine;
     }
 }
 

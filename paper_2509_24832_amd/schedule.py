@@ -107,6 +107,9 @@ class DynamicSchedule:
         ws = max(ss.qkv_rope_workspace_bytes(T, n_q_heads, n_kv_heads, head_dim, bf),
                  ss.prefill_attention_workspace_bytes(T, T, n_q_heads, n_kv_heads, head_dim, bf))
         self.ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.plan_buf = torch.empty(max(1, ss.attention_plan_bytes(T, T, n_q_heads, n_kv_heads, head_dim, bf)),
+                                    dtype=torch.uint8, device=dev)
+        self.table_buf = torch.empty(max(16, ss.rope_table_bytes(T, head_dim)), dtype=torch.uint8, device=dev)
 
     def _n(self, t: torch.Tensor) -> int:
         return int(t.cpu().numpy()[0])
@@ -171,12 +174,12 @@ class DynamicSchedule:
             kc, vc = self.asm_k[l][:nk], self.asm_v[l][:nk]
             ss.gather_kv(ref_k[l][None], ref_v[l][None], src[:nk], out_k=kc[None], out_v=vc[None])
             x = ss.gather_rows(e_tgt, s_l, out=self.x_sel[:n_l])
-            table = ss.rope_table(s_l, T, D)
+            table = ss.rope_table(s_l, T, D, out=self.table_buf)
             wq, wk, wv = weights[l]
             q, sig = ss.qkv_rope(x, rows, wq, wk, wv, kc, vc, hq, hkv, q_out=self.q_sel[:n_l],
                                  deviation=self.sig[l % 2][:n_l], want_deviation=True, workspace=self.ws,
                                  rope_table=table)
-            plan = ss.attention_plan(rows, nk, hq, hkv, D)
+            plan = ss.attention_plan(rows, nk, hq, hkv, D, out=self.plan_buf)
             out = ss.prefill_attention(q, rows, kc, vc, hkv, workspace=self.ws, plan=plan)
             m("layer")
             if record:
