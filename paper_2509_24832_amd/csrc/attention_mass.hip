@@ -5,29 +5,37 @@
 // Mass of token j at a fully computed layer: the causal softmax attention
 // P_h[i][j] of every head h, averaged over the heads and over the query rows
 // i (rows before j contribute zero).  Two MFMA passes over the causal score
-// matrix, bf16 operands and fp32 accumulation, exponentials in base 2:
+// matrix, bf16 operands and fp32 accumulation, exponentials in base 2, both
+// computing S^T = K Q^T so that each lane owns one query row:
 //   mass_lse_kernel  four waves per (8 query blocks of 32, head), two blocks
-//                    each: S^T = K Q^T, so each lane owns a query column and
-//                    keeps its row's running max and sum over its 16 keys per
-//                    block; the two lane halves merge at the end -> lse2[h][i].
-//   mass_col_kernel  four waves per (8 key blocks of 32, head): S^T = K Q^T
-//                    again, so each lane owns one query row of a tile and
-//                    its normaliser is one value per tile; the lane adds
-//                    exp2(s - lse2[i]) to a sum per key row, and the 32
-//                    lanes of each half are summed once at the end ->
-//                    part[h][j].  (With S = Q K^T each lane owned a key
-//                    column but needed 16 normalisers per tile, each a
-//                    bounds-checked load: 365 -> 239 us at 5120 tokens.)
+//                    each, the key tiles streamed: each lane keeps its row's
+//                    running reference and sum over its 16 keys per block;
+//                    the two lane halves merge at the end -> lse2[h][i].
+//   mass_col_kernel  four waves per (8 key blocks of 32, head), two blocks
+//                    each, the query tiles streamed with their normalisers:
+//                    each lane adds exp2(s - lse2[i]) of its row to a sum per
+//                    key row, and the 32 lanes of each half are summed once
+//                    at the end -> part[h][j].
 //   mass_final_kernel sums the heads in a fixed order and divides by H_q T.
-// Each wave keeps the operands of its 2 fixed blocks (queries, resp. keys)
-// in VGPRs; the other operand streams through a 4-stage LDS ring of 32-row
-// tiles filled by direct-to-LDS loads and shared by the workgroup's 4 waves,
-// one 32 x 128 tile feeding 2 x 8 MFMAs per wave (with one wave per
-// workgroup streaming its own tiles from L2, 790 instead of 652 us at 5120
-// tokens, bit-identical).  The normaliser pass takes no per-tile maximum: each
-// lane exponentiates against a reference it saw earlier and falls back to the
-// tile's maximum only while it has none or when the tile's sum exceeds 2^64
-// (652 -> 612 us; fp32 sums keep their relative precision above 1).
+// Each wave keeps the operands of its 2 fixed blocks in VGPRs; the other
+// operand streams through a 4-stage LDS ring of 32-row tiles filled by
+// direct-to-LDS loads and shared by the workgroup's 4 waves (with one wave
+// per workgroup streaming its own tiles from L2, 790 instead of 652 us at
+// 5120 tokens, bit-identical).  Where no key of a tile lies past a query
+// row, a wave's two blocks are software-pipelined: the MFMAs of one block
+// run while the exponentials of the other block's scores (of the same or the
+// previous tile) are formed, each MFMA followed by two of them; the (at
+// most two) tiles on the diagonal go block by block with their masks.  The
+// normaliser pass takes no per-tile maximum: each lane exponentiates against
+// a reference it saw earlier and falls back to the tile's maximum only
+// while it has none or when the tile's sum exceeds 2^64 (fp32 sums keep
+// their relative precision above 1).  At 5120 tokens, 32 / 8 heads: the
+// normaliser pass 203 us, the column pass 190 us (365 us with S = Q K^T, a
+// key column per lane and 16 bounds-checked normaliser loads per tile; 239
+// us transposed; 190 us pipelined, with the normalisers brought in through
+// the ring and the fixed operands waited for before the ring starts: the
+// compiler had placed memory waits inside the loop that also covered the
+// ring's loads).  Pipelining the normaliser pass moved it from 208 us only.
 //
 // dyn_select_kernel (one workgroup): tokens sorted by mass (descending, lower
 // position first on ties); AR is the smallest count whose prefix reaches
@@ -96,11 +104,26 @@ struct MassRing {
     }
 };
 
-// wait until at most N of this wave's tiles are in flight, then meet the other waves
-template <int N>
+// wait until at most N of this wave's tiles are in flight (kPer direct loads
+// each), then meet the other waves
+template <int N, int kPer = kMassLoads>
 __device__ __forceinline__ void ring_wait() {
-    wait_vmcnt<N * kMassLoads>();
+    wait_vmcnt<N * kPer>();
     ring_barrier();
+}
+
+// 4 bytes per lane from gbase + off straight into LDS at lds_base + 4 * lane
+// (global_load_lds_dword; the direct-load counterpart of g2lds for one float
+// per lane)
+__device__ __forceinline__ void g2lds_b32(const void* gbase, uint32_t off, uint32_t lds_base) {
+    const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+    const uint32_t g_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t g_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    const uint64_t gs = ((uint64_t)g_hi << 32) | (uint64_t)g_lo;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+                 :
+                 : "v"(off), "s"(reinterpret_cast<const void*>(gs)), "s"((uint32_t)__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory", "m0");
 }
 
 __global__ __launch_bounds__(64 * kMassWaves) void mass_lse_kernel(const uint16_t* __restrict__ q,
@@ -124,6 +147,7 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_lse_kernel(const uint16_
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) bq[b][ks] = ld8(row + 16 * ks);
     }
+    wait_vmcnt<0>();  // the fixed operands are in before the ring's loads start
     float m[kNB], l[kNB];
 #pragma unroll
     for (int b = 0; b < kNB; ++b) { m[b] = kNegInf; l[b] = 0.0f; }
@@ -136,57 +160,120 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_lse_kernel(const uint16_
     auto issue = [&](int64_t kb) {
         ring.issue(kbase + kb * 32 * (int64_t)Hkv * 128, T - kb * 32, kstride, (int)(kb & (kMassStages - 1)));
     };
-    for (int64_t kb = 0; kb < kMassStages - 1; ++kb)
-        if (kb < kb_end) issue(kb);
-    for (int64_t kb = 0; kb < kb_end; ++kb) {
-        // tile kb has landed: in flight after it are at most tiles kb + 1, kb + 2
+    // tile kb has landed for every wave (and every wave is done with tile
+    // kb - 1, whose stage then takes tile kb + 3)
+    auto open_tile = [&](int64_t kb) {
         if (kb + 2 < kb_end) ring_wait<2>();
         else if (kb + 1 < kb_end) ring_wait<1>();
         else ring_wait<0>();
-        // every wave is past tile kb - 1: its stage takes tile kb + 3
         if (kb + kMassStages - 1 < kb_end) issue(kb + kMassStages - 1);
+    };
+    bf16x8_t ak[8];
+    auto read_tile = [&](int64_t kb) {
         const int st = (int)(kb & (kMassStages - 1));
-        bf16x8_t ak[8];
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) ak[ks] = ring.frag(st, l32, half, ks);
+    };
+    auto s_tile = [&](int b) {
+        f32x16_t acc = {};
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], acc, 0, 0, 0);
+        return acc;  // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32]
+    };
+    // Exponentials against the lane's reference m (a maximum seen earlier,
+    // scaled): the sum of a tile's 16 is accepted when m is set and the sum
+    // shows no value far above it; otherwise (no reference yet, or a large
+    // upward jump) the tile's own maximum becomes the reference and l is
+    // rescaled.  The max is taken on the raw scores (the scale is positive).
+    auto settle = [&](int b, const f32x16_t& acc, float ts) {
+        if (m[b] != kNegInf && ts <= 0x1p64f) {
+            l[b] += ts;
+            return;
+        }
+        float bm = kNegInf;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) bm = fmaxf(bm, acc[v]);
+        const float mn = fmaxf(m[b], bm * scale_log2e);
+        if (mn == kNegInf) return;  // no key of this half seen yet
+        float sum = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -mn));
+        l[b] = (m[b] == kNegInf ? 0.0f : l[b] * __builtin_amdgcn_exp2f(m[b] - mn)) + sum;
+        m[b] = mn;
+    };
+    // 8 MFMAs of S^T for block b of the tile in ak into `nxt`, each followed
+    // by two exponentials of `cur` against block cb's reference, summed in
+    // four partial sums; returns the sum
+    auto step = [&](int b, f32x16_t& nxt, const f32x16_t& cur, int cb) {
+        nxt = f32x16_t{};
+        const float mc = m[cb];
+        float e[16], ps[4];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], nxt, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int v = 2 * ks; v < 2 * ks + 2; ++v) e[v] = __builtin_amdgcn_exp2f(fmaf(cur[v], scale_log2e, -mc));
+            if (ks > 0) {
+#pragma unroll
+                for (int v = 2 * ks - 2; v < 2 * ks; ++v) ps[v & 3] = v < 4 ? e[v] : ps[v & 3] + e[v];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        ps[2] += e[14];
+        ps[3] += e[15];
+        return (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    };
+    for (int64_t kb = 0; kb < kMassStages - 1; ++kb)
+        if (kb < kb_end) issue(kb);
+    // key tiles below both of the wave's query blocks need no mask: there the
+    // blocks are pipelined (one block's MFMAs beside the other's
+    // exponentials); the diagonal tiles go one block after the other; tiles
+    // past the wave's blocks only take part in the ring
+    const int64_t p_end = qb0 < kb_end ? qb0 : kb_end;
+    int64_t kb = 0;
+    if (p_end > 0) {
+        open_tile(0);
+        read_tile(0);
+        f32x16_t accA = s_tile(0), accB;
+        for (; kb + 1 < p_end; ++kb) {
+            const float t0 = step(1, accB, accA, 0);  // block 1 of tile kb beside block 0's exponentials
+            settle(0, accA, t0);
+            open_tile(kb + 1);
+            read_tile(kb + 1);
+            const float t1 = step(0, accA, accB, 1);  // block 0 of tile kb + 1 beside block 1's of tile kb
+            settle(1, accB, t1);
+        }
+        const float t0 = step(1, accB, accA, 0);  // the last unmasked tile
+        settle(0, accA, t0);
+        float t1 = 0.0f;
+        {
+            const float mc = m[1];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) t1 += __builtin_amdgcn_exp2f(fmaf(accB[v], scale_log2e, -mc));
+        }
+        settle(1, accB, t1);
+        ++kb;
+    }
+    for (; kb < kb_end; ++kb) {
+        open_tile(kb);
+        if (kb > qb0 + 1) continue;  // wave-uniform: past both blocks
+        read_tile(kb);
 #pragma unroll
         for (int b = 0; b < kNB; ++b) {
             if (kb > qb0 + b) continue;  // wave-uniform: the block lies above the diagonal
-            f32x16_t acc = {};
-#pragma unroll
-            for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[ks], bq[b][ks], acc, 0, 0, 0);
-            // acc[v] = S^T[key = 32 kb + out_row(v)][query = 32 (qb0 + b) + l32];
-            // only the diagonal block has keys after its queries; the max is
-            // taken on the raw scores (the scale is positive) and the scale
-            // folded into one fma per score
+            f32x16_t acc = s_tile(b);
+            // only the diagonal block has keys after its queries
             if (kb == qb0 + b) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
                     if (out_row(v, half) > l32) acc[v] = kNegInf;
             }
-            // exponentials against the lane's reference m (a maximum seen
-            // earlier, scaled); only while none is set, or when the tile's sum
-            // shows values far above it, the tile's own maximum becomes the
-            // reference and l is rescaled
-            float sum = 0.0f;
-            if (m[b] != kNegInf) {
+            float ts = 0.0f;
+            const float mc = m[b];
 #pragma unroll
-                for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -m[b]));
-            }
-            if (m[b] != kNegInf && sum <= 0x1p64f) {
-                l[b] += sum;
-            } else {
-                float bm = kNegInf;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) bm = fmaxf(bm, acc[v]);
-                const float mn = fmaxf(m[b], bm * scale_log2e);
-                if (mn == kNegInf) continue;  // no key of this half seen yet
-                sum = 0.0f;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) sum += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -mn));
-                l[b] = (m[b] == kNegInf ? 0.0f : l[b] * __builtin_amdgcn_exp2f(m[b] - mn)) + sum;
-                m[b] = mn;
-            }
+            for (int v = 0; v < 16; ++v) ts += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -mc));
+            settle(b, acc, ts);
         }
     }
 #pragma unroll
@@ -200,13 +287,20 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_lse_kernel(const uint16_
     }
 }
 
+// The column pass streams the query tiles together with their rows' normalisers:
+// per tile each wave also loads the 32 normalisers (one per lane, the two lane
+// halves alike) into its own 256-byte slot of the stage, so they arrive
+// through LDS and no wait for a global load sits in the loop.
+constexpr int kColLoads = kMassLoads + 1;  // direct loads per wave per tile
+constexpr int kLseSlots = kMassStages * kMassTile;  // LDS offset of the normaliser slots
+
 __global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_t* __restrict__ q,
                                                                    const uint16_t* __restrict__ k, int64_t T,
                                                                    int64_t row_begin, int32_t Hq, int32_t Hkv,
                                                                    float scale_log2e,
                                                                    const float* __restrict__ lse2,
                                                                    float* __restrict__ part) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[kMassStages * kMassTile];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[kMassStages * kMassTile + kMassStages * kMassWaves * 256];
     const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = blockIdx.y, kvh = h / (Hq / Hkv);
@@ -222,8 +316,9 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) bk[b][ks] = ld8(row + 16 * ks);
     }
-    // per lane and key row v of each block: the sum over the query columns
-    // this lane has held (one per tile); the lanes are summed at the end
+    wait_vmcnt<0>();  // the fixed operands are in before the ring's loads start
+    // per lane and key row v of each block: the sum over the query rows this
+    // lane has held (one per tile); the lanes are summed at the end
     float col[kNB][16];
 #pragma unroll
     for (int b = 0; b < kNB; ++b)
@@ -234,50 +329,101 @@ __global__ __launch_bounds__(64 * kMassWaves) void mass_col_kernel(const uint16_
     const int64_t qb_first = wg0 > row_begin / 32 ? wg0 : row_begin / 32;
     const int64_t qstride = (int64_t)Hq * 128 * 2;
     const uint16_t* qbase = q + (int64_t)h * 128;
+    const uint32_t smem_base = lds_addr(smem);
     MassRing ring;
-    ring.init(qstride, wave, lds_addr(smem));
+    ring.init(qstride, wave, smem_base);
+    auto stage_of = [&](int64_t qb) { return (int)((qb - qb_first) & (kMassStages - 1)); };
     auto issue = [&](int64_t qb) {
-        ring.issue(qbase + qb * 32 * (int64_t)Hq * 128, T - qb * 32, qstride,
-                   (int)((qb - qb_first) & (kMassStages - 1)));
+        const int st = stage_of(qb);
+        ring.issue(qbase + qb * 32 * (int64_t)Hq * 128, T - qb * 32, qstride, st);
+        // the tile's normalisers (rows past T read the last row: replaced below)
+        const int64_t r0 = qb * 32;
+        const int64_t r = r0 + l32 < T ? r0 + l32 : T - 1;
+        g2lds_b32(lse_h + r0, (uint32_t)((r - r0) * 4), smem_base + kLseSlots + (st * kMassWaves + wave) * 256);
+    };
+    // tile qb has landed for every wave (and every wave is done with tile
+    // qb - 1, whose stage then takes tile qb + 3)
+    auto open_tile = [&](int64_t qb) {
+        if (qb + 2 < nb) ring_wait<2, kColLoads>();
+        else if (qb + 1 < nb) ring_wait<1, kColLoads>();
+        else ring_wait<0, kColLoads>();
+        if (qb + kMassStages - 1 < nb) issue(qb + kMassStages - 1);
+    };
+    // this lane's query row of tile qb: its operand fragments and its
+    // normaliser (+inf outside the window or past T: such rows add 0)
+    bf16x8_t aq[8];
+    auto read_tile = [&](int64_t qb) {
+        const int st = stage_of(qb);
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) aq[ks] = ring.frag(st, l32, half, ks);
+        const float x = *(const __attribute__((address_space(3))) float*)(uintptr_t)(
+            smem_base + kLseSlots + (st * kMassWaves + wave) * 256 + 4 * lane);
+        const int64_t r = qb * 32 + l32;
+        return r < T && r >= row_begin ? x : __builtin_inff();
+    };
+    auto s_tile = [&](int b) {
+        f32x16_t acc = {};
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bk[b][ks], aq[ks], acc, 0, 0, 0);
+        return acc;  // acc[v] = S^T[key = 32 (kb0 + b) + out_row(v)][query = 32 qb + l32]
+    };
+    // 8 MFMAs of S^T for block b of the tile in aq into `nxt`, each followed
+    // by two scores of `cur` (fma, exponential, sum) under normaliser L
+    auto step = [&](int b, f32x16_t& nxt, const f32x16_t& cur, float (&cs)[16], float L) {
+        nxt = f32x16_t{};
+        float e[16];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bk[b][ks], aq[ks], nxt, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int v = 2 * ks; v < 2 * ks + 2; ++v) e[v] = __builtin_amdgcn_exp2f(fmaf(cur[v], scale_log2e, -L));
+            if (ks > 0) {
+#pragma unroll
+                for (int v = 2 * ks - 2; v < 2 * ks; ++v) cs[v] += e[v];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        cs[14] += e[14];
+        cs[15] += e[15];
     };
     for (int64_t qb = qb_first; qb < qb_first + kMassStages - 1; ++qb)
         if (qb < nb) issue(qb);
-    // the normaliser of this lane's query row of a tile (+inf outside the
-    // window or past T: such rows add 0)
-    auto load_l = [&](int64_t qb) {
-        const int64_t r = qb * 32 + l32;
-        return r < T && r >= row_begin ? lse_h[r] : __builtin_inff();
-    };
-    float Ln = qb_first < nb ? load_l(qb_first) : 0.0f;
-    for (int64_t qb = qb_first; qb < nb; ++qb) {
-        const float L = Ln;
-        if (qb + 2 < nb) ring_wait<2>();
-        else if (qb + 1 < nb) ring_wait<1>();
-        else ring_wait<0>();
-        if (qb + kMassStages - 1 < nb) issue(qb + kMassStages - 1);
-        if (qb + 1 < nb) Ln = load_l(qb + 1);
-        const int st = (int)((qb - qb_first) & (kMassStages - 1));
-        bf16x8_t aq[8];
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) aq[ks] = ring.frag(st, l32, half, ks);
+    // tiles before the wave's first key block only take part in the ring;
+    // the (at most two) tiles where a block's keys reach past a query row go
+    // one block after the other with the keys after each row masked; from
+    // there on the blocks are pipelined: one block's MFMAs run while the
+    // other block's scores are exponentiated and summed
+    const int64_t start = kb0 > qb_first ? kb0 : qb_first;
+    const int64_t p0 = kb0 + 2 > start ? kb0 + 2 : start;
+    int64_t qb = qb_first;
+    for (; qb < nb && qb < start; ++qb) open_tile(qb);
+    for (; qb < nb && qb < p0; ++qb) {
+        open_tile(qb);
+        const float L = read_tile(qb);
 #pragma unroll
         for (int b = 0; b < kNB; ++b) {
-            if (qb < kb0 + b) continue;  // wave-uniform: every row of the block precedes the keys
-            f32x16_t acc = {};
+            f32x16_t acc = s_tile(b);
+            const int64_t lim = qb * 32 + l32 - (kb0 + b) * 32;  // key row v is kept iff out_row(v) <= lim
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bk[b][ks], aq[ks], acc, 0, 0, 0);
-            // acc[v] = S^T[key = 32 (kb0 + b) + out_row(v)][query = 32 qb + l32];
-            // only the diagonal block has keys after its queries: their
-            // scores become -inf (weight 0) in place, then one common path
-            if (qb == kb0 + b) {
-#pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    if (out_row(v, half) > l32) acc[v] = kNegInf;
-                asm volatile("" : "+v"(acc));
-            }
-#pragma unroll
-            for (int v = 0; v < 16; ++v) col[b][v] += __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -L));
+            for (int v = 0; v < 16; ++v)
+                col[b][v] += out_row(v, half) <= lim ? __builtin_amdgcn_exp2f(fmaf(acc[v], scale_log2e, -L)) : 0.0f;
         }
+    }
+    if (qb < nb) {
+        open_tile(qb);
+        float L = read_tile(qb);
+        f32x16_t accA = s_tile(0), accB;
+        for (; qb + 1 < nb; ++qb) {
+            step(1, accB, accA, col[0], L);  // block 1 of tile qb beside block 0's scores
+            open_tile(qb + 1);
+            const float Ln = read_tile(qb + 1);
+            step(0, accA, accB, col[1], L);  // block 0 of tile qb + 1 beside block 1's scores of tile qb
+            L = Ln;
+        }
+        step(1, accB, accA, col[0], L);  // the last tile
+#pragma unroll
+        for (int v = 0; v < 16; ++v) col[1][v] += __builtin_amdgcn_exp2f(fmaf(accB[v], scale_log2e, -L));
     }
     // sum over the 32 query lanes of each half (a fixed butterfly), then lane
     // v of the half writes key row v
