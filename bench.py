@@ -94,7 +94,7 @@ def parse():
 # scaled by the same counters on a plain copy of known size; valid only for the
 # attention source they were taken on (its SHA-256 below), otherwise null.
 ATTN_TRAFFIC = {"source_sha256": "655f0832f7023c3c55e80f8258eaed498f72414721d2e5fbce93bf4983d10604",
-                "bytes_per_call": 94617507}
+                "bytes_per_call": 94579646}
 
 
 def source_sha256(rel):
@@ -169,7 +169,6 @@ class Path:
         self.n_sel = self.cfg.n_sel(frac)
         n = self.n_sel
         self.sel = torch.empty(n, dtype=torch.int32, device="cuda")
-        self.x_sel = torch.empty((n, self.d), dtype=bf, device="cuda")
         self.q_sel = torch.empty((n, self.hq, self.D), dtype=bf, device="cuda")
         self.out_sel = torch.empty_like(self.q_sel)
         # the attention work plan of the selection, made once per step and shared by layers 1..L-1
@@ -240,13 +239,11 @@ class Path:
                                   out_v=self.asm_v[l:l + 1], except_pos=self.sel)
                 self.gather_done[l].record(self.side)
 
-    def s_xsel(self):
-        self.ss.gather_rows(self.e_tgt, self.sel, out=self.x_sel)
-
     def s_qkv(self, l):
+        # the recomputed tokens' rows are read from the target's embeddings in place
         wq, wk, wv = self.w[l]
-        self.ss.qkv_rope(self.x_sel, self.sel, wq, wk, wv, self.asm_k[l], self.asm_v[l], self.hq, self.hkv,
-                         q_out=self.q_sel, workspace=self.ws, rope_table=self.rope_sel)
+        self.ss.qkv_rope(self.e_tgt, self.sel, wq, wk, wv, self.asm_k[l], self.asm_v[l], self.hq, self.hkv,
+                         q_out=self.q_sel, workspace=self.ws, rope_table=self.rope_sel, x_rows=self.sel)
 
     def s_attn(self, l):
         self.ss.prefill_attention(self.q_sel, self.sel, self.asm_k[l], self.asm_v[l], self.hkv, out=self.out_sel,
@@ -265,7 +262,6 @@ class Path:
             self.s_gather_layers_async()
         else:
             self.s_gather_rest()
-        self.s_xsel()
         main = self.torch.cuda.current_stream()
         for l in range(1, self.L):
             self.s_qkv(l)
@@ -306,7 +302,7 @@ def stage_times(torch, path, reps):
     stream = torch.cuda.current_stream()
     once = [("rope_lsh", path.s_encode), ("match", path.s_match)]
     once += [("gather_rest", path.s_gather_rest)] if path.gather_except else [("gather", path.s_gather)]
-    once += [("qkv0", path.s_qkv0), ("attn0", path.s_attn0), ("select", path.s_select), ("xsel", path.s_xsel)]
+    once += [("qkv0", path.s_qkv0), ("attn0", path.s_attn0), ("select", path.s_select)]
     out = {}
     n_once = max(10, 5 * reps)
     for name, fn in once:

@@ -285,6 +285,24 @@ semshare_status_t semshare_qkv_rope_tabled(const void* rope_table, size_t rope_t
                                            size_t workspace_bytes, semshare_dtype_t dtype, void* stream);
 
 /*
+ * semshare_qkv_rope_tabled with the selected rows read in place: input row i
+ * is row x_rows[i] of x ([n_x][hidden] bf16, 16-byte aligned, under 2 GiB),
+ * so the recomputed tokens' embeddings need not be gathered into a separate
+ * x_sel first (Section 4.2: the recomputed tokens are a subset of the
+ * target's).  Results equal gathering x_sel[i] = x[x_rows[i]] and calling
+ * semshare_qkv_rope_tabled, bit for bit.  x_rows [n_sel] int32 (device);
+ * entries outside [0, n_x) read row 0 or row n_x - 1 (never out of bounds).
+ * dtype FP32: SEMSHARE_E_UNSUPPORTED.
+ */
+semshare_status_t semshare_qkv_rope_tabled_rows(const void* rope_table, size_t rope_table_bytes, const void* x,
+                                                int64_t n_x, const int32_t* x_rows, const int32_t* sel_pos,
+                                                int64_t n_sel, const void* wq, const void* wk, const void* wv,
+                                                void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
+                                                int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void* q_out,
+                                                float* deviation_out, void* workspace, size_t workspace_bytes,
+                                                semshare_dtype_t dtype, void* stream);
+
+/*
  * Step 2 of semshare_partial_prefill on its own (same kernels): causal
  * grouped-query attention of the selected rows over the cache (step 4
  * above), for q as semshare_qkv_rope writes it.  Keys j <= sel_pos[i] of kv

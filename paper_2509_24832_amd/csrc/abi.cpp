@@ -404,7 +404,8 @@ semshare_status_t qkv_rope_impl(const char* fn, const void* rope_table, size_t r
                                 const void* wv, void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, double rope_base,
                                 void* q_out, float* deviation_out, void* workspace, size_t workspace_bytes,
-                                semshare_dtype_t dtype, void* stream, const DevRef* ref = nullptr) {
+                                semshare_dtype_t dtype, void* stream, const DevRef* ref = nullptr,
+                                const int32_t* x_rows = nullptr, int64_t n_x = 0) {
     semshare_status_t st = check_prefill_shapes(fn, n_sel, n_tok, hidden, n_q_heads, n_kv_heads, head_dim, dtype, true);
     if (st != SEMSHARE_OK) return st;
     if (!(rope_base > 0.0) || !std::isfinite(rope_base)) return fail(SEMSHARE_E_INVAL, "%s: rope_base must be finite and > 0", fn);
@@ -418,6 +419,14 @@ semshare_status_t qkv_rope_impl(const char* fn, const void* rope_table, size_t r
     if (st != SEMSHARE_OK) return st;
     semshare::QkvArgs a{x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok, hidden, n_q_heads,
                         n_kv_heads, head_dim, rope_base, q_out, deviation_out, workspace};
+    if (x_rows) {
+        if (dtype != SEMSHARE_BF16) return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 only", fn);
+        if (n_x <= 0) return fail(SEMSHARE_E_INVAL, "%s: n_x must be > 0", fn);
+        if (2 * n_x * hidden >= (int64_t(1) << 31))
+            return fail(SEMSHARE_E_UNSUPPORTED, "%s: bf16 x of 2 GiB or more", fn);
+        a.x_rows = x_rows;
+        a.n_x = n_x;
+    }
     if (rope_table) {
         if (dtype != SEMSHARE_BF16) return fail(SEMSHARE_E_UNSUPPORTED, "%s: the RoPE table is for bf16 only", fn);
         if (!aligned16(rope_table)) return fail(SEMSHARE_E_INVAL, "%s: rope_table must be 16-byte aligned", fn);
@@ -499,6 +508,21 @@ semshare_status_t semshare_qkv_rope_tabled(const void* rope_table, size_t rope_t
     return qkv_rope_impl(fn, rope_table, rope_table_bytes, x_sel, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache,
                          n_tok, hidden, n_q_heads, n_kv_heads, head_dim, 10000.0, q_out, deviation_out, workspace,
                          workspace_bytes, dtype, stream);
+}
+
+semshare_status_t semshare_qkv_rope_tabled_rows(const void* rope_table, size_t rope_table_bytes, const void* x,
+                                                int64_t n_x, const int32_t* x_rows, const int32_t* sel_pos,
+                                                int64_t n_sel, const void* wq, const void* wk, const void* wv,
+                                                void* k_cache, void* v_cache, int64_t n_tok, int32_t hidden,
+                                                int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void* q_out,
+                                                float* deviation_out, void* workspace, size_t workspace_bytes,
+                                                semshare_dtype_t dtype, void* stream) {
+    const char* fn = "qkv_rope_tabled_rows";
+    if (n_x < 0) return fail(SEMSHARE_E_INVAL, "%s: negative n_x", fn);
+    if (n_sel > 0 && (!rope_table || !x_rows)) return fail(SEMSHARE_E_INVAL, "%s: null rope_table or x_rows", fn);
+    return qkv_rope_impl(fn, rope_table, rope_table_bytes, x, sel_pos, n_sel, wq, wk, wv, k_cache, v_cache, n_tok,
+                         hidden, n_q_heads, n_kv_heads, head_dim, 10000.0, q_out, deviation_out, workspace,
+                         workspace_bytes, dtype, stream, nullptr, x_rows, n_x);
 }
 
 namespace {

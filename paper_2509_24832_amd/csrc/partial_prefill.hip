@@ -90,6 +90,8 @@ hipError_t launch_qkv_bf16(const QkvArgs& a, hipStream_t s) {
     const int32_t bn = qkv_gemm_bn(a.n_sel, a.n_q_heads, a.n_kv_heads, a.head_dim);
     GemmArgs g{};
     g.x = static_cast<const uint16_t*>(a.x_sel);
+    g.x_rows = a.x_rows;
+    g.n_x = a.n_x;
     g.pos = a.sel_pos;
     g.w[0] = static_cast<const uint16_t*>(a.wq);
     g.w[1] = static_cast<const uint16_t*>(a.wk);

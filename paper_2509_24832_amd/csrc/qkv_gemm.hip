@@ -98,6 +98,11 @@ __global__ __launch_bounds__(64 * NW, 1) void qkv_gemm_kernel(GemmArgs g) {
         const int row = 8 * (wave * C::kALoads + i) + lrow;
         int64_t grow = m0 + row;
         if (grow > g.n_sel - 1) grow = g.n_sel - 1;  // tail rows: computed, never stored
+        if (g.x_rows) {  // the row of x that input row grow reads, kept inside x
+            int64_t xr = g.x_rows[grow];
+            xr = xr < 0 ? 0 : (xr > g.n_x - 1 ? g.n_x - 1 : xr);
+            grow = xr;
+        }
         a_off[i] = 2u * (uint32_t)(grow * g.hidden + 8 * (lpc ^ ((row >> 1) & 7)));
     }
 #pragma unroll

@@ -195,6 +195,10 @@ struct QkvArgs {
     const void* ref_v = nullptr;
     const int32_t* ref_idx = nullptr;
     int64_t ref_n = 0;
+    // bf16 path: input row i is row x_rows[i] of x_sel ([n_x][hidden],
+    // entries clamped to [0, n_x)); null: row i of x_sel
+    const int32_t* x_rows = nullptr;
+    int64_t n_x = 0;
 };
 
 // Step 2: causal GQA attention of the selected rows over the cache.
@@ -228,7 +232,9 @@ int32_t qkv_dev_parts(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads, int3
 
 // The bf16 projection GEMM (qkv_gemm.hip).
 struct GemmArgs {
-    const uint16_t* x;     // [n_sel][hidden]
+    const uint16_t* x;     // [n_sel][hidden], or [n_x][hidden] read through x_rows
+    const int32_t* x_rows; // [n_sel] rows of x (clamped to [0, n_x)), or null: row i
+    int64_t n_x;
     const int32_t* pos;    // [n_sel]
     const uint16_t* w[3];  // Wq, Wk, Wv (rows = output features)
     int32_t seg_tiles[3];  // BN-wide column tiles per segment (0 for q in K/V-only mode)

@@ -102,7 +102,6 @@ class DynamicSchedule:
         self.counts = torch.empty(3, **i32)
         self.sel = [torch.empty(T, **i32) for _ in range(2)]     # S_l, alternating
         self.sig = [torch.empty(T, **f32) for _ in range(2)]     # sigma_l, alternating
-        self.x_sel = torch.empty((T, dim), dtype=bf, device=dev)
         self.q_sel = torch.empty((T, n_q_heads, head_dim), dtype=bf, device=dev)
         ws = max(ss.qkv_rope_workspace_bytes(T, n_q_heads, n_kv_heads, head_dim, bf),
                  ss.prefill_attention_workspace_bytes(T, T, n_q_heads, n_kv_heads, head_dim, bf))
@@ -173,12 +172,12 @@ class DynamicSchedule:
             nk = min(T, n_ret + n_l)
             kc, vc = self.asm_k[l][:nk], self.asm_v[l][:nk]
             ss.gather_kv(ref_k[l][None], ref_v[l][None], src[:nk], out_k=kc[None], out_v=vc[None])
-            x = ss.gather_rows(e_tgt, s_l, out=self.x_sel[:n_l])
             table = ss.rope_table(s_l, T, D, out=self.table_buf)
             wq, wk, wv = weights[l]
-            q, sig = ss.qkv_rope(x, rows, wq, wk, wv, kc, vc, hq, hkv, q_out=self.q_sel[:n_l],
+            # the recomputed tokens' embeddings are read in place (rows s_l of e_tgt)
+            q, sig = ss.qkv_rope(e_tgt, rows, wq, wk, wv, kc, vc, hq, hkv, q_out=self.q_sel[:n_l],
                                  deviation=self.sig[l % 2][:n_l], want_deviation=True, workspace=self.ws,
-                                 rope_table=table)
+                                 rope_table=table, x_rows=s_l)
             plan = ss.attention_plan(rows, nk, hq, hkv, D, out=self.plan_buf)
             out = ss.prefill_attention(q, rows, kc, vc, hkv, workspace=self.ws, plan=plan)
             m("layer")

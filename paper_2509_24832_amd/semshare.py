@@ -82,6 +82,8 @@ def load() -> ctypes.CDLL:
         "semshare_rope_table": (I32, [P, I64, I64, I32, F64, P, SZ, P]),
         "semshare_qkv_rope_tabled": (I32, [P, SZ, P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, P, P, P, SZ,
                                            I32, P]),
+        "semshare_qkv_rope_tabled_rows": (I32, [P, SZ, P, I64, P, P, I64, P, P, P, P, P, I64, I32, I32, I32, I32, P,
+                                                P, P, SZ, I32, P]),
         "semshare_attention_plan_bytes": (SZ, [I64, I64, I32, I32, I32, I32]),
         "semshare_attention_plan": (I32, [P, I64, I64, I32, I32, I32, I32, P, SZ, P]),
         "semshare_prefill_attention_planned": (I32, [P, SZ, P, P, I64, P, P, I64, I32, I32, I32, F32, P, P, SZ,
@@ -405,9 +407,12 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
              wv: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, n_q_heads: int, n_kv_heads: int,
              rope_base: float = 10000.0, q_out: Optional[torch.Tensor] = None, want_q: bool = True,
              deviation: Optional[torch.Tensor] = None, want_deviation: bool = False,
-             workspace: Optional[torch.Tensor] = None, rope_table: Optional[torch.Tensor] = None):
+             workspace: Optional[torch.Tensor] = None, rope_table: Optional[torch.Tensor] = None,
+             x_rows: Optional[torch.Tensor] = None):
     """Projection + RoPE + deviation + cache scatter of the selected rows (with `rope_table` from
-    rope_table(), bf16: its factors instead of rope_base).
+    rope_table(), bf16: its factors instead of rope_base).  With x_rows (int32 [n_sel], bf16 with a
+    rope_table only): input row i is row x_rows[i] of x_sel, which then holds every row [n_x, hidden]
+    (no gathered copy; the same results as gather_rows then qkv_rope).
     Returns (q [n_sel, Hq, D] or None, deviation [n_sel] or None)."""
     _dev(x_sel, "x_sel")
     dt = x_sel.dtype
@@ -415,6 +420,13 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
     for name, t in (("wk", wk), ("wv", wv), ("k_cache", k_cache), ("v_cache", v_cache)):
         _dev(t, name, dt)
     n_sel, hidden = x_sel.shape
+    if x_rows is not None:
+        _dev(x_rows, "x_rows", torch.int32)
+        if rope_table is None:
+            raise ValueError("x_rows needs a rope_table")
+        n_sel = x_rows.numel()
+        if sel_pos.numel() < n_sel:
+            raise ValueError("sel_pos shorter than x_rows")
     n_tok, head_dim = k_cache.shape[0], k_cache.shape[-1]
     if k_cache.numel() != n_tok * n_kv_heads * head_dim or v_cache.shape != k_cache.shape:
         raise ValueError("caches must be [n_tok, n_kv_heads, head_dim]")
@@ -430,6 +442,13 @@ def qkv_rope(x_sel: torch.Tensor, sel_pos: torch.Tensor, wq: Optional[torch.Tens
     if not want_deviation:
         deviation = None
     ws = _workspace(qkv_rope_workspace_bytes(n_sel, n_q_heads, n_kv_heads, head_dim, dt), workspace, x_sel)
+    if x_rows is not None:
+        _dev(rope_table, "rope_table", torch.uint8)
+        _call("semshare_qkv_rope_tabled_rows", _ptr(rope_table), rope_table.numel(), _ptr(x_sel), x_sel.shape[0],
+              _ptr(x_rows), _ptr(sel_pos), n_sel, _ptr(wq) if want_q else None, _ptr(wk), _ptr(wv), _ptr(k_cache),
+              _ptr(v_cache), n_tok, hidden, n_q_heads, n_kv_heads, head_dim, _ptr(q_out), _ptr(deviation),
+              _ptr(ws), 0 if ws is None else ws.numel(), _dt(x_sel), _stream())
+        return q_out, deviation
     if rope_table is not None:
         _dev(rope_table, "rope_table", torch.uint8)
         _call("semshare_qkv_rope_tabled", _ptr(rope_table), rope_table.numel(), _ptr(x_sel), _ptr(sel_pos), n_sel,

@@ -278,6 +278,17 @@ def test_rope_table_validation(lib):
     assert L.semshare_qkv_rope_tabled(FAKE, 1 << 20, *rest, 0, None) == b.E_UNSUPPORTED  # fp32 projection
     bad_n = (FAKE, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 256, 8, 2, 128, FAKE, None, FAKE, 1 << 30)
     assert L.semshare_qkv_rope_tabled(FAKE, 1 << 20, *bad_n, 1, None) == b.E_INVAL  # n_sel > n_tok
+    # the same with the rows read in place through x_rows: the row index and n_x, then the shared checks
+    rows = L.semshare_qkv_rope_tabled_rows
+    tail = (FAKE, FAKE, FAKE, FAKE, FAKE, 16, 256, 8, 2, 128, FAKE, None, FAKE, 1 << 30)
+    assert rows(FAKE, 1 << 20, FAKE, 100, None, FAKE, 8, *tail, 1, None) == b.E_INVAL  # no x_rows
+    assert rows(None, 0, FAKE, 100, FAKE, FAKE, 8, *tail, 1, None) == b.E_INVAL  # no table
+    assert rows(FAKE, 1 << 20, FAKE, 0, FAKE, FAKE, 8, *tail, 1, None) == b.E_INVAL  # n_x = 0
+    assert rows(FAKE, 1 << 20, FAKE, -1, FAKE, FAKE, 8, *tail, 1, None) == b.E_INVAL
+    assert rows(FAKE, 1 << 20, FAKE, 1 << 22, FAKE, FAKE, 8, *tail, 1, None) == b.E_UNSUPPORTED  # x of 2 GiB
+    assert rows(FAKE, 1 << 20, FAKE, 100, FAKE, FAKE, 8, *tail, 0, None) == b.E_UNSUPPORTED  # fp32
+    assert rows(FAKE, 1 << 20, FAKE_ODD, 100, FAKE, FAKE, 8, *tail, 1, None) == b.E_INVAL  # x alignment
+    assert rows(None, 0, None, 0, None, None, 0, *tail, 1, None) == b.OK  # nothing to do
 
 
 def test_bank_similarity_validation(lib):

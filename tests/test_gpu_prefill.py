@@ -252,6 +252,37 @@ def test_shared_rope_table_equals_own(n_tok, hidden, hq, hkv, d, n_sel):
         q2, dev2 = ss.qkv_rope(xs, ps, wq, wk, wv, k2, v2, hq, hkv, want_deviation=True, rope_table=table)
         for a, b in ((q1, q2), (dev1, dev2), (k1, k2), (v1, v2)):
             assert torch.equal(a, b)
+        # the same rows read in place from every row of x (no gathered copy)
+        k3, v3 = dev(k, dt), dev(v, dt)
+        q3, dev3 = ss.qkv_rope(dev(x_all, dt), ps, wq, wk, wv, k3, v3, hq, hkv, want_deviation=True,
+                               rope_table=table, x_rows=ps)
+        for a, b in ((q1, q3), (dev1, dev3), (k1, k3), (v1, v3)):
+            assert torch.equal(a, b)
+
+
+def test_projection_rows_read_in_place_clamped():
+    """semshare_qkv_rope_tabled_rows with input rows in any order, repeated,
+    and outside [0, n_x) (read as row 0 or row n_x - 1): equal, bit for bit,
+    to gathering those rows first (700 x rows, 300 selected, hidden 512,
+    16 q / 4 kv heads, head_dim 128)."""
+    cfg = CONFIGS[1]
+    n_tok, hidden, hq, hkv, d, n_sel = 700, 512, 16, 4, 128, 300
+    announce("projection with rows read in place, clamped row indices")
+    dt = cfg.dtype
+    x_all, w, k, v, sel = _case(cfg, n_tok, hidden, hq, hkv, d, n_sel, tag=70)
+    r = np.random.default_rng(70)
+    rows = r.integers(-50, n_tok + 50, n_sel).astype(np.int32)
+    rows[:3] = [-1, n_tok, n_tok + 7]
+    ps, pr = dev_i32(sel), dev_i32(rows)
+    table = ss.rope_table(ps, n_tok, d)
+    wq, wk, wv = dev(w.wq, dt), dev(w.wk, dt), dev(w.wv, dt)
+    k1, v1, k2, v2 = dev(k, dt), dev(v, dt), dev(k, dt), dev(v, dt)
+    xs = dev(x_all[np.clip(rows, 0, n_tok - 1)], dt)
+    q1, dev1 = ss.qkv_rope(xs, ps, wq, wk, wv, k1, v1, hq, hkv, want_deviation=True, rope_table=table)
+    q2, dev2 = ss.qkv_rope(dev(x_all, dt), ps, wq, wk, wv, k2, v2, hq, hkv, want_deviation=True, rope_table=table,
+                           x_rows=pr)
+    for a, b in ((q1, q2), (dev1, dev2), (k1, k2), (v1, v2)):
+        assert torch.equal(a, b)
 
 
 def test_attention_plan_over_1024_row_tiles():
